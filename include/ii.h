@@ -1,0 +1,250 @@
+/*
+ * ii.h -- merged tensor loading on AMD Instinct MI355X (gfx950).
+ *
+ * C-ABI of libii.so. The library implements the refined tensor
+ * materialisation of InstantInfer (arXiv 2607.18957, Sec. 4.2): instead of
+ * one small host-to-device copy per tensor, the bytes of a weight blob are cut
+ * into a few large equal chunks, each chunk is streamed host -> HBM in bulk
+ * through a pinned staging ring, and a device kernel scatters the chunk into
+ * every tensor it holds while the next chunk is still in flight.
+ *
+ * Conventions for every entry point:
+ *   - Return value: II_OK (0) or one of the II_E* codes below. On error a
+ *     thread-local description is available from ii_last_error().
+ *   - Pointers are plain host or device addresses; sizes are bytes.
+ *   - Nothing here allocates on behalf of the caller except ii_host_alloc and
+ *     the plan's own staging buffers (see ii_load).
+ *   - A plan is not thread-safe: two calls that use the same plan at the same
+ *     time from different host threads get II_EBUSY for the later one.
+ */
+#ifndef II_H
+#define II_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------ */
+enum {
+    II_OK = 0,
+    II_EINVAL = 1,    /* NULL argument, bad chunk size, bad dtype/shape/alignment */
+    II_EOVERFLOW = 2, /* a byte size or offset does not fit in 64 bits */
+    II_EOVERLAP = 3,  /* source ranges overlap, or destination ranges overlap */
+    II_EALIGN = 4,    /* a destination pointer is not aligned to its dst_align */
+    II_ENOMEM = 5,    /* host or device allocation failed */
+    II_EARENA = 6,    /* the arena is smaller than the new plan's arena_bytes */
+    II_EBUSY = 7,     /* the plan is in use by another call */
+    II_EHIP = 8,      /* any other HIP runtime error (detail in ii_last_error) */
+    II_ERANGE = 9     /* the blob or image is shorter than the plan's span end */
+};
+
+/* ---- element types (storage width in brackets) ---------------------------- */
+enum {
+    II_U8 = 1,       /* [1] */
+    II_I8 = 2,       /* [1] */
+    II_FP8_E4M3 = 3, /* [1] */
+    II_FP8_E5M2 = 4, /* [1] */
+    II_BF16 = 5,     /* [2] */
+    II_F16 = 6,      /* [2] */
+    II_F32 = 7,      /* [4] */
+    II_I32 = 8,      /* [4] */
+    II_F64 = 9,      /* [8] */
+    II_I64 = 10      /* [8] */
+};
+
+/*
+ * One row of the tensor table: a tensor's logical description and where its
+ * bytes sit in the blob (the model file image in host memory; in the paper,
+ * the checkpoint read from storage or tmpfs, Sec. 5).
+ *   name        optional, may be NULL; copied by ii_plan.
+ *   dtype       one of the II_* element types above.
+ *   ndim        number of dimensions (0 = scalar).
+ *   shape       ndim non-negative extents; copied by ii_plan. nbytes =
+ *               product(shape) x width(dtype). Zero-size tensors are allowed.
+ *   src_offset  byte offset of the tensor's first byte in the blob.
+ *   dst_align   required alignment (power of two) of the tensor's
+ *               destination address.
+ */
+typedef struct ii_tensor_desc {
+    const char* name;
+    int32_t dtype;
+    int32_t ndim;
+    const int64_t* shape;
+    uint64_t src_offset;
+    uint64_t dst_align;
+} ii_tensor_desc;
+
+typedef struct ii_plan_s ii_plan_t; /* opaque */
+
+/*
+ * ii_plan -- precompute the chunk <-> tensor association (Sec. 4.2, "Refined
+ * CFA Model": the file is divided into equal-length chunks, the last one
+ * possibly partial, and the tensor.chunks / chunk.tensors maps are computed in
+ * advance).
+ *
+ * Chunks are windows of chunk_bytes over the span [lo, hi) of the table's
+ * source bytes (lo = smallest source offset, hi = largest source end over
+ * non-empty tensors); chunk k covers [lo + k*chunk_bytes, min(lo +
+ * (k+1)*chunk_bytes, hi)). A segment is one tensor's piece of one chunk.
+ * Destination layout (used by ii_switch and by callers carving an arena): in
+ * table order, tensor i starts at the smallest multiple of dst_align[i] at or
+ * after the end of tensor i-1; arena_bytes is the end rounded up to the
+ * largest alignment.
+ *
+ *   table        n rows; read only during the call (names and shapes copied).
+ *   n            number of rows; 0 is valid (a plan with no chunks).
+ *   chunk_bytes  chunk size: a multiple of 16, 16 <= chunk_bytes < 2^32.
+ *   out          receives the plan; release with ii_plan_free.
+ * Host only: touches no device. Errors: II_EINVAL (NULL out, NULL table with
+ * n > 0, bad chunk_bytes, unknown dtype, negative ndim or extent, dst_align
+ * not a power of two), II_EOVERFLOW, II_EOVERLAP (two non-empty source
+ * ranges share a byte), II_ENOMEM.
+ */
+int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_bytes, ii_plan_t** out);
+
+/* Release a plan and everything it owns (staging rings, device tables).
+ * Waits for the plan's outstanding device work first. NULL is a no-op. */
+void ii_plan_free(ii_plan_t* plan);
+
+/*
+ * ii_load -- materialise every tensor of the plan from a host blob into
+ * device memory (Sec. 4.2). For each chunk in order: stage it into a pinned
+ * host slot (skipped when the blob itself is pinned), copy it to a device
+ * slot with one hipMemcpyAsync, then scatter it into its tensors with the
+ * device kernel. Chunk k+1's copy overlaps chunk k's scatter; a slot is
+ * reused only after the scatter that read it has finished (Sec. 4.2:
+ * (C_i,InMem)->(C_i+1,InDisk), (C_i,InGPU)->(C_i+1,InMem),
+ * (C_i,InGPU)->(T_j,Alloc), (T_j,Loaded)->(C_i,InGPU)).
+ *
+ *   plan        from ii_plan. On first use it allocates, on the current
+ *               device, a ring of `depth` pinned host slots and `depth`
+ *               device slots of chunk_bytes each (default depth 3, see
+ *               ii_plan_set_ring) plus the plan's device tables; they are
+ *               kept for later loads until ii_plan_release / ii_plan_free.
+ *   host_blob   host address of blob byte 0. Pageable or pinned. Pageable
+ *               blobs are read only during the call; a pinned blob
+ *               (hipHostMalloc / ii_host_alloc) is read by DMA after the call
+ *               returns and must stay valid and unchanged until `stream`
+ *               reaches the point after this call.
+ *   blob_bytes  size of the blob; must be >= the plan's span end hi.
+ *   dst_ptrs    n device addresses, one per table row (NULL allowed only for
+ *               zero-size tensors); dst_ptrs[i] must be a multiple of
+ *               dst_align[i]; the ranges [dst_ptrs[i], +nbytes[i]) must not
+ *               overlap. Read during the call only; the memory they point to
+ *               must stay allocated until `stream` passes this call.
+ *   stream      HIP stream (0 = null stream). Writes into the destinations
+ *               start only after all work already enqueued on `stream`, and
+ *               complete before any work enqueued on `stream` afterwards.
+ * Only the tensors' bytes are written: destination padding and every other
+ * byte are left untouched. Returns once all work is enqueued (for a
+ * pageable blob also after its bytes have been staged). Errors: II_EINVAL,
+ * II_EALIGN, II_EOVERLAP, II_ERANGE, II_ENOMEM, II_EBUSY, II_EHIP. After an
+ * error nothing remains enqueued that writes caller memory and the plan stays
+ * usable.
+ */
+int ii_load(ii_plan_t* plan, const void* host_blob, uint64_t blob_bytes, void* const* dst_ptrs,
+            hipStream_t stream);
+
+/*
+ * ii_load_device -- the same materialisation from a blob image that is
+ * already resident in device memory (for example a checkpoint image parked in
+ * HBM): no staging and no host-to-device copy, every chunk is scattered
+ * straight from the image by the same kernel, in one launch on `stream`.
+ *
+ *   dev_image    device address of blob byte 0 (any alignment).
+ *   image_bytes  size of the image; must be >= the plan's span end hi.
+ *   dst_ptrs     as for ii_load; must not overlap [dev_image, +hi).
+ *   stream       the kernel runs on this stream, after the work already on
+ *                it. The caller keeps the image and destinations alive
+ *                until the stream passes this call.
+ * Errors: as ii_load.
+ */
+int ii_load_device(ii_plan_t* plan, const void* dev_image, uint64_t image_bytes,
+                   void* const* dst_ptrs, hipStream_t stream);
+
+/*
+ * ii_switch -- reuse a device arena that holds plan_old's tensors (at
+ * plan_old's layout offsets) for plan_new's tensors (at plan_new's offsets),
+ * following the model-switch dependency (Sec. 4.3): the new model's
+ * preparation that does not need the arena (staging and host-to-device
+ * copies into the ring) starts at once, while the first write into the arena
+ * waits for all work enqueued on `stream` before this call, i.e. for the old
+ * model to have finished with its memory, (M1,GMemFreed)->(M2,EnvReady).
+ * Afterwards every byte of a new tensor holds the new blob's bytes, every
+ * byte that belonged to an old tensor and to no new tensor is zero, and all
+ * other arena bytes are untouched.
+ *
+ *   plan_old     layout of what the arena holds now (only its layout is used).
+ *   plan_new     the table to load; its ring and tables are used as in ii_load.
+ *   arena        device address, aligned to plan_new's largest dst_align.
+ *   arena_bytes  must be >= both plans' arena_bytes, else II_EARENA.
+ *   host_blob_new, blob_bytes, stream   as for ii_load.
+ * Errors: as ii_load, plus II_EARENA.
+ */
+int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint64_t arena_bytes,
+              const void* host_blob_new, uint64_t blob_bytes, hipStream_t stream);
+
+/*
+ * Ring configuration, before the plan's first load or after
+ * ii_plan_release. depth = number of chunk slots in flight (1..8; default 3
+ * or $II_RING_DEPTH); host_threads = threads copying a pageable blob into
+ * the pinned slots (1..64; default min(8, cores) or $II_HOST_THREADS).
+ * Errors: II_EINVAL (out of range), II_EBUSY (ring already allocated).
+ */
+int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads);
+
+/* Free the plan's staging ring and device tables after waiting for its
+ * outstanding work (the paper frees its I/O buffers as soon as loading
+ * completes, Sec. 6.6). The plan stays valid; the next load reallocates. */
+int ii_plan_release(ii_plan_t* plan);
+
+/* ---- plan inspection (host only) ----------------------------------------- */
+size_t ii_plan_num_tensors(const ii_plan_t* plan);
+size_t ii_plan_num_chunks(const ii_plan_t* plan);
+size_t ii_plan_num_segments(const ii_plan_t* plan);
+uint64_t ii_plan_chunk_bytes(const ii_plan_t* plan);
+uint64_t ii_plan_payload_bytes(const ii_plan_t* plan); /* sum of nbytes */
+uint64_t ii_plan_arena_bytes(const ii_plan_t* plan);
+/* span [lo, hi) of source bytes; both 0 when every tensor is empty */
+void ii_plan_span(const ii_plan_t* plan, uint64_t* lo, uint64_t* hi);
+/* per tensor (arrays of num_tensors; NULL skips a field) */
+int ii_plan_tensors(const ii_plan_t* plan, uint64_t* nbytes, uint64_t* dst_offset);
+/* per chunk (arrays of num_chunks; seg_begin has num_chunks + 1 entries: the
+ * segments of chunk k are [seg_begin[k], seg_begin[k+1])) */
+int ii_plan_chunks(const ii_plan_t* plan, uint64_t* src_begin, uint64_t* len,
+                   uint64_t* seg_begin);
+/* per segment, ordered by chunk then by offset in the chunk (arrays of
+ * num_segments) */
+int ii_plan_segments(const ii_plan_t* plan, uint32_t* chunk, uint32_t* chunk_off,
+                     uint32_t* tensor, uint64_t* tensor_off, uint32_t* len);
+/* the kernel's work split: each chunk is cut into tiles_per_chunk windows of
+ * tile_bytes; tile g = k * tiles_per_chunk + t of chunk k covers chunk bytes
+ * [t * tile_bytes, min((t+1) * tile_bytes, len_k)) and meets exactly the
+ * segments [first[g], last[g]). Arrays of num_chunks * tiles_per_chunk
+ * entries; pass NULL arrays to read only the two sizes. */
+int ii_plan_tiles(const ii_plan_t* plan, uint32_t* tile_bytes, uint32_t* tiles_per_chunk,
+                  uint32_t* first, uint32_t* last);
+/* name of row i as given to ii_plan ("" if none); valid while the plan lives */
+const char* ii_plan_tensor_name(const ii_plan_t* plan, size_t i);
+
+/* ---- pinned host memory for blobs ---------------------------------------- */
+/* Page-locked, device-accessible host allocation (hipHostMalloc) of exactly
+ * `bytes`; a blob placed here is copied by DMA without staging. */
+int ii_host_alloc(uint64_t bytes, void** out);
+int ii_host_free(void* ptr);
+
+/* ---- errors ------------------------------------------------------------- */
+const char* ii_strerror(int status);
+/* Detail of the last error raised on the calling thread ("" if none). */
+const char* ii_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* II_H */

@@ -1,0 +1,86 @@
+// Internal declarations shared by the planner, the runtime and the kernels.
+#pragma once
+
+#include <atomic>
+#include <cstdint>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "ii.h"
+
+namespace ii {
+
+// One segment as the scatter kernel reads it: a piece of one tensor inside
+// one chunk. 16 bytes so a wave loads its rows with dwordx4 loads.
+struct SegDev {
+    uint32_t off;  // offset of the piece inside its chunk
+    uint32_t len;  // bytes
+    uint64_t dst;  // device address the piece's first byte goes to
+};
+static_assert(sizeof(SegDev) == 16, "SegDev must stay 16 bytes");
+
+// Work split of a chunk: a tile is a window of tile_bytes of the chunk; its
+// segments are [first, last) (every segment whose bytes meet the window).
+struct TileDev {
+    uint32_t first;
+    uint32_t last;
+};
+static_assert(sizeof(TileDev) == 8, "TileDev must stay 8 bytes");
+
+// Zero-fill range for the switch scrub: [begin, end) as device addresses.
+struct RangeDev {
+    uint64_t begin;
+    uint64_t end;
+};
+
+constexpr uint32_t kBlock = 256;              // threads per scatter workgroup
+constexpr uint32_t kDefaultTile = 16u << 10;  // bytes of chunk per workgroup
+constexpr uint32_t kMaxSegBatch = kBlock;     // segment rows staged in LDS at once
+
+struct Runtime;  // device-side state (runtime.hip)
+
+void set_error(const char* fmt, ...);
+int fail(int code, const char* fmt, ...);
+
+}  // namespace ii
+
+struct ii_plan_s {
+    // table as given
+    std::vector<std::string> names;
+    std::vector<int32_t> dtype;
+    std::vector<int32_t> ndim;
+    std::vector<int64_t> shape_flat;
+    std::vector<uint64_t> shape_start;
+    std::vector<uint64_t> src_offset;
+    std::vector<uint64_t> dst_align;
+    // derived
+    std::vector<uint64_t> nbytes;
+    std::vector<uint64_t> dst_offset;
+    uint64_t payload = 0, arena_bytes = 0, max_align = 1;
+    uint64_t lo = 0, hi = 0;
+    uint64_t chunk_bytes = 0;
+    size_t num_chunks = 0;
+    std::vector<uint64_t> chunk_seg_begin;  // num_chunks + 1
+    // segments in chunk order, then by offset inside the chunk
+    std::vector<uint32_t> seg_chunk, seg_off, seg_tensor, seg_len;
+    std::vector<uint64_t> seg_toff;
+    // tiles
+    uint32_t tile_bytes = ii::kDefaultTile;
+    uint32_t tiles_per_chunk = 0;
+    std::vector<ii::TileDev> tiles;  // num_chunks * tiles_per_chunk
+    // runtime configuration
+    uint32_t ring_depth = 3;
+    uint32_t host_threads = 8;
+    // device state, created by the first load
+    ii::Runtime* rt = nullptr;
+    std::atomic<int> busy{0};
+
+    uint64_t chunk_len(size_t k) const {
+        return k + 1 < num_chunks ? chunk_bytes : (hi - lo) - chunk_bytes * (num_chunks - 1);
+    }
+};
+
+namespace ii {
+void runtime_destroy(ii_plan_t* p);
+}

@@ -1,0 +1,338 @@
+// Merge planner: tensor table -> chunks, segments, destination layout, tiles.
+//
+// Sec. 4.2 ("Refined CFA Model") of InstantInfer (arXiv 2607.18957) divides
+// the model file into equal-length chunks, the last possibly partial, and
+// precomputes which tensors each chunk holds and which chunks each tensor
+// spans. This file computes that association once, on the host, so that the
+// load path only walks precomputed tables.
+//
+// Method: sort the non-empty tensors by source offset (which also finds
+// overlaps), then sweep them in source order and cut each tensor's range at
+// chunk boundaries. Because source ranges are disjoint, the pieces come out
+// already ordered by chunk and by offset inside the chunk: O(N log N + S).
+// The per-tile segment windows used by the kernel come from one more linear
+// sweep per chunk.
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <unistd.h>
+
+#include "ii_internal.h"
+
+namespace ii {
+
+static thread_local std::string g_last_error;
+
+void set_error(const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+}
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+static int width_of(int32_t dtype) {
+    switch (dtype) {
+    case II_U8: case II_I8: case II_FP8_E4M3: case II_FP8_E5M2: return 1;
+    case II_BF16: case II_F16: return 2;
+    case II_F32: case II_I32: return 4;
+    case II_F64: case II_I64: return 8;
+    default: return 0;
+    }
+}
+
+static bool pow2(uint64_t x) { return x && !(x & (x - 1)); }
+
+static uint32_t env_u32(const char* name, uint32_t dflt, uint32_t lo, uint32_t hi) {
+    const char* s = getenv(name);
+    if (!s || !*s) return dflt;
+    char* end = nullptr;
+    unsigned long v = strtoul(s, &end, 10);
+    if (end == s || v < lo || v > hi) return dflt;
+    return (uint32_t)v;
+}
+
+}  // namespace ii
+
+using namespace ii;
+
+extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_bytes,
+                       ii_plan_t** out) {
+    if (!out) return fail(II_EINVAL, "ii_plan: out is NULL");
+    *out = nullptr;
+    if (n && !table) return fail(II_EINVAL, "ii_plan: table is NULL");
+    if (chunk_bytes < 16 || chunk_bytes % 16 || chunk_bytes >= (1ull << 32))
+        return fail(II_EINVAL, "ii_plan: chunk_bytes %llu must be a multiple of 16 in [16, 2^32)",
+                    (unsigned long long)chunk_bytes);
+    if (n >= (1ull << 32) - 1) return fail(II_EINVAL, "ii_plan: too many tensors");
+
+    std::unique_ptr<ii_plan_t> p;
+    try {
+        p.reset(new ii_plan_t());
+        p->names.resize(n);
+        p->dtype.resize(n);
+        p->ndim.resize(n);
+        p->shape_start.resize(n);
+        p->src_offset.resize(n);
+        p->dst_align.resize(n);
+        p->nbytes.resize(n);
+        p->dst_offset.resize(n);
+    } catch (const std::bad_alloc&) {
+        return fail(II_ENOMEM, "ii_plan: host allocation failed");
+    }
+    p->chunk_bytes = chunk_bytes;
+
+    // 1. copy the table and compute byte sizes
+    for (size_t i = 0; i < n; ++i) {
+        const ii_tensor_desc& d = table[i];
+        int w = width_of(d.dtype);
+        if (!w) return fail(II_EINVAL, "ii_plan: row %zu: unknown dtype %d", i, d.dtype);
+        if (d.ndim < 0 || (d.ndim > 0 && !d.shape))
+            return fail(II_EINVAL, "ii_plan: row %zu: bad ndim/shape", i);
+        if (!pow2(d.dst_align))
+            return fail(II_EINVAL, "ii_plan: row %zu: dst_align %llu is not a power of two", i,
+                        (unsigned long long)d.dst_align);
+        uint64_t numel = 1;
+        bool zero = false;
+        p->shape_start[i] = p->shape_flat.size();
+        for (int32_t k = 0; k < d.ndim; ++k) {
+            if (d.shape[k] < 0) return fail(II_EINVAL, "ii_plan: row %zu: negative extent", i);
+            p->shape_flat.push_back(d.shape[k]);
+            uint64_t x = (uint64_t)d.shape[k];
+            if (x == 0) zero = true;
+        }
+        if (zero) {
+            numel = 0;
+        } else {
+            for (int32_t k = 0; k < d.ndim; ++k) {
+                uint64_t x = (uint64_t)d.shape[k];
+                if (__builtin_mul_overflow(numel, x, &numel))
+                    return fail(II_EOVERFLOW, "ii_plan: row %zu: element count overflows", i);
+            }
+        }
+        uint64_t nb;
+        if (__builtin_mul_overflow(numel, (uint64_t)w, &nb))
+            return fail(II_EOVERFLOW, "ii_plan: row %zu: byte size overflows", i);
+        uint64_t end;
+        if (__builtin_add_overflow(d.src_offset, nb, &end))
+            return fail(II_EOVERFLOW, "ii_plan: row %zu: source end overflows", i);
+        p->names[i] = d.name ? d.name : "";
+        p->dtype[i] = d.dtype;
+        p->ndim[i] = d.ndim;
+        p->src_offset[i] = d.src_offset;
+        p->dst_align[i] = d.dst_align;
+        p->nbytes[i] = nb;
+        p->payload += nb;  // cannot overflow: disjoint ranges below 2^64
+    }
+
+    // 2. destination layout in table order
+    {
+        uint64_t end = 0, maxal = 1;
+        for (size_t i = 0; i < n; ++i) {
+            uint64_t a = p->dst_align[i], off;
+            if (__builtin_add_overflow(end, a - 1, &off))
+                return fail(II_EOVERFLOW, "ii_plan: destination layout overflows");
+            off &= ~(a - 1);
+            if (__builtin_add_overflow(off, p->nbytes[i], &end))
+                return fail(II_EOVERFLOW, "ii_plan: destination layout overflows");
+            p->dst_offset[i] = off;
+            maxal = std::max(maxal, a);
+        }
+        uint64_t ar;
+        if (__builtin_add_overflow(end, maxal - 1, &ar))
+            return fail(II_EOVERFLOW, "ii_plan: arena size overflows");
+        p->arena_bytes = ar & ~(maxal - 1);
+        p->max_align = maxal;
+    }
+
+    // 3. source order, overlap check, span
+    std::vector<uint32_t> order;
+    order.reserve(n);
+    for (size_t i = 0; i < n; ++i)
+        if (p->nbytes[i]) order.push_back((uint32_t)i);
+    std::sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) {
+        return p->src_offset[a] < p->src_offset[b];
+    });
+    for (size_t j = 1; j < order.size(); ++j) {
+        uint32_t a = order[j - 1], b = order[j];
+        if (p->src_offset[b] < p->src_offset[a] + p->nbytes[a])
+            return fail(II_EOVERLAP, "ii_plan: source ranges of rows %u and %u overlap", a, b);
+    }
+    if (!order.empty()) {
+        p->lo = p->src_offset[order.front()];
+        uint32_t l = order.back();
+        p->hi = p->src_offset[l] + p->nbytes[l];
+    }
+    const uint64_t C = chunk_bytes, lo = p->lo, span = p->hi - p->lo;
+    p->num_chunks = span ? (size_t)((span - 1) / C + 1) : 0;
+    if (p->num_chunks >= (1ull << 32))
+        return fail(II_EINVAL, "ii_plan: more than 2^32 chunks");
+
+    // 4. cut every tensor at chunk boundaries, in source order
+    try {
+        size_t S = 0;
+        for (uint32_t i : order) {
+            uint64_t b = p->src_offset[i] - lo, e = b + p->nbytes[i];
+            S += (size_t)((e - 1) / C - b / C + 1);
+        }
+        p->seg_chunk.resize(S);
+        p->seg_off.resize(S);
+        p->seg_tensor.resize(S);
+        p->seg_len.resize(S);
+        p->seg_toff.resize(S);
+        p->chunk_seg_begin.assign(p->num_chunks + 1, 0);
+        size_t s = 0;
+        for (uint32_t i : order) {
+            uint64_t b = p->src_offset[i] - lo, e = b + p->nbytes[i];
+            for (uint64_t x = b; x < e;) {
+                uint64_t k = x / C, cend = std::min(e, (k + 1) * C);
+                p->seg_chunk[s] = (uint32_t)k;
+                p->seg_off[s] = (uint32_t)(x - k * C);
+                p->seg_tensor[s] = i;
+                p->seg_len[s] = (uint32_t)(cend - x);
+                p->seg_toff[s] = x - b;
+                p->chunk_seg_begin[k + 1]++;
+                ++s;
+                x = cend;
+            }
+        }
+        for (size_t k = 0; k < p->num_chunks; ++k)
+            p->chunk_seg_begin[k + 1] += p->chunk_seg_begin[k];
+        if (S >= (1ull << 32)) return fail(II_EINVAL, "ii_plan: more than 2^32 segments");
+
+        // 5. tiles: per chunk, windows of tile_bytes and the segments meeting them
+        uint32_t T = env_u32("II_TILE_BYTES", kDefaultTile, 1024, 1u << 24) & ~15u;
+        p->tile_bytes = T;
+        p->tiles_per_chunk = (uint32_t)((C + T - 1) / T);
+        p->tiles.assign(p->num_chunks * p->tiles_per_chunk, TileDev{0, 0});
+        for (size_t k = 0; k < p->num_chunks; ++k) {
+            uint64_t s0 = p->chunk_seg_begin[k], s1 = p->chunk_seg_begin[k + 1];
+            uint64_t len = p->chunk_len(k);
+            uint64_t first = s0, last = s0;
+            for (uint32_t t = 0; t < p->tiles_per_chunk; ++t) {
+                uint64_t w0 = (uint64_t)t * T, w1 = std::min(len, w0 + T);
+                TileDev& td = p->tiles[k * p->tiles_per_chunk + t];
+                if (w0 >= len) {
+                    td.first = td.last = (uint32_t)s1;
+                    continue;
+                }
+                while (first < s1 && (uint64_t)p->seg_off[first] + p->seg_len[first] <= w0) ++first;
+                if (last < first) last = first;
+                while (last < s1 && p->seg_off[last] < w1) ++last;
+                td.first = (uint32_t)first;
+                td.last = (uint32_t)last;
+            }
+        }
+    } catch (const std::bad_alloc&) {
+        return fail(II_ENOMEM, "ii_plan: host allocation failed");
+    }
+
+    p->ring_depth = env_u32("II_RING_DEPTH", 3, 1, 8);
+    {
+        long cores = sysconf(_SC_NPROCESSORS_ONLN);
+        uint32_t dflt = (uint32_t)std::max(1L, std::min(8L, cores));
+        p->host_threads = env_u32("II_HOST_THREADS", dflt, 1, 64);
+    }
+    *out = p.release();
+    return II_OK;
+}
+
+extern "C" void ii_plan_free(ii_plan_t* plan) {
+    if (!plan) return;
+    runtime_destroy(plan);
+    delete plan;
+}
+
+extern "C" size_t ii_plan_num_tensors(const ii_plan_t* p) { return p ? p->nbytes.size() : 0; }
+extern "C" size_t ii_plan_num_chunks(const ii_plan_t* p) { return p ? p->num_chunks : 0; }
+extern "C" size_t ii_plan_num_segments(const ii_plan_t* p) { return p ? p->seg_len.size() : 0; }
+extern "C" uint64_t ii_plan_chunk_bytes(const ii_plan_t* p) { return p ? p->chunk_bytes : 0; }
+extern "C" uint64_t ii_plan_payload_bytes(const ii_plan_t* p) { return p ? p->payload : 0; }
+extern "C" uint64_t ii_plan_arena_bytes(const ii_plan_t* p) { return p ? p->arena_bytes : 0; }
+
+extern "C" void ii_plan_span(const ii_plan_t* p, uint64_t* lo, uint64_t* hi) {
+    if (lo) *lo = p ? p->lo : 0;
+    if (hi) *hi = p ? p->hi : 0;
+}
+
+extern "C" int ii_plan_tensors(const ii_plan_t* p, uint64_t* nbytes, uint64_t* dst_offset) {
+    if (!p) return fail(II_EINVAL, "ii_plan_tensors: plan is NULL");
+    size_t n = p->nbytes.size();
+    if (nbytes && n) memcpy(nbytes, p->nbytes.data(), n * 8);
+    if (dst_offset && n) memcpy(dst_offset, p->dst_offset.data(), n * 8);
+    return II_OK;
+}
+
+extern "C" int ii_plan_chunks(const ii_plan_t* p, uint64_t* src_begin, uint64_t* len,
+                              uint64_t* seg_begin) {
+    if (!p) return fail(II_EINVAL, "ii_plan_chunks: plan is NULL");
+    for (size_t k = 0; k < p->num_chunks; ++k) {
+        if (src_begin) src_begin[k] = p->lo + k * p->chunk_bytes;
+        if (len) len[k] = p->chunk_len(k);
+    }
+    if (seg_begin)
+        for (size_t k = 0; k <= p->num_chunks; ++k) seg_begin[k] = p->chunk_seg_begin[k];
+    return II_OK;
+}
+
+extern "C" int ii_plan_segments(const ii_plan_t* p, uint32_t* chunk, uint32_t* chunk_off,
+                                uint32_t* tensor, uint64_t* tensor_off, uint32_t* len) {
+    if (!p) return fail(II_EINVAL, "ii_plan_segments: plan is NULL");
+    size_t S = p->seg_len.size();
+    if (!S) return II_OK;
+    if (chunk) memcpy(chunk, p->seg_chunk.data(), S * 4);
+    if (chunk_off) memcpy(chunk_off, p->seg_off.data(), S * 4);
+    if (tensor) memcpy(tensor, p->seg_tensor.data(), S * 4);
+    if (tensor_off) memcpy(tensor_off, p->seg_toff.data(), S * 8);
+    if (len) memcpy(len, p->seg_len.data(), S * 4);
+    return II_OK;
+}
+
+extern "C" int ii_plan_tiles(const ii_plan_t* p, uint32_t* tile_bytes, uint32_t* tiles_per_chunk,
+                             uint32_t* first, uint32_t* last) {
+    if (!p) return fail(II_EINVAL, "ii_plan_tiles: plan is NULL");
+    if (tile_bytes) *tile_bytes = p->tile_bytes;
+    if (tiles_per_chunk) *tiles_per_chunk = p->tiles_per_chunk;
+    for (size_t g = 0; g < p->tiles.size(); ++g) {
+        if (first) first[g] = p->tiles[g].first;
+        if (last) last[g] = p->tiles[g].last;
+    }
+    return II_OK;
+}
+
+extern "C" const char* ii_plan_tensor_name(const ii_plan_t* p, size_t i) {
+    if (!p || i >= p->names.size()) return "";
+    return p->names[i].c_str();
+}
+
+extern "C" const char* ii_strerror(int status) {
+    switch (status) {
+    case II_OK: return "success";
+    case II_EINVAL: return "invalid argument";
+    case II_EOVERFLOW: return "size or offset overflows 64 bits";
+    case II_EOVERLAP: return "overlapping ranges";
+    case II_EALIGN: return "destination not aligned to dst_align";
+    case II_ENOMEM: return "out of memory";
+    case II_EARENA: return "arena too small";
+    case II_EBUSY: return "plan in use by another call";
+    case II_EHIP: return "HIP runtime error";
+    case II_ERANGE: return "blob or image shorter than the plan's span";
+    default: return "unknown status";
+    }
+}
+
+extern "C" const char* ii_last_error(void) { return g_last_error.c_str(); }

@@ -1,0 +1,612 @@
+// Load pipeline: pinned staging ring, bulk host-to-device copies on a
+// dedicated copy stream, per-chunk scatter on a dedicated scatter stream,
+// hipEvent edges between them, and the C-ABI entry points that drive it.
+//
+// The chunk lifecycle of InstantInfer's refined tensor materialisation
+// (arXiv 2607.18957, Sec. 4.2) maps onto the ring as follows.
+//   InDisk -> InMem   host threads copy chunk k from the blob into pinned
+//                     slot k mod D (skipped when the blob is pinned). The
+//                     slot is reused only once the copy that last read it
+//                     has finished: host wait on copy_done[slot].
+//   InMem  -> InGPU   one hipMemcpyAsync per chunk into device slot k mod D on
+//                     the copy stream, after scatter_done[slot] (the device
+//                     slot is free); records copy_done[slot]. One copy stream
+//                     keeps the bulk copies back to back and in chunk order,
+//                     the paper's (C_i,InGPU)->(C_i+1,InMem) edge, and avoids
+//                     the bus congestion of unrestricted concurrent copies.
+//   InGPU  -> tensors the scatter stream waits for copy_done[slot] and runs
+//                     the scatter kernel for chunk k, moving its tensor pieces
+//                     from Alloc to Loaded; records scatter_done[slot].
+//   Destroyed         scatter_done[slot] releases the slot to chunk k + D.
+// The caller's stream gates the first write into destination memory (entry
+// event) and waits for the last scatter (done event), so the load is ordered
+// on it like any other stream work.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <condition_variable>
+#include <cstring>
+#include <functional>
+#include <mutex>
+#include <thread>
+#include <vector>
+
+#include "ii_internal.h"
+
+namespace ii {
+
+hipError_t launch_scatter_slot(const uint8_t* slot, uint32_t k, const SegDev* segs,
+                               const TileDev* tiles, uint64_t chunk_bytes, uint64_t last_len,
+                               uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes,
+                               hipStream_t stream);
+hipError_t launch_scatter_image(const uint8_t* span, const SegDev* segs, const TileDev* tiles,
+                                uint64_t chunk_bytes, uint64_t last_len, uint32_t num_chunks,
+                                uint32_t tpc, uint32_t tile_bytes, hipStream_t stream);
+hipError_t launch_zero(const RangeDev* ranges, uint32_t n, hipStream_t stream);
+
+#define II_HIP(call)                                                                   \
+    do {                                                                               \
+        hipError_t e_ = (call);                                                        \
+        if (e_ != hipSuccess) {                                                        \
+            (void)hipGetLastError();                                                   \
+            return fail(e_ == hipErrorOutOfMemory ? II_ENOMEM : II_EHIP, "%s: %s (%s:%d)", \
+                        #call, hipGetErrorString(e_), __FILE__, __LINE__);             \
+        }                                                                              \
+    } while (0)
+
+// Fixed set of host threads that split one large memcpy between them.
+class CopyPool {
+   public:
+    explicit CopyPool(uint32_t n) : n_(n) {
+        for (uint32_t i = 1; i < n_; ++i) threads_.emplace_back([this, i] { worker(i); });
+    }
+    ~CopyPool() {
+        {
+            std::lock_guard<std::mutex> g(m_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        for (auto& t : threads_) t.join();
+    }
+    // Copy len bytes from src to dst using every thread of the pool.
+    void copy(void* dst, const void* src, uint64_t len) {
+        if (n_ <= 1 || len < (4u << 20)) {
+            memcpy(dst, src, len);
+            return;
+        }
+        {
+            std::lock_guard<std::mutex> g(m_);
+            dst_ = static_cast<uint8_t*>(dst);
+            src_ = static_cast<const uint8_t*>(src);
+            len_ = len;
+            pending_ = n_ - 1;
+            ++gen_;
+        }
+        cv_.notify_all();
+        part(0);
+        std::unique_lock<std::mutex> l(m_);
+        done_.wait(l, [this] { return pending_ == 0; });
+    }
+
+   private:
+    void part(uint32_t i) {
+        const uint64_t per = ((len_ + n_ - 1) / n_ + 4095) & ~4095ull;
+        const uint64_t b = std::min(len_, (uint64_t)i * per), e = std::min(len_, b + per);
+        if (e > b) memcpy(dst_ + b, src_ + b, e - b);
+    }
+    void worker(uint32_t i) {
+        uint64_t seen = 0;
+        for (;;) {
+            {
+                std::unique_lock<std::mutex> l(m_);
+                cv_.wait(l, [&] { return stop_ || gen_ != seen; });
+                if (stop_) return;
+                seen = gen_;
+            }
+            part(i);
+            {
+                std::lock_guard<std::mutex> g(m_);
+                if (--pending_ == 0) done_.notify_one();
+            }
+        }
+    }
+    uint32_t n_;
+    std::vector<std::thread> threads_;
+    std::mutex m_;
+    std::condition_variable cv_, done_;
+    bool stop_ = false;
+    uint64_t gen_ = 0;
+    uint32_t pending_ = 0;
+    uint8_t* dst_ = nullptr;
+    const uint8_t* src_ = nullptr;
+    uint64_t len_ = 0;
+};
+
+struct Runtime {
+    int device = -1;
+    // device tables
+    SegDev* d_segs = nullptr;
+    SegDev* h_segs = nullptr;  // pinned staging for d_segs uploads
+    TileDev* d_tiles = nullptr;
+    bool tiles_ready = false;
+    hipEvent_t tables_idle = nullptr;   // after the last kernel that read d_segs
+    hipEvent_t upload_done = nullptr;   // after the last read of h_segs
+    bool tables_used = false, uploaded = false;
+    std::vector<uint64_t> cached_dst;   // destination addresses d_segs was built for
+    bool cached_valid = false;
+    // scrub ranges
+    RangeDev* d_ranges = nullptr;
+    RangeDev* h_ranges = nullptr;
+    size_t ranges_cap = 0;
+    hipEvent_t ranges_idle = nullptr;
+    bool ranges_used = false;
+    // ring
+    uint32_t depth = 0;
+    std::vector<uint8_t*> hslot, dslot;
+    std::vector<hipEvent_t> copy_done, scatter_done;
+    std::vector<char> copy_rec, scatter_rec;
+    hipStream_t copy_s = nullptr, scatter_s = nullptr;
+    hipEvent_t entry = nullptr, done = nullptr;
+    CopyPool* pool = nullptr;
+};
+
+// ---------------------------------------------------------------------------
+// state management
+
+static void free_ring(Runtime* r) {
+    for (auto p : r->hslot) if (p) (void)hipHostFree(p);
+    for (auto p : r->dslot) if (p) (void)hipFree(p);
+    for (auto e : r->copy_done) if (e) (void)hipEventDestroy(e);
+    for (auto e : r->scatter_done) if (e) (void)hipEventDestroy(e);
+    r->hslot.clear();
+    r->dslot.clear();
+    r->copy_done.clear();
+    r->scatter_done.clear();
+    r->copy_rec.clear();
+    r->scatter_rec.clear();
+    if (r->copy_s) (void)hipStreamDestroy(r->copy_s);
+    if (r->scatter_s) (void)hipStreamDestroy(r->scatter_s);
+    if (r->entry) (void)hipEventDestroy(r->entry);
+    if (r->done) (void)hipEventDestroy(r->done);
+    r->copy_s = r->scatter_s = nullptr;
+    r->entry = r->done = nullptr;
+    delete r->pool;
+    r->pool = nullptr;
+    r->depth = 0;
+}
+
+static void destroy(Runtime* r) {
+    if (!r) return;
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (r->device >= 0 && cur != r->device) (void)hipSetDevice(r->device);
+    // drain everything the plan may still have in flight
+    if (r->copy_s) (void)hipStreamSynchronize(r->copy_s);
+    if (r->scatter_s) (void)hipStreamSynchronize(r->scatter_s);
+    if (r->tables_idle && r->tables_used) (void)hipEventSynchronize(r->tables_idle);
+    if (r->upload_done && r->uploaded) (void)hipEventSynchronize(r->upload_done);
+    if (r->ranges_idle && r->ranges_used) (void)hipEventSynchronize(r->ranges_idle);
+    free_ring(r);
+    if (r->d_segs) (void)hipFree(r->d_segs);
+    if (r->h_segs) (void)hipHostFree(r->h_segs);
+    if (r->d_tiles) (void)hipFree(r->d_tiles);
+    if (r->d_ranges) (void)hipFree(r->d_ranges);
+    if (r->h_ranges) (void)hipHostFree(r->h_ranges);
+    if (r->tables_idle) (void)hipEventDestroy(r->tables_idle);
+    if (r->upload_done) (void)hipEventDestroy(r->upload_done);
+    if (r->ranges_idle) (void)hipEventDestroy(r->ranges_idle);
+    (void)hipGetLastError();
+    if (r->device >= 0 && cur >= 0 && cur != r->device) (void)hipSetDevice(cur);
+    delete r;
+}
+
+void runtime_destroy(ii_plan_t* p) {
+    destroy(p->rt);
+    p->rt = nullptr;
+}
+
+static int ensure_tables(ii_plan_t* p) {
+    int dev = -1;
+    II_HIP(hipGetDevice(&dev));
+    if (!p->rt) {
+        p->rt = new (std::nothrow) Runtime();
+        if (!p->rt) return fail(II_ENOMEM, "runtime state allocation failed");
+        p->rt->device = dev;
+    }
+    Runtime* r = p->rt;
+    if (r->device != dev)
+        return fail(II_EINVAL, "plan was first used on device %d, current device is %d",
+                    r->device, dev);
+    if (!r->tables_idle) {
+        II_HIP(hipEventCreateWithFlags(&r->tables_idle, hipEventDisableTiming));
+        II_HIP(hipEventCreateWithFlags(&r->upload_done, hipEventDisableTiming));
+        II_HIP(hipEventCreateWithFlags(&r->ranges_idle, hipEventDisableTiming));
+    }
+    const size_t S = p->seg_len.size();
+    if (S && !r->d_segs) {
+        II_HIP(hipMalloc(&r->d_segs, S * sizeof(SegDev)));
+        II_HIP(hipHostMalloc(&r->h_segs, S * sizeof(SegDev), 0));
+    }
+    if (!p->tiles.empty() && !r->d_tiles) {
+        II_HIP(hipMalloc(&r->d_tiles, p->tiles.size() * sizeof(TileDev)));
+        // synchronous, once per plan: the tile windows never change afterwards
+        II_HIP(hipMemcpy(r->d_tiles, p->tiles.data(), p->tiles.size() * sizeof(TileDev),
+                         hipMemcpyHostToDevice));
+    }
+    return II_OK;
+}
+
+static int ensure_ring(ii_plan_t* p) {
+    Runtime* r = p->rt;
+    if (r->depth) return II_OK;
+    const uint32_t D = p->ring_depth;
+    r->hslot.assign(D, nullptr);
+    r->dslot.assign(D, nullptr);
+    r->copy_done.assign(D, nullptr);
+    r->scatter_done.assign(D, nullptr);
+    r->copy_rec.assign(D, 0);
+    r->scatter_rec.assign(D, 0);
+    r->depth = D;  // free_ring() cleans up partial state on failure below
+    int rc = II_OK;
+    auto bail = [&](int code) {
+        free_ring(r);
+        return code;
+    };
+#define II_RING(call)                                                                    \
+    do {                                                                                 \
+        rc = [&]() -> int { II_HIP(call); return II_OK; }();                             \
+        if (rc) return bail(rc);                                                         \
+    } while (0)
+    const uint64_t C = p->chunk_bytes;
+    for (uint32_t i = 0; i < D; ++i) {
+        II_RING(hipHostMalloc(&r->hslot[i], C, 0));
+        II_RING(hipMalloc(&r->dslot[i], C));
+        II_RING(hipEventCreateWithFlags(&r->copy_done[i], hipEventDisableTiming));
+        II_RING(hipEventCreateWithFlags(&r->scatter_done[i], hipEventDisableTiming));
+    }
+    II_RING(hipStreamCreateWithFlags(&r->copy_s, hipStreamNonBlocking));
+    II_RING(hipStreamCreateWithFlags(&r->scatter_s, hipStreamNonBlocking));
+    II_RING(hipEventCreateWithFlags(&r->entry, hipEventDisableTiming));
+    II_RING(hipEventCreateWithFlags(&r->done, hipEventDisableTiming));
+#undef II_RING
+    r->pool = new (std::nothrow) CopyPool(p->host_threads);
+    if (!r->pool) return bail(fail(II_ENOMEM, "host copy pool allocation failed"));
+    return II_OK;
+}
+
+// ---------------------------------------------------------------------------
+// argument checks
+
+struct DstRange {
+    uint64_t b, e;
+    size_t i;
+};
+
+// Check destination addresses: present, aligned, pairwise disjoint, and
+// disjoint from [avoid_b, avoid_e) (a device-resident source image).
+static int check_dst(const ii_plan_t* p, const uint64_t* dst, uint64_t avoid_b, uint64_t avoid_e) {
+    const size_t n = p->nbytes.size();
+    std::vector<DstRange> v;
+    v.reserve(n);
+    for (size_t i = 0; i < n; ++i) {
+        if (!p->nbytes[i]) continue;
+        if (!dst[i]) return fail(II_EINVAL, "dst_ptrs[%zu] is NULL for a non-empty tensor", i);
+        if (dst[i] & (p->dst_align[i] - 1))
+            return fail(II_EALIGN, "dst_ptrs[%zu]=%#llx is not aligned to %llu", i,
+                        (unsigned long long)dst[i], (unsigned long long)p->dst_align[i]);
+        uint64_t e;
+        if (__builtin_add_overflow(dst[i], p->nbytes[i], &e))
+            return fail(II_EOVERFLOW, "dst_ptrs[%zu] + nbytes overflows", i);
+        if (dst[i] < avoid_e && avoid_b < e)
+            return fail(II_EOVERLAP, "tensor %zu's destination overlaps the source image", i);
+        v.push_back({dst[i], e, i});
+    }
+    std::sort(v.begin(), v.end(), [](const DstRange& a, const DstRange& b) { return a.b < b.b; });
+    for (size_t j = 1; j < v.size(); ++j)
+        if (v[j].b < v[j - 1].e)
+            return fail(II_EOVERLAP, "destinations of tensors %zu and %zu overlap", v[j - 1].i,
+                        v[j].i);
+    return II_OK;
+}
+
+// Make d_segs hold this load's resolved destination addresses. The upload is
+// ordered on `s`, after every kernel that read the previous table.
+static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, uint64_t avoid_b,
+                            uint64_t avoid_e) {
+    Runtime* r = p->rt;
+    const size_t n = p->nbytes.size(), S = p->seg_len.size();
+    if (r->cached_valid && r->cached_dst.size() == n &&
+        (n == 0 || memcmp(r->cached_dst.data(), dst, n * sizeof(uint64_t)) == 0)) {
+        // same destinations as the table on the device: only the image check remains
+        if (avoid_e > avoid_b) {
+            int rc = check_dst(p, dst, avoid_b, avoid_e);
+            if (rc) return rc;
+        }
+        return II_OK;
+    }
+    int rc = check_dst(p, dst, avoid_b, avoid_e);
+    if (rc) return rc;
+    if (S) {
+        if (r->uploaded) II_HIP(hipEventSynchronize(r->upload_done));  // h_segs free again
+        for (size_t i = 0; i < S; ++i)
+            r->h_segs[i] = SegDev{p->seg_off[i], p->seg_len[i],
+                                  dst[p->seg_tensor[i]] + p->seg_toff[i]};
+        if (r->tables_used) II_HIP(hipStreamWaitEvent(s, r->tables_idle, 0));
+        II_HIP(hipMemcpyAsync(r->d_segs, r->h_segs, S * sizeof(SegDev), hipMemcpyHostToDevice, s));
+        II_HIP(hipEventRecord(r->upload_done, s));
+        r->uploaded = true;
+    }
+    r->cached_dst.assign(dst, dst + n);
+    r->cached_valid = true;
+    return II_OK;
+}
+
+// Upload the scrub ranges and launch the zero fill on `s`.
+static int launch_scrub(ii_plan_t* p, const std::vector<RangeDev>& ranges, hipStream_t s) {
+    Runtime* r = p->rt;
+    if (ranges.empty()) return II_OK;
+    if (ranges.size() > 0x7fffffffull) return fail(II_EINVAL, "too many scrub ranges");
+    if (r->ranges_used) II_HIP(hipEventSynchronize(r->ranges_idle));
+    if (ranges.size() > r->ranges_cap) {
+        if (r->d_ranges) II_HIP(hipFree(r->d_ranges));
+        if (r->h_ranges) II_HIP(hipHostFree(r->h_ranges));
+        r->d_ranges = nullptr;
+        r->h_ranges = nullptr;
+        r->ranges_cap = 0;
+        II_HIP(hipMalloc(&r->d_ranges, ranges.size() * sizeof(RangeDev)));
+        II_HIP(hipHostMalloc(&r->h_ranges, ranges.size() * sizeof(RangeDev), 0));
+        r->ranges_cap = ranges.size();
+    }
+    memcpy(r->h_ranges, ranges.data(), ranges.size() * sizeof(RangeDev));
+    II_HIP(hipMemcpyAsync(r->d_ranges, r->h_ranges, ranges.size() * sizeof(RangeDev),
+                          hipMemcpyHostToDevice, s));
+    II_HIP(launch_zero(r->d_ranges, (uint32_t)ranges.size(), s));
+    II_HIP(hipEventRecord(r->ranges_idle, s));
+    r->ranges_used = true;
+    return II_OK;
+}
+
+static bool is_pinned_host(const void* ptr) {
+    hipPointerAttribute_t a;
+    hipError_t e = hipPointerGetAttributes(&a, ptr);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return a.type == hipMemoryTypeHost;
+}
+
+static bool is_device_ptr(const void* ptr) {
+    hipPointerAttribute_t a;
+    hipError_t e = hipPointerGetAttributes(&a, ptr);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return a.type == hipMemoryTypeDevice;
+}
+
+// Drain the plan's streams after an error so that nothing enqueued by the
+// failed call still touches caller memory.
+static int drain(ii_plan_t* p, hipStream_t caller, int rc) {
+    if (p->rt) {
+        if (p->rt->copy_s) (void)hipStreamSynchronize(p->rt->copy_s);
+        if (p->rt->scatter_s) (void)hipStreamSynchronize(p->rt->scatter_s);
+    }
+    (void)hipStreamSynchronize(caller);
+    (void)hipGetLastError();
+    return rc;
+}
+
+struct BusyGuard {
+    ii_plan_t* p;
+    bool ok;
+    explicit BusyGuard(ii_plan_t* q) : p(q) {
+        int expect = 0;
+        ok = p->busy.compare_exchange_strong(expect, 1);
+    }
+    ~BusyGuard() {
+        if (ok) p->busy.store(0);
+    }
+};
+
+// ---------------------------------------------------------------------------
+// the pipeline
+
+static int run_ring(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst, hipStream_t stream,
+                    const std::vector<RangeDev>* scrub) {
+    int rc = ensure_tables(p);
+    if (rc) return rc;
+    rc = ensure_ring(p);
+    if (rc) return rc;
+    Runtime* r = p->rt;
+    const bool pinned = is_pinned_host(blob);
+
+    // entry edge: destination writes start after the caller's prior work
+    II_HIP(hipEventRecord(r->entry, stream));
+    II_HIP(hipStreamWaitEvent(r->scatter_s, r->entry, 0));
+    rc = prepare_segments(p, dst, r->scatter_s, 0, 0);
+    if (rc) return rc;
+    if (scrub) {
+        rc = launch_scrub(p, *scrub, r->scatter_s);
+        if (rc) return rc;
+    }
+
+    const uint32_t D = r->depth, K = (uint32_t)p->num_chunks;
+    const uint64_t C = p->chunk_bytes, last_len = K ? p->chunk_len(K - 1) : 0;
+    for (uint32_t k = 0; k < K; ++k) {
+        const uint32_t slot = k % D;
+        const uint64_t len = p->chunk_len(k);
+        const uint8_t* from = blob + p->lo + (uint64_t)k * C;
+        if (!pinned) {
+            // InDisk -> InMem: the pinned slot is free once its last copy finished
+            if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
+            r->pool->copy(r->hslot[slot], from, len);
+            from = r->hslot[slot];
+        }
+        // InMem -> InGPU, once the device slot's previous scatter is done
+        if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(r->copy_s, r->scatter_done[slot], 0));
+        II_HIP(hipMemcpyAsync(r->dslot[slot], from, len, hipMemcpyHostToDevice, r->copy_s));
+        II_HIP(hipEventRecord(r->copy_done[slot], r->copy_s));
+        r->copy_rec[slot] = 1;
+        // InGPU -> tensors Loaded, then the slot is released
+        II_HIP(hipStreamWaitEvent(r->scatter_s, r->copy_done[slot], 0));
+        II_HIP(launch_scatter_slot(r->dslot[slot], k, r->d_segs, r->d_tiles, C, last_len, K,
+                                   p->tiles_per_chunk, p->tile_bytes, r->scatter_s));
+        II_HIP(hipEventRecord(r->scatter_done[slot], r->scatter_s));
+        r->scatter_rec[slot] = 1;
+    }
+    II_HIP(hipEventRecord(r->tables_idle, r->scatter_s));
+    r->tables_used = true;
+    II_HIP(hipEventRecord(r->done, r->scatter_s));
+    II_HIP(hipStreamWaitEvent(stream, r->done, 0));
+    return II_OK;
+}
+
+static int run_device(ii_plan_t* p, const uint8_t* image, const uint64_t* dst, hipStream_t stream) {
+    int rc = ensure_tables(p);
+    if (rc) return rc;
+    Runtime* r = p->rt;
+    const uint64_t ib = reinterpret_cast<uint64_t>(image);
+    rc = prepare_segments(p, dst, stream, ib + p->lo, ib + p->hi);
+    if (rc) return rc;
+    const uint32_t K = (uint32_t)p->num_chunks;
+    if (K) {
+        II_HIP(launch_scatter_image(image + p->lo, r->d_segs, r->d_tiles, p->chunk_bytes,
+                                    p->chunk_len(K - 1), K, p->tiles_per_chunk, p->tile_bytes,
+                                    stream));
+    }
+    II_HIP(hipEventRecord(r->tables_idle, stream));
+    r->tables_used = true;
+    return II_OK;
+}
+
+}  // namespace ii
+
+using namespace ii;
+
+extern "C" int ii_load(ii_plan_t* p, const void* host_blob, uint64_t blob_bytes,
+                       void* const* dst_ptrs, hipStream_t stream) {
+    if (!p) return fail(II_EINVAL, "ii_load: plan is NULL");
+    const size_t n = p->nbytes.size();
+    if (n && !dst_ptrs) return fail(II_EINVAL, "ii_load: dst_ptrs is NULL");
+    if (p->num_chunks && !host_blob) return fail(II_EINVAL, "ii_load: host_blob is NULL");
+    if (blob_bytes < p->hi)
+        return fail(II_ERANGE, "ii_load: blob has %llu bytes, plan needs %llu",
+                    (unsigned long long)blob_bytes, (unsigned long long)p->hi);
+    if (p->num_chunks && is_device_ptr(host_blob))
+        return fail(II_EINVAL, "ii_load: host_blob is device memory (use ii_load_device)");
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_load: plan in use");
+    int rc = run_ring(p, static_cast<const uint8_t*>(host_blob),
+                      reinterpret_cast<const uint64_t*>(dst_ptrs), stream, nullptr);
+    return rc ? drain(p, stream, rc) : II_OK;
+}
+
+extern "C" int ii_load_device(ii_plan_t* p, const void* dev_image, uint64_t image_bytes,
+                              void* const* dst_ptrs, hipStream_t stream) {
+    if (!p) return fail(II_EINVAL, "ii_load_device: plan is NULL");
+    const size_t n = p->nbytes.size();
+    if (n && !dst_ptrs) return fail(II_EINVAL, "ii_load_device: dst_ptrs is NULL");
+    if (p->num_chunks && !dev_image) return fail(II_EINVAL, "ii_load_device: dev_image is NULL");
+    if (image_bytes < p->hi)
+        return fail(II_ERANGE, "ii_load_device: image has %llu bytes, plan needs %llu",
+                    (unsigned long long)image_bytes, (unsigned long long)p->hi);
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_load_device: plan in use");
+    int rc = run_device(p, static_cast<const uint8_t*>(dev_image),
+                        reinterpret_cast<const uint64_t*>(dst_ptrs), stream);
+    return rc ? drain(p, stream, rc) : II_OK;
+}
+
+// Bytes of the old layout's tensor ranges that no new tensor covers, as
+// device address ranges inside the arena, split into pieces of at most
+// 1 MiB (one workgroup each).
+static std::vector<RangeDev> scrub_ranges(const ii_plan_t* po, const ii_plan_t* pn, uint64_t arena) {
+    std::vector<std::pair<uint64_t, uint64_t>> olds, news;
+    for (size_t i = 0; i < po->nbytes.size(); ++i)
+        if (po->nbytes[i]) olds.push_back({po->dst_offset[i], po->dst_offset[i] + po->nbytes[i]});
+    for (size_t i = 0; i < pn->nbytes.size(); ++i)
+        if (pn->nbytes[i]) news.push_back({pn->dst_offset[i], pn->dst_offset[i] + pn->nbytes[i]});
+    // both layouts are in increasing, non-overlapping order by construction
+    std::vector<RangeDev> out;
+    const uint64_t piece = 1u << 20;
+    size_t j = 0;
+    for (auto [b, e] : olds) {
+        uint64_t x = b;
+        while (j < news.size() && news[j].second <= x) ++j;
+        size_t jj = j;
+        while (x < e) {
+            uint64_t y = e;
+            if (jj < news.size() && news[jj].first < e) y = std::max(x, news[jj].first);
+            for (uint64_t c = x; c < y; c += piece)
+                out.push_back(RangeDev{arena + c, arena + std::min(y, c + piece)});
+            if (jj < news.size() && news[jj].first < e) {
+                x = std::max(x, news[jj].second);
+                ++jj;
+            } else {
+                x = e;
+            }
+        }
+    }
+    return out;
+}
+
+extern "C" int ii_switch(const ii_plan_t* po, ii_plan_t* pn, void* arena, uint64_t arena_bytes,
+                         const void* host_blob_new, uint64_t blob_bytes, hipStream_t stream) {
+    if (!po || !pn) return fail(II_EINVAL, "ii_switch: plan is NULL");
+    if (!arena) return fail(II_EINVAL, "ii_switch: arena is NULL");
+    if (arena_bytes < pn->arena_bytes || arena_bytes < po->arena_bytes)
+        return fail(II_EARENA, "ii_switch: arena has %llu bytes, plans need %llu (new) / %llu (old)",
+                    (unsigned long long)arena_bytes, (unsigned long long)pn->arena_bytes,
+                    (unsigned long long)po->arena_bytes);
+    const uint64_t a = reinterpret_cast<uint64_t>(arena);
+    if (a & (pn->max_align - 1))
+        return fail(II_EALIGN, "ii_switch: arena not aligned to %llu",
+                    (unsigned long long)pn->max_align);
+    if (pn->num_chunks && !host_blob_new) return fail(II_EINVAL, "ii_switch: host blob is NULL");
+    if (blob_bytes < pn->hi)
+        return fail(II_ERANGE, "ii_switch: blob has %llu bytes, plan needs %llu",
+                    (unsigned long long)blob_bytes, (unsigned long long)pn->hi);
+    if (pn->num_chunks && is_device_ptr(host_blob_new))
+        return fail(II_EINVAL, "ii_switch: host blob is device memory");
+    BusyGuard g(pn);
+    if (!g.ok) return fail(II_EBUSY, "ii_switch: plan in use");
+    std::vector<uint64_t> dst(pn->nbytes.size());
+    for (size_t i = 0; i < dst.size(); ++i) dst[i] = a + pn->dst_offset[i];
+    std::vector<RangeDev> scrub = scrub_ranges(po, pn, a);
+    int rc = run_ring(pn, static_cast<const uint8_t*>(host_blob_new), dst.data(), stream, &scrub);
+    return rc ? drain(pn, stream, rc) : II_OK;
+}
+
+extern "C" int ii_plan_set_ring(ii_plan_t* p, uint32_t depth, uint32_t host_threads) {
+    if (!p) return fail(II_EINVAL, "ii_plan_set_ring: plan is NULL");
+    if (depth < 1 || depth > 8 || host_threads < 1 || host_threads > 64)
+        return fail(II_EINVAL, "ii_plan_set_ring: depth must be 1..8, host_threads 1..64");
+    if (p->rt && p->rt->depth) return fail(II_EBUSY, "ii_plan_set_ring: ring already allocated");
+    p->ring_depth = depth;
+    p->host_threads = host_threads;
+    return II_OK;
+}
+
+extern "C" int ii_plan_release(ii_plan_t* p) {
+    if (!p) return fail(II_EINVAL, "ii_plan_release: plan is NULL");
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_plan_release: plan in use");
+    runtime_destroy(p);
+    return II_OK;
+}
+
+extern "C" int ii_host_alloc(uint64_t bytes, void** out) {
+    if (!out) return fail(II_EINVAL, "ii_host_alloc: out is NULL");
+    *out = nullptr;
+    if (!bytes) return II_OK;
+    II_HIP(hipHostMalloc(out, bytes, 0));
+    return II_OK;
+}
+
+extern "C" int ii_host_free(void* ptr) {
+    if (!ptr) return II_OK;
+    II_HIP(hipHostFree(ptr));
+    return II_OK;
+}

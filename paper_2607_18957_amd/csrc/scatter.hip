@@ -1,0 +1,226 @@
+// Chunk -> tensor scatter for gfx950 (CDNA4), and the zero-fill used by the
+// arena switch.
+//
+// The scatter is the device half of the refined tensor materialisation in
+// InstantInfer (arXiv 2607.18957, Sec. 4.2): once a chunk is resident in
+// device memory, every tensor piece it holds is copied into the tensor's own
+// buffer ((C_i,InGPU)->(T_j,Alloc) moves T_j to Loaded). It is pure data
+// movement, bound by HBM bandwidth: per payload byte one read of the chunk
+// and one write of the tensor.
+//
+// Work split. A chunk is cut into tiles of tile_bytes; one 256-thread
+// workgroup owns one tile. The planner stores, per tile, the window of
+// segment rows whose bytes meet it, so a workgroup reads only its own rows.
+//
+// Units. Destination memory is written in 16-byte blocks aligned to 16
+// bytes, so every store of a block that a segment covers completely is one
+// dwordx4 store. A unit is one (segment, destination block) pair. A unit
+// belongs to the tile holding the source byte of the first destination byte
+// it covers (its anchor), so every unit has exactly one owner even when the
+// source and destination phases (address mod 16) differ, and the units a
+// tile owns are contiguous within each segment.
+//
+// Lanes to units. The workgroup stages its segment rows in LDS, counts each
+// segment's units in the tile, and forms an exclusive prefix sum. Lane u of
+// the tile's unit range then finds its segment by binary search over the
+// prefix sums in LDS. Consecutive lanes get consecutive units, so a large
+// segment is copied with fully coalesced 16-byte accesses, and many
+// segments smaller than a wavefront (64 lanes x 16 B = 1 KiB) are served by
+// one wavefront in the same pass.
+//
+// Phase shift. The 16 source bytes of a destination block start at any
+// address a. The lane loads the aligned 16-byte words at a & ~15 and
+// (a & ~15) + 16 -- each only if it holds a byte the unit needs, so no load
+// touches a 16-byte word outside the source data -- and assembles the block
+// with byte funnel shifts (v_alignbyte). Blocks a segment covers only partly (its first and last
+// block, or a segment shorter than 16 bytes) are written with 8/4/2/1-byte
+// stores of exactly the covered bytes: padding and neighbouring tensors are
+// never read-modify-written.
+#include <hip/hip_runtime.h>
+
+#include "ii_internal.h"
+#include "scatter_math.h"
+
+namespace ii {
+
+namespace {
+
+// Global-address-space accesses: plain pointers made from integer addresses
+// would be generic (flat) accesses, which also count against the LDS wait
+// counter.
+#define II_GLOBAL __attribute__((address_space(1)))
+typedef uint32_t v4u32 __attribute__((ext_vector_type(4)));
+typedef II_GLOBAL v4u32 g_v4;
+typedef II_GLOBAL uint64_t g_u64;
+typedef II_GLOBAL uint32_t g_u32;
+typedef II_GLOBAL uint16_t g_u16;
+typedef II_GLOBAL uint8_t g_u8;
+
+struct DevMem {
+    __device__ __forceinline__ U4 ld16(uint64_t a) const {
+        const v4u32 x = *reinterpret_cast<const g_v4*>(a);
+        return U4{x.x, x.y, x.z, x.w};
+    }
+    __device__ __forceinline__ void st16(uint64_t a, U4 v) {
+        v4u32 x = {v.x, v.y, v.z, v.w};
+        *reinterpret_cast<g_v4*>(a) = x;
+    }
+    __device__ __forceinline__ void st8(uint64_t a, uint32_t lo, uint32_t hi) {
+        *reinterpret_cast<g_u64*>(a) = ((uint64_t)hi << 32) | lo;
+    }
+    __device__ __forceinline__ void st4(uint64_t a, uint32_t v) { *reinterpret_cast<g_u32*>(a) = v; }
+    __device__ __forceinline__ void st2(uint64_t a, uint16_t v) { *reinterpret_cast<g_u16*>(a) = v; }
+    __device__ __forceinline__ void st1(uint64_t a, uint8_t v) { *reinterpret_cast<g_u8*>(a) = v; }
+};
+
+// Inclusive prefix sum across the 64 lanes of a wavefront.
+__device__ __forceinline__ uint32_t wave_scan(uint32_t v) {
+    const uint32_t lane = threadIdx.x & 63u;
+#pragma unroll
+    for (uint32_t d = 1; d < 64; d <<= 1) {
+        const uint32_t t = __shfl_up(v, d, 64);
+        if (lane >= d) v += t;
+    }
+    return v;
+}
+
+constexpr int kUnroll = 4;  // units in flight per lane
+
+}  // namespace
+
+// One workgroup's share of the scatter: tile t of chunk k, whose bytes start
+// at device address cbase.
+__device__ __forceinline__ void scatter_tile(uint64_t cbase, uint32_t k, uint32_t t,
+                                             const SegDev* __restrict__ segs,
+                                             const TileDev* __restrict__ tiles,
+                                             uint64_t chunk_bytes, uint64_t last_len,
+                                             uint32_t num_chunks, uint32_t tpc,
+                                             uint32_t tile_bytes) {
+    __shared__ SegRow rows[kMaxSegBatch];
+    __shared__ uint32_t pre[kMaxSegBatch];
+    __shared__ uint32_t wsum[kBlock / 64];
+
+    const uint32_t tid = threadIdx.x;
+    const uint64_t clen = (k + 1 == num_chunks) ? last_len : chunk_bytes;
+    const uint64_t w0 = (uint64_t)t * tile_bytes;
+    if (k >= num_chunks || w0 >= clen) return;  // uniform across the workgroup
+    const uint64_t w1 = min(clen, w0 + tile_bytes);
+    const TileDev td = tiles[(uint64_t)k * tpc + t];
+    DevMem mem;
+
+    for (uint32_t s0 = td.first; s0 < td.last; s0 += kMaxSegBatch) {
+        const uint32_t ns = min((uint32_t)kMaxSegBatch, td.last - s0);
+        uint32_t cnt = 0;
+        if (tid < ns) {
+            const SegDev sd = segs[s0 + tid];
+            rows[tid] = make_row(sd.dst, sd.off, sd.len, cbase, w0, w1, &cnt);
+        }
+        const uint32_t inc = wave_scan(cnt);
+        if ((tid & 63u) == 63u) wsum[tid >> 6] = inc;
+        __syncthreads();
+        uint32_t before_wave = 0, total = 0;
+#pragma unroll
+        for (uint32_t w = 0; w < kBlock / 64; ++w) {
+            const uint32_t x = wsum[w];
+            before_wave += (w < (tid >> 6)) ? x : 0u;
+            total += x;
+        }
+        if (tid < ns) {
+            const uint32_t ex = before_wave + inc - cnt;
+            pre[tid] = ex;
+            rows[tid].ubase -= ex;
+        }
+        __syncthreads();
+
+        for (uint32_t base = 0; base < total; base += kBlock * kUnroll) {
+            U4 v[kUnroll];
+            UnitIO io[kUnroll];
+#pragma unroll
+            for (int j = 0; j < kUnroll; ++j) {
+                const uint32_t u = base + (uint32_t)j * kBlock + tid;
+                io[j].c0 = io[j].c1 = 0;
+                if (u < total) {
+                    io[j] = unit_io(rows[find_row(pre, ns, u)], u);
+                    U4 x0{0, 0, 0, 0}, x1{0, 0, 0, 0};
+                    if (io[j].need0) x0 = mem.ld16(io[j].A);
+                    if (io[j].need1) x1 = mem.ld16(io[j].A + 16);
+                    v[j] = funnel16(x0, x1, io[j].p);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kUnroll; ++j)
+                if (io[j].c1 > io[j].c0) store_unit(mem, io[j].d, v[j], io[j].c0, io[j].c1);
+        }
+        __syncthreads();  // rows/pre are rewritten by the next batch
+    }
+}
+
+// Ring path: chunk k, staged in a device slot that starts at `slot`. One
+// workgroup per tile of the chunk.
+__global__ __launch_bounds__(kBlock) void scatter_slot(
+    const uint8_t* __restrict__ slot, uint32_t k, const SegDev* __restrict__ segs,
+    const TileDev* __restrict__ tiles, uint64_t chunk_bytes, uint64_t last_len,
+    uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes) {
+    scatter_tile(reinterpret_cast<uint64_t>(slot), k, blockIdx.x, segs, tiles, chunk_bytes,
+                 last_len, num_chunks, tpc, tile_bytes);
+}
+
+// Resident-image path: every chunk in one launch; `span` is the device address
+// of the blob's span byte lo, so chunk k starts at span + k * chunk_bytes.
+// Workgroup g handles tile g % tpc of chunk g / tpc.
+__global__ __launch_bounds__(kBlock) void scatter_image(
+    const uint8_t* __restrict__ span, const SegDev* __restrict__ segs,
+    const TileDev* __restrict__ tiles, uint64_t chunk_bytes, uint64_t last_len,
+    uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes) {
+    const uint32_t k = blockIdx.x / tpc, t = blockIdx.x % tpc;
+    scatter_tile(reinterpret_cast<uint64_t>(span) + (uint64_t)k * chunk_bytes, k, t, segs, tiles,
+                 chunk_bytes, last_len, num_chunks, tpc, tile_bytes);
+}
+
+// Zero the byte ranges [r.begin, r.end) (device addresses). One workgroup per
+// range; 16-byte stores for whole aligned blocks, exact narrow stores at the
+// edges.
+__global__ __launch_bounds__(kBlock) void zero_ranges(const RangeDev* __restrict__ ranges,
+                                                       uint32_t n) {
+    if (blockIdx.x >= n) return;
+    const RangeDev r = ranges[blockIdx.x];
+    if (r.end <= r.begin) return;
+    DevMem mem;
+    const uint64_t b0 = r.begin >> 4, b1 = (r.end - 1) >> 4;
+    const U4 z{0, 0, 0, 0};
+    for (uint64_t b = b0 + threadIdx.x; b <= b1; b += kBlock) {
+        const uint64_t d = b << 4;
+        const uint64_t ds = d > r.begin ? d : r.begin;
+        const uint64_t de = (d + 16) < r.end ? d + 16 : r.end;
+        store_unit(mem, d, z, (uint32_t)(ds - d), (uint32_t)(de - d));
+    }
+}
+
+hipError_t launch_scatter_slot(const uint8_t* slot, uint32_t k, const SegDev* segs,
+                               const TileDev* tiles, uint64_t chunk_bytes, uint64_t last_len,
+                               uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes,
+                               hipStream_t stream) {
+    if (tpc == 0) return hipSuccess;
+    hipLaunchKernelGGL(scatter_slot, dim3(tpc), dim3(kBlock), 0, stream, slot, k, segs, tiles,
+                       chunk_bytes, last_len, num_chunks, tpc, tile_bytes);
+    return hipGetLastError();
+}
+
+hipError_t launch_scatter_image(const uint8_t* span, const SegDev* segs, const TileDev* tiles,
+                                uint64_t chunk_bytes, uint64_t last_len, uint32_t num_chunks,
+                                uint32_t tpc, uint32_t tile_bytes, hipStream_t stream) {
+    const uint64_t blocks = (uint64_t)num_chunks * tpc;
+    if (blocks == 0) return hipSuccess;
+    if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(scatter_image, dim3((uint32_t)blocks), dim3(kBlock), 0, stream, span, segs,
+                       tiles, chunk_bytes, last_len, num_chunks, tpc, tile_bytes);
+    return hipGetLastError();
+}
+
+hipError_t launch_zero(const RangeDev* ranges, uint32_t n, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(zero_ranges, dim3(n), dim3(kBlock), 0, stream, ranges, n);
+    return hipGetLastError();
+}
+
+}  // namespace ii

@@ -1,0 +1,128 @@
+"""The scatter kernel's arithmetic, run on the CPU against the oracle.
+
+The emulator (tests/emu) executes the kernel's own per-lane code
+(scatter_math.h) lane by lane over the plan's real tiles and segment rows,
+with every load and store bounds-checked (see its header). Its output arena
+must equal the oracle's byte for byte, for aligned and misaligned
+destinations, every source phase, tiny and large tables, and LDS batches
+smaller than a tile's row count.
+"""
+import itertools
+import random
+
+import numpy as np
+import pytest
+
+import emu
+import oracle_pins
+from paper_2607_18957_amd import ii, synth
+
+
+def _run(orc, table, *, chunk=None, arena_phase=0, src_phase=0, batch=256, dst_of=None,
+         tile=None, monkeypatch=None):
+    if tile:
+        monkeypatch.setenv("II_TILE_BYTES", str(tile))
+    plan = ii.ii_plan(table, chunk or table.chunk_bytes)
+    nb, off = plan.tensors()
+    blob = synth.blob(table) if hasattr(table, "seed") else table.blob
+    rel = off if dst_of is None else dst_of(nb, off)
+    arena_len = max(plan.arena_bytes, int((rel + nb).max()) if len(nb) else 0) + 64
+    base = (1 << 36) + arena_phase
+    dst = base + rel
+    can = synth.canary(arena_len)
+    got = can.copy()
+    ok, msg, stats = emu.scatter(plan, blob, dst, base, got, (1 << 40) + src_phase, batch)
+    assert ok, msg
+    want = can.copy()
+    # the oracle arena, at the same (possibly shifted) offsets
+    if dst_of is None:
+        orc.arena(orc.nbytes(table), table.src_offset, table.dst_align, blob, want)
+    else:
+        outs = orc.load(orc.nbytes(table), table.src_offset, blob)
+        for o, d in zip(outs, dst - base):
+            want[int(d):int(d) + o.size] = o
+    assert np.array_equal(got, want), int(np.flatnonzero(got != want)[0])
+    return stats
+
+
+def test_tiny(orc):
+    _run(orc, synth.tiny())
+    _run(orc, synth.tiny(dst_align=4096))
+    _run(orc, synth.tiny(header=1000), src_phase=3)
+
+
+def test_stress_subset_all_phases(orc):
+    t = synth.stress(n=4000, chunk=1 << 20)
+    for ap, sp in [(0, 0), (1, 0), (0, 7), (13, 5), (8, 8)]:
+        stats = _run(orc, t, arena_phase=ap, src_phase=sp)
+    assert stats[3] > 1  # tiles with several rows
+
+
+def test_packed_destinations_misaligned(orc):
+    # dst_align 1: tensors packed back to back, every destination phase occurs
+    t = synth.stress(n=3000, chunk=1 << 18, dst_align=1)
+    _run(orc, t, arena_phase=3, src_phase=11)
+
+
+def test_multi_batch_rows(orc, monkeypatch):
+    # many tiny tensors per tile and a batch of 4 rows: several LDS batches per tile
+    t = synth.stress(n=2000, lo_bytes=1, hi_bytes=40, chunk=1 << 12, dst_align=1)
+    stats = _run(orc, t, batch=4, arena_phase=5, src_phase=9)
+    assert stats[3] > 4
+    stats = _run(orc, t, batch=256, tile=1024, monkeypatch=monkeypatch)
+
+
+def test_small_tiles_many_per_chunk(orc, monkeypatch):
+    t = synth.stress(n=1500, chunk=1 << 16)
+    _run(orc, t, tile=1024, monkeypatch=monkeypatch, arena_phase=6, src_phase=2)
+
+
+def test_exhaustive_tiny_grid(orc):
+    """Every table with up to two tensors from the size grid, every source
+    order, gaps, header offsets, chunk sizes and a spread of destination and
+    source phases."""
+    sizes_set = [0, 1, 2, 3, 15, 16, 17, 31, 33]
+    rng = np.random.default_rng(1)
+    count = 0
+    for n in (1, 2):
+        for sizes in itertools.product(sizes_set, repeat=n):
+            for order in itertools.permutations(range(n)):
+                for gap, H, C in itertools.product((0, 1, 7), (0, 5), (16, 32, 48, 64)):
+                    src, pos = [0] * n, H
+                    for i in order:
+                        src[i] = pos
+                        pos += sizes[i] + gap
+                    t = oracle_pins._u8_table(list(sizes), src, [1] * n)
+                    t.blob = rng.integers(0, 256, size=max(pos, 1), dtype=np.uint8)
+                    t.chunk_bytes = C
+                    ap, sp = count % 16, (count * 7) % 16
+                    _run(orc, t, arena_phase=ap, src_phase=sp)
+                    count += 1
+    assert count > 3000
+
+
+def test_random_dst_gaps(orc):
+    """Destinations not from the plan's layout: arbitrary gaps and phases."""
+    rng = random.Random(4)
+    for trial in range(40):
+        n = rng.randint(1, 30)
+        sizes = [rng.randint(0, 300) for _ in range(n)]
+        order = list(range(n))
+        rng.shuffle(order)
+        src, pos = [0] * n, rng.randint(0, 20)
+        for i in order:
+            src[i] = pos
+            pos += sizes[i] + rng.choice([0, 0, 3, 17])
+        t = oracle_pins._u8_table(sizes, src, [1] * n)
+        t.blob = np.frombuffer(rng.randbytes(pos + 1), dtype=np.uint8).copy()
+        t.chunk_bytes = 16 * rng.randint(1, 20)
+
+        def dst_of(nb, off, rng=rng):
+            out, p = [], 0
+            for x in nb:
+                p += rng.randint(0, 21)
+                out.append(p)
+                p += int(x)
+            return np.array(out, dtype=np.uint64)
+
+        _run(orc, t, dst_of=dst_of, arena_phase=rng.randint(0, 15), src_phase=rng.randint(0, 15))

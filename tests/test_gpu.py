@@ -1,0 +1,327 @@
+"""Device parity: every load goes through the C-ABI (libii.so) on cuda:0 and is
+compared byte for byte with the CPU oracle, with canary-filled destination
+memory and guard bands so that stray writes show up.
+
+Sizes: the tiny and stress sets run whole; the Llama-8B-shaped set (16 GB)
+runs whole in the configuration bench.py times (64 MiB chunks, ring depth 3,
+pageable blob, and the resident-image path); the switch from that arena to
+the Mistral-7B-shaped set runs whole.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU machines, never run there
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2607_18957_amd import ii, synth  # noqa: E402  (fails loudly if libii.so is missing)
+
+import oracle_pins  # noqa: E402
+
+DEV = torch.device("cuda:0")
+GUARD = 4096
+
+
+def _say(msg):
+    print(msg, flush=True)
+
+
+def _canary_buffer(nbytes, seed=0xC0FFEE):
+    can = synth.canary(nbytes, seed=seed)
+    buf = torch.from_numpy(can).to(DEV)
+    return buf, can
+
+
+def _expect_arena(orc, table, blob, canary_slice):
+    want = canary_slice.copy()
+    orc.arena(orc.nbytes(table), table.src_offset, table.dst_align, blob, want)
+    return want
+
+
+def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=None,
+                stream=None, chunk=None):
+    """Load `table` into a canary-filled arena (plan layout) and compare the
+    whole buffer, guard bands included, with the oracle."""
+    plan = ii.ii_plan(table, chunk or table.chunk_bytes)
+    if depth:
+        plan.set_ring(depth, threads or 4)
+    nb, off = plan.tensors()
+    total = plan.arena_bytes + 2 * GUARD
+    buf, can = _canary_buffer(total)
+    base = buf.data_ptr() + GUARD
+    if blob is None:
+        blob = synth.blob(table)
+    _say(f"[{table.name}] mode={mode} N={table.n} K={plan.num_chunks} S={plan.num_segments} "
+         f"depth={depth} arena={plan.arena_bytes}")
+    s = stream or torch.cuda.current_stream(DEV)
+    if mode == "pageable":
+        ii.ii_load(plan, blob, base + off, s)
+    elif mode == "pinned":
+        hb = ii.ii_host_alloc(blob.size)
+        hb.numpy()[:] = blob
+        ii.ii_load(plan, hb, base + off, s)
+    elif mode == "image":
+        img = torch.from_numpy(blob).to(DEV)
+        ii.ii_load_device(plan, img, base + off, s)
+    s.synchronize()
+    got = buf.cpu().numpy()
+    want = can.copy()
+    want[GUARD:GUARD + plan.arena_bytes] = _expect_arena(orc, table, blob,
+                                                         can[GUARD:GUARD + plan.arena_bytes])
+    if not np.array_equal(got, want):
+        bad = np.flatnonzero(got != want)
+        raise AssertionError(f"{table.name}/{mode}: {bad.size} bytes differ, first at "
+                             f"{int(bad[0]) - GUARD} of the arena")
+    return plan
+
+
+@pytest.mark.parametrize("mode", ["pageable", "pinned", "image"])
+def test_tiny(orc, mode):
+    _load_arena(orc, synth.tiny(), mode=mode)
+
+
+@pytest.mark.parametrize("mode", ["pageable", "image"])
+def test_tiny_padded_and_offset(orc, mode):
+    _load_arena(orc, synth.tiny(dst_align=4096), mode=mode)
+    _load_arena(orc, synth.tiny(header=1000), mode=mode)        # every source at 8 mod 16
+    _load_arena(orc, synth.tiny(dst_align=1, header=5), mode=mode)
+
+
+@pytest.mark.parametrize("mode", ["pageable", "pinned", "image"])
+def test_stress_full(orc, mode):
+    """100,000 tensors, 64 B - 64 KiB, 94% of them at a different phase in the
+    source than in the destination, 16 MiB chunks."""
+    _load_arena(orc, synth.stress(), mode=mode)
+
+
+@pytest.mark.parametrize("depth", [1, 2, 3])
+def test_ring_depths_small_chunks(orc, depth):
+    """4 KiB chunks: hundreds of slot reuses per load."""
+    t = synth.stress(n=3000, chunk=4096, dst_align=16)
+    _load_arena(orc, t, depth=depth, threads=2)
+
+
+def test_separate_tensor_buffers(orc):
+    """Destinations are independent allocations, not an arena."""
+    for table in (synth.tiny(), synth.stress(n=5000)):
+        plan = ii.ii_plan(table)
+        nb, _ = plan.tensors()
+        bufs = [torch.empty(max(int(x), 1), dtype=torch.uint8, device=DEV) for x in nb]
+        for b in bufs:
+            b.fill_(0x5A)
+        blob = synth.blob(table)
+        ii.ii_load(plan, blob, [b.data_ptr() for b in bufs])
+        torch.cuda.synchronize()
+        outs = orc.load(orc.nbytes(table), table.src_offset, blob)
+        for i, (b, o) in enumerate(zip(bufs, outs)):
+            got = b.cpu().numpy()
+            assert got[:o.size].tobytes() == o.tobytes(), (table.name, i)
+            if o.size == 0:
+                assert got[0] == 0x5A
+
+
+def test_back_to_back_loads_no_sync(orc):
+    """Two loads on one plan into different arenas with no host sync between
+    them: slot reuse carries across calls."""
+    t = synth.stress(n=8000, chunk=1 << 16)
+    plan = ii.ii_plan(t)
+    plan.set_ring(2, 2)
+    nb, off = plan.tensors()
+    blob_a = synth.blob(t)
+    blob_b = synth.blob(t.blob_bytes, seed=77)
+    a = torch.zeros(plan.arena_bytes, dtype=torch.uint8, device=DEV)
+    b = torch.zeros(plan.arena_bytes, dtype=torch.uint8, device=DEV)
+    s = torch.cuda.current_stream(DEV)
+    for _ in range(3):
+        ii.ii_load(plan, blob_a, a.data_ptr() + off, s)
+        ii.ii_load(plan, blob_b, b.data_ptr() + off, s)
+        ii.ii_load_device(plan, torch.from_numpy(blob_a).to(DEV), b.data_ptr() + off, s)
+        ii.ii_load(plan, blob_b, b.data_ptr() + off, s)
+    s.synchronize()
+    wa = orc.nbytes(t)
+    ea = np.zeros(plan.arena_bytes, np.uint8)
+    eb = np.zeros(plan.arena_bytes, np.uint8)
+    orc.arena(wa, t.src_offset, t.dst_align, blob_a, ea)
+    orc.arena(wa, t.src_offset, t.dst_align, blob_b, eb)
+    assert np.array_equal(a.cpu().numpy(), ea)
+    assert np.array_equal(b.cpu().numpy(), eb)
+
+
+def test_other_stream(orc):
+    """The load is ordered on the caller's stream: a fill enqueued before it on
+    the same stream is overwritten, a copy enqueued after it sees the data."""
+    t = synth.tiny()
+    plan = ii.ii_plan(t)
+    nb, off = plan.tensors()
+    s = torch.cuda.Stream(DEV)
+    arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=DEV)
+    out = torch.empty_like(arena)
+    blob = synth.blob(t)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        arena.fill_(7)
+        ii.ii_load(plan, blob, arena.data_ptr() + off, s)
+        out.copy_(arena)
+    s.synchronize()
+    want = np.full(plan.arena_bytes, 7, np.uint8)
+    orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob, want)
+    assert np.array_equal(out.cpu().numpy(), want)
+
+
+def test_exhaustive_tiny_grid(orc):
+    """Every table with up to two tensors from the size grid, all source
+    orders, gaps, header offsets and chunk sizes, through the resident-image
+    path; every 8th case also through the ring."""
+    import itertools
+    sizes_set = [0, 1, 2, 3, 15, 16, 17, 31, 33]
+    rng = np.random.default_rng(3)
+    img = torch.empty(1 << 12, dtype=torch.uint8, device=DEV)
+    arena = torch.empty(1 << 12, dtype=torch.uint8, device=DEV)
+    count = 0
+    for n in (1, 2):
+        for sizes in itertools.product(sizes_set, repeat=n):
+            for order in itertools.permutations(range(n)):
+                for gap, H, C in itertools.product((0, 1, 7), (0, 5), (16, 32, 48, 64)):
+                    src, pos = [0] * n, H
+                    for i in order:
+                        src[i] = pos
+                        pos += sizes[i] + gap
+                    al = 1
+                    t = oracle_pins._u8_table(list(sizes), src, [al] * n)
+                    blob = rng.integers(0, 256, size=max(pos, 1), dtype=np.uint8)
+                    plan = ii.ii_plan(t, C)
+                    _, off = plan.tensors()
+                    phase = count % 16
+                    base = arena.data_ptr() + 64 + phase
+                    arena.fill_(0xA5)
+                    img_off = (count * 5) % 16
+                    img[img_off:img_off + blob.size].copy_(torch.from_numpy(blob))
+                    if count % 8 == 0:
+                        ii.ii_load(plan, blob, base + off)
+                    else:
+                        ii.ii_load_device(plan, (img.data_ptr() + img_off, blob.size), base + off)
+                    got = arena.cpu().numpy()
+                    want = np.full(arena.numel(), 0xA5, np.uint8)
+                    for o, d, x in zip(orc.load(orc.nbytes(t), t.src_offset, blob), off, sizes):
+                        want[64 + phase + int(d):64 + phase + int(d) + x] = o
+                    assert np.array_equal(got, want), (sizes, src, C, phase)
+                    plan.free()
+                    count += 1
+    _say(f"{count} tiny tables bit-exact")
+
+
+def test_errors_leave_plan_usable(orc):
+    t = synth.tiny()
+    plan = ii.ii_plan(t)
+    nb, off = plan.tensors()
+    arena = torch.empty(plan.arena_bytes + 512, dtype=torch.uint8, device=DEV)
+    blob = synth.blob(t)
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_load(plan, blob, arena.data_ptr() + 1 + off)           # misaligned
+    assert e.value.name == "II_EALIGN"
+    bad = (arena.data_ptr() + off).copy()
+    bad[3] = bad[2]                                                    # two tensors share bytes
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_load(plan, blob, bad)
+    assert e.value.name == "II_EOVERLAP"
+    img = torch.from_numpy(blob).to(DEV)
+    with pytest.raises(ii.IIError) as e:                               # dst inside the image
+        ii.ii_load_device(plan, img, img.data_ptr() + off)
+    assert e.value.name == "II_EOVERLAP"
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_load(plan, img, arena.data_ptr() + off)                 # device "host" blob
+    assert e.value.name == "II_EINVAL"
+    # still usable
+    ii.ii_load(plan, blob, arena.data_ptr() + off)
+    torch.cuda.synchronize()
+    want = arena.cpu().numpy().copy()
+    orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob, want)
+    assert np.array_equal(arena.cpu().numpy(), want)
+
+
+def test_switch_small(orc):
+    """Switch semantics on small sets: new bytes where new tensors are,
+    zeros where only old tensors were, the rest untouched."""
+    old = synth.stress(n=3000, chunk=1 << 18, seed=5)
+    new = synth.stress(n=2000, rng_seed=9, chunk=1 << 18, seed=6)
+    po, pn = ii.ii_plan(old), ii.ii_plan(new)
+    size = max(po.arena_bytes, pn.arena_bytes)
+    buf, can = _canary_buffer(size + 2 * GUARD)
+    base = buf.data_ptr() + GUARD
+    blob_o, blob_n = synth.blob(old), synth.blob(new)
+    ii.ii_load(po, blob_o, base + po.tensors()[1])
+    ii.ii_switch(po, pn, base, size, blob_n)
+    torch.cuda.synchronize()
+    want = can.copy()
+    view = want[GUARD:GUARD + size]
+    orc.arena(orc.nbytes(old), old.src_offset, old.dst_align, blob_o, view)
+    orc.switch(orc.nbytes(old), old.dst_align, orc.nbytes(new), new.src_offset, new.dst_align,
+               blob_n, view)
+    assert np.array_equal(buf.cpu().numpy(), want)
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_switch(po, pn, base, min(po.arena_bytes, pn.arena_bytes) - 256, blob_n)
+    assert e.value.name == "II_EARENA"
+
+
+@pytest.mark.slow
+def test_llama8b_full(orc):
+    """The benchmarked workload at full size (16.06 GB, 291 tensors, 240
+    chunks of 64 MiB, ring depth 3): pageable ring path and resident-image
+    path, whole arena compared with the oracle, guard bands checked."""
+    t = synth.llama8b()
+    plan = ii.ii_plan(t)
+    nb, off = plan.tensors()
+    assert plan.arena_bytes == plan.payload_bytes == 16_060_522_496
+    blob = synth.blob(t)
+    _say("llama8b: oracle arena")
+    want = np.empty(plan.arena_bytes, np.uint8)
+    orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob, want)
+    buf = torch.empty(plan.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
+    base = buf.data_ptr() + GUARD
+    for mode in ("pageable", "image"):
+        buf.fill_(0xA5)
+        _say(f"llama8b: {mode} load")
+        if mode == "pageable":
+            ii.ii_load(plan, blob, base + off)
+        else:
+            img = torch.from_numpy(blob).to(DEV)
+            ii.ii_load_device(plan, img, base + off)
+        torch.cuda.synchronize()
+        if mode == "image":
+            del img
+        got = buf.cpu().numpy()
+        assert (got[:GUARD] == 0xA5).all() and (got[GUARD + plan.arena_bytes:] == 0xA5).all()
+        assert np.array_equal(got[GUARD:GUARD + plan.arena_bytes], want), mode
+        del got
+    _say("llama8b: bit-exact")
+
+
+@pytest.mark.slow
+def test_switch_llama8b_to_mistral7b(orc):
+    """The arena holding the Llama-8B-shaped set is reused for the
+    Mistral-7B-shaped set: new bytes at the new offsets, the 1.58 GB tail of
+    the old set cleared to zero."""
+    old, new = synth.llama8b(), synth.mistral7b()
+    po, pn = ii.ii_plan(old), ii.ii_plan(new)
+    assert po.arena_bytes - pn.arena_bytes == 1_577_058_304
+    arena = torch.empty(po.arena_bytes, dtype=torch.uint8, device=DEV)
+    blob_o = synth.blob(old)
+    ii.ii_load(po, blob_o, arena.data_ptr() + po.tensors()[1])
+    torch.cuda.synchronize()
+    before = arena.cpu().numpy()
+    del blob_o
+    blob_n = synth.blob(new)
+    _say("switch: llama8b arena -> mistral7b")
+    ii.ii_switch(po, pn, arena, po.arena_bytes, blob_n)
+    torch.cuda.synchronize()
+    got = arena.cpu().numpy()
+    orc.switch(orc.nbytes(old), old.dst_align, orc.nbytes(new), new.src_offset, new.dst_align,
+               blob_n, before)
+    assert np.array_equal(got, before)
+    assert (got[pn.arena_bytes:] == 0).all()

@@ -1,0 +1,196 @@
+"""The planner (host side of the C-ABI) against the oracle, bit for bit.
+
+Every integer the planner produces -- chunk windows, segments, destination
+offsets, arena size, span -- is compared with the oracle's brute-force
+answer; error classification is compared where the oracle defines it. The
+per-tile segment windows (an implementation detail of the kernel's work
+split) are checked against a brute-force intersection.
+"""
+import itertools
+import random
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from paper_2607_18957_amd import synth
+from paper_2607_18957_amd import ii
+
+import oracle_pins
+
+
+def _compare(orc, table, chunk=None):
+    chunk = chunk or table.chunk_bytes
+    plan = ii.ii_plan(table, chunk)
+    nb = orc.nbytes(table)
+    op = orc.plan(nb, table.src_offset, chunk)
+    off, arena = orc.layout(nb, table.dst_align)
+    pnb, poff = plan.tensors()
+    assert np.array_equal(pnb, nb)
+    assert np.array_equal(poff, off)
+    assert plan.arena_bytes == arena
+    assert plan.payload_bytes == int(nb.sum())
+    assert plan.span == orc.span(nb, table.src_offset)
+    b, l, sb = plan.chunks()
+    assert np.array_equal(b, op["chunk_begin"]) and np.array_equal(l, op["chunk_len"])
+    s = plan.segments()
+    assert plan.num_segments == len(op["seg_len"])
+    assert np.array_equal(s["chunk"], op["seg_chunk"])
+    assert np.array_equal(s["chunk_off"].astype(np.uint64), op["seg_chunk_off"])
+    assert np.array_equal(s["tensor"], op["seg_tensor"])
+    assert np.array_equal(s["tensor_off"], op["seg_tensor_off"])
+    assert np.array_equal(s["len"].astype(np.uint64), op["seg_len"])
+    # CSR chunk -> segments
+    assert sb[0] == 0 and sb[-1] == plan.num_segments
+    assert np.array_equal(np.diff(sb.astype(np.int64)),
+                          np.bincount(op["seg_chunk"], minlength=plan.num_chunks))
+    _check_tiles(plan, s, l)
+    return plan
+
+
+def _check_tiles(plan, s, chunk_len):
+    tb, tpc, first, last = plan.tiles()
+    assert tb % 16 == 0 and tpc == -(-plan.chunk_bytes // tb)
+    _, _, sb = plan.chunks()
+    off = s["chunk_off"].astype(np.int64)
+    end = off + s["len"].astype(np.int64)
+    for k in range(plan.num_chunks):
+        a, b = int(sb[k]), int(sb[k + 1])
+        t = np.arange(tpc, dtype=np.int64)
+        w0 = t * tb
+        w1 = np.minimum(int(chunk_len[k]), w0 + tb)
+        live = w0 < int(chunk_len[k])
+        # segments meeting [w0, w1): end > w0 and off < w1 (rows are sorted and disjoint)
+        f = a + np.searchsorted(end[a:b], w0, side="right")
+        l = a + np.searchsorted(off[a:b], w1, side="left")
+        g = k * tpc + t
+        nonempty = live & (f < l)
+        assert np.array_equal(first[g[nonempty]], f[nonempty]), k
+        assert np.array_equal(last[g[nonempty]], l[nonempty]), k
+        empty = live & ~(f < l)
+        assert np.array_equal(first[g[empty]], last[g[empty]]), k
+        # brute force on a few windows
+        for tt in list(np.flatnonzero(live)[:3]) + list(np.flatnonzero(live)[-2:]):
+            meet = np.flatnonzero((off[a:b] < w1[tt]) & (end[a:b] > w0[tt])) + a
+            if meet.size:
+                assert (first[k * tpc + tt], last[k * tpc + tt]) == (meet[0], meet[-1] + 1)
+
+
+@pytest.mark.parametrize("name", ["tiny", "llama8b", "mistral7b", "llama70b"])
+def test_named_sets(orc, name):
+    t = synth.SETS[name]()
+    plan = _compare(orc, t)
+    want = {"tiny": (5, 42), "llama8b": (240, 530), "mistral7b": (216, 506),
+            "llama70b": (526, 1248)}[name]
+    assert (plan.num_chunks, plan.num_segments) == want
+
+
+def test_stress_set(orc):
+    t = synth.stress()
+    plan = _compare(orc, t)
+    assert plan.num_chunks == 57
+    assert plan.payload_bytes == t.blob_bytes  # packed from offset 0, no gaps
+
+
+def test_header_offset_and_alignment_variants(orc):
+    for t in (synth.tiny(header=1000), synth.tiny(dst_align=4096), synth.tiny(dst_align=1),
+              synth.stress(n=5000, header=5, dst_align=16)):
+        _compare(orc, t)
+
+
+def test_small_tiles(orc, monkeypatch):
+    monkeypatch.setenv("II_TILE_BYTES", "1024")
+    t = synth.stress(n=3000, chunk=1 << 16)
+    plan = _compare(orc, t)
+    assert plan.tiles()[0] == 1024
+
+
+def test_exhaustive_tiny_tables(orc):
+    sizes_set = [0, 1, 2, 3, 15, 16, 17, 31, 33]
+    for n in (0, 1, 2):
+        for sizes in itertools.product(sizes_set, repeat=n):
+            for order in itertools.permutations(range(n)):
+                for gap, H, C in itertools.product((0, 1, 7), (0, 5), (16, 32, 48, 64)):
+                    src, pos = [0] * n, H
+                    for i in order:
+                        src[i] = pos
+                        pos += sizes[i] + gap
+                    t = oracle_pins._u8_table(list(sizes), src, [1] * n)
+                    t.chunk_bytes = C
+                    _compare(orc, t)
+
+
+@settings(max_examples=150, deadline=None)
+@given(st.data())
+def test_random_tables(orc, data):
+    n = data.draw(st.integers(0, 40))
+    dts = data.draw(st.lists(st.sampled_from(list(synth.DTYPE_CODES.values())), min_size=n,
+                             max_size=n))
+    shapes = data.draw(st.lists(st.lists(st.integers(0, 40), min_size=0, max_size=3),
+                                min_size=n, max_size=n))
+    aligns = data.draw(st.lists(st.sampled_from([1, 2, 4, 16, 256, 4096]), min_size=n,
+                                max_size=n))
+    gaps = data.draw(st.lists(st.integers(0, 70), min_size=n, max_size=n))
+    order = data.draw(st.permutations(list(range(n))))
+    C = 16 * data.draw(st.integers(1, 40))
+    t = oracle_pins._T(dts, shapes, [0] * n, aligns)
+    nb = [int(x) for x in __import__("oracle").default().nbytes(t)]
+    pos = data.draw(st.integers(0, 100))
+    src = [0] * n
+    for j, i in enumerate(order):
+        src[i] = pos
+        pos += nb[i] + gaps[j]
+    t = oracle_pins._T(dts, shapes, src, aligns)
+    t.chunk_bytes = C
+    _compare(orc, t)
+
+
+def _err(table, chunk):
+    try:
+        ii.ii_plan(table, chunk).free()
+    except ii.IIError as e:
+        return e.name
+    return "II_OK"
+
+
+def test_errors(orc):
+    good = oracle_pins._u8_table([10, 10], [0, 10], [1, 1])
+    for c in (0, 8, 17, 1 << 32, (1 << 32) + 16):
+        assert _err(good, c) == "II_EINVAL", c
+    assert _err(good, 16) == "II_OK"
+    assert _err(good, (1 << 32) - 16) == "II_OK"
+    assert _err(oracle_pins._u8_table([10, 10], [0, 9], [1, 1]), 64) == "II_EOVERLAP"
+    assert _err(oracle_pins._u8_table([10, 0], [0, 5], [1, 1]), 64) == "II_OK"
+    assert _err(oracle_pins._u8_table([10], [0], [3]), 64) == "II_EINVAL"
+    assert _err(oracle_pins._T([42], [(4,)], [0], [1]), 64) == "II_EINVAL"
+    assert _err(oracle_pins._T([1], [(-1,)], [0], [1]), 64) == "II_EINVAL"
+    assert _err(oracle_pins._T([1], [(1 << 32, 1 << 32)], [0], [1]), 64) == "II_EOVERFLOW"
+    assert _err(oracle_pins._T([10], [(1 << 62,)], [0], [1]), 64) == "II_EOVERFLOW"
+    assert _err(oracle_pins._T([5], [(1 << 62,)], [0], [1]), 64) == "II_EINVAL"  # 2^63 B: > 2^32 chunks
+    assert _err(oracle_pins._T([1], [(16,)], [(1 << 64) - 8], [1]), 64) == "II_EOVERFLOW"
+    # the error classes the oracle also defines agree on random bad tables
+    rng = random.Random(3)
+    for _ in range(300):
+        n = rng.randint(1, 6)
+        sizes = [rng.randint(0, 50) for _ in range(n)]
+        src = [rng.randint(0, 120) for _ in range(n)]
+        al = [rng.choice([1, 2, 3, 16, 256]) for _ in range(n)]
+        want = {0: "II_OK", 1: "II_EINVAL", 2: "II_EOVERFLOW", 3: "II_EOVERLAP"}[
+            orc.check(sizes, src, al)]
+        assert _err(oracle_pins._u8_table(sizes, src, al), 64) == want, (sizes, src, al)
+
+
+def test_names_and_detail():
+    t = synth.tiny()
+    plan = ii.ii_plan(t)
+    assert plan.name(0) == "embed" and plan.name(38) == "lm_head" and plan.name(99) == ""
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_plan(t, 17)
+    assert "chunk_bytes" in e.value.detail
+
+
+def test_empty_plan():
+    plan = ii.ii_plan(oracle_pins._u8_table([], [], []), 64)
+    assert (plan.num_tensors, plan.num_chunks, plan.num_segments, plan.arena_bytes) == (0, 0, 0, 0)
+    plan = ii.ii_plan(oracle_pins._u8_table([0, 0], [3, 9], [16, 16]), 64)
+    assert (plan.num_chunks, plan.num_segments, plan.span) == (0, 0, (0, 0))
