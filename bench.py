@@ -87,6 +87,28 @@ def h2d_peak(torch, dev, chunk_bytes: int) -> dict:
     return {"GBps": results[best], "variant": best, "all": results}
 
 
+def d2d_ceiling(torch, dev, nbytes: int = 4 << 30, reps: int = 10) -> dict:
+    """Device-to-device hipMemcpyAsync of `nbytes` (read + write counted):
+    the measured ceiling for a plain copy on this GPU. Also the plain copy
+    kernel of known size that hardware-counter readings are scaled by."""
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    a.fill_(3)
+    b.copy_(a)
+    s = torch.cuda.current_stream(dev)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    torch.cuda.synchronize(dev)
+    for x, y in ev:
+        x.record(s)
+        b.copy_(a)
+        y.record(s)
+    torch.cuda.synchronize(dev)
+    ms = statistics.median(x.elapsed_time(y) for x, y in ev)
+    del a, b
+    return {"GBps": 2 * nbytes / (ms * 1e-3) / 1e9, "bytes": nbytes, "median_ms": ms}
+
+
 def cpu_baseline(table, blob, budget_s: float = 12.0, max_passes: int = 4) -> dict:
     """The CPU oracle (sequential allocate-and-copy loader), pinned to one
     core, on the whole table; passes until the budget is used."""
@@ -112,7 +134,110 @@ def cpu_baseline(table, blob, budget_s: float = 12.0, max_passes: int = 4) -> di
                       f"{len(cores)} host cores"}
 
 
+# ---------------------------------------------------------------------------
+# profile summaries (rocprofv3 CSV output -> profiles/*.txt, *.json)
+
+PROFILE_CMDS = {
+    "trace": "cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv -d <out>/trace "
+             "-o run -- python3 <repo>/bench.py",
+    "fetch": "cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/pmc_fetch "
+             "-o run -- python3 <repo>/bench.py --e2e-reps 1",
+    "write": "cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/pmc_write "
+             "-o run -- python3 <repo>/bench.py --e2e-reps 1",
+}
+
+
+def _counter_means(path: str, counter: str) -> dict:
+    """Mean counter value per dispatch, keyed by (kernel name, grid size)."""
+    import csv
+    acc: dict = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] != counter:
+                continue
+            k = (r["Kernel_Name"], int(r["Grid_Size"]))
+            acc.setdefault(k, []).append(float(r["Counter_Value"]))
+    return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
+
+
+def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -> None:
+    """Write the committed profile summaries for the scatter kernel from one
+    kernel-trace run and two counter runs of this benchmark."""
+    import csv
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
+    run = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    lines = ["# Kernel statistics, llama8b-shaped workload (291 tensors, 16,060,522,496 B,",
+             "# 240 chunks of 64 MiB), one GPU",
+             f"# command: {PROFILE_CMDS['trace']}",
+             "# (rocprofv3 --stats summary, durations in ns)", ""]
+    lines.append(f"{'kernel':<34}{'calls':>7}{'avg_ns':>14}{'min_ns':>12}{'max_ns':>12}{'pct':>8}")
+    for r in rows:
+        name = r["Name"].split("(")[0][:33]
+        lines.append(f"{name:<34}{r['Calls']:>7}{float(r['AverageNs']):>14.1f}"
+                     f"{float(r['MinNs']):>12.0f}{float(r['MaxNs']):>12.0f}"
+                     f"{float(r['Percentage']):>8.2f}")
+    img = [r for r in rows if r["Name"].startswith("ii::scatter_image")][0]
+    avg_ms = float(img["AverageNs"]) / 1e6
+    lines += ["", f"scatter_image average per launch: {avg_ms:.4f} ms (rocprofv3)",
+              f"bench.py HIP-event mean in the same run: {run['roofline']['kernel_ms']:.4f} ms",
+              f"bench.py value in the same run: {run['value']:.1f} GB/s, "
+              f"roofline frac {run['roofline']['frac']:.4f}"]
+    open(os.path.join(ROOT, "profiles", "scatter_image_llama8b_kernel_stats.txt"), "w").write(
+        "\n".join(lines) + "\n")
+
+    fetch = _counter_means(os.path.join(fetch_dir, "run_counter_collection.csv"), "FETCH_SIZE")
+    write = _counter_means(os.path.join(write_dir, "run_counter_collection.csv"), "WRITE_SIZE")
+    # calibration: the 4 GiB device-to-device copy (the largest runtime copy kernel)
+    copies = [k for k in fetch if k[0].startswith("__amd_rocclr_copyBuffer")]
+    cal = max(copies, key=lambda k: fetch[k][0])
+    cal_kib = (4 << 30) / 1024
+    f_scale = cal_kib / fetch[cal][0]
+    w_scale = cal_kib / write[cal][0]
+    key = [k for k in fetch if k[0].startswith("ii::scatter_image")][0]
+    fetch_b = fetch[key][0] * 1024 * f_scale
+    write_b = write[key][0] * 1024 * w_scale
+    payload = run["config"]["payload_bytes"]
+    out = {"kernel": "scatter_image", "workload": "llama8b", "kernel_source_hash":
+           kernel_source_hash(), "fetch_bytes": fetch_b, "write_bytes": write_b,
+           "bytes_per_launch": fetch_b + write_b, "algorithmic_bytes":
+           run["roofline"]["bytes_per_launch"], "dispatches": fetch[key][1],
+           "calibration": {"kernel": cal[0], "grid": cal[1], "bytes_copied": 4 << 30,
+                           "fetch_kib": fetch[cal][0], "write_kib": write[cal][0],
+                           "fetch_scale": f_scale, "write_scale": w_scale}}
+    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+    t = ["# HBM traffic of scatter_image, llama8b-shaped workload, from rocprofv3 counters",
+         f"# command 1: {PROFILE_CMDS['fetch']}",
+         f"# command 2: {PROFILE_CMDS['write']}",
+         "# Counters are KiB per dispatch. Scale factors come from the 4 GiB device-to-device",
+         "# copy in the same runs (a plain copy kernel of known size: 4 GiB read, 4 GiB written).",
+         "",
+         f"calibration kernel        {cal[0]} (grid {cal[1]}), {fetch[cal][1]} dispatches",
+         f"  FETCH_SIZE per dispatch {fetch[cal][0]:.1f} KiB  -> scale {f_scale:.4f}",
+         f"  WRITE_SIZE per dispatch {write[cal][0]:.1f} KiB  -> scale {w_scale:.4f}",
+         f"scatter_image             {fetch[key][1]} dispatches (grid {key[1]})",
+         f"  FETCH_SIZE per dispatch {fetch[key][0]:.1f} KiB  -> {fetch_b:.0f} B",
+         f"  WRITE_SIZE per dispatch {write[key][0]:.1f} KiB  -> {write_b:.0f} B",
+         f"  measured HBM bytes per launch  {fetch_b + write_b:.0f}",
+         f"  algorithmic bytes per launch   {run['roofline']['bytes_per_launch']} "
+         f"(2 x payload {payload} + segment and tile tables)",
+         f"  measured / algorithmic         {(fetch_b + write_b) / run['roofline']['bytes_per_launch']:.4f}",
+         f"kernel source hash        {kernel_source_hash()}"]
+    slot = [k for k in fetch if k[0].startswith("ii::scatter_slot")]
+    if slot:
+        k = slot[0]
+        t += [f"scatter_slot (ring path)  {fetch[k][1]} dispatches, per 64 MiB chunk: "
+              f"fetch {fetch[k][0] * 1024 * f_scale:.0f} B, "
+              f"write {write[k][0] * 1024 * w_scale:.0f} B"]
+    open(os.path.join(ROOT, "profiles", "scatter_image_llama8b_counters.txt"), "w").write(
+        "\n".join(t) + "\n")
+    print("\n".join(lines + [""] + t))
+
+
 def main() -> int:
+    if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
+        summarize(*sys.argv[2:6])
+        return 0
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
@@ -184,6 +309,9 @@ def main() -> int:
         if rec.get("kernel_source_hash") == kernel_source_hash():
             traffic = rec.get("bytes_per_launch")
 
+    d2d = d2d_ceiling(torch, dev)
+    log(f"D2D copy ceiling {d2d['GBps']:.0f} GB/s")
+
     # ---- end to end through the host: pageable and pinned blobs
     del image
     torch.cuda.empty_cache()
@@ -236,7 +364,8 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": KERNEL, "bytes_per_launch": alg_bytes,
-                     "kernel_ms": kernel_ms},
+                     "kernel_ms": kernel_ms, "d2d_copy_ceiling_GBps": d2d["GBps"],
+                     "frac_of_d2d_ceiling": achieved / d2d["GBps"]},
         "cpu_baseline": cpu,
         "e2e": e2e,
     }
