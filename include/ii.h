@@ -193,10 +193,16 @@ int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint6
  * Ring configuration, before the plan's first load or after
  * ii_plan_release. depth = number of chunk slots in flight (1..8; default 3
  * or $II_RING_DEPTH); host_threads = threads copying a pageable blob into
- * the pinned slots (1..64; default min(8, cores) or $II_HOST_THREADS).
- * Errors: II_EINVAL (out of range), II_EBUSY (ring already allocated).
+ * the pinned slots (1..64; default min(8, cores) or $II_HOST_THREADS);
+ * copy_streams = host-to-device copy streams the chunks alternate between
+ * (1..min(2, depth); default 2 or $II_COPY_STREAMS). With 1, chunk copies run
+ * strictly one after another in chunk order; with 2, the copies of chunks k
+ * and k+1 may overlap, which keeps the link busy while the device maps
+ * freshly pinned host pages. Errors: II_EINVAL (out of range), II_EBUSY
+ * (ring already allocated).
  */
-int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads);
+int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads,
+                     uint32_t copy_streams);
 
 /* Free the plan's staging ring and device tables after waiting for its
  * outstanding work (the paper frees its I/O buffers as soon as loading

@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "ii.h"
+#include "scatter_math.h"
 
 namespace ii {
 
@@ -34,9 +35,8 @@ struct RangeDev {
     uint64_t end;
 };
 
-constexpr uint32_t kBlock = 256;              // threads per scatter workgroup
-constexpr uint32_t kDefaultTile = 16u << 10;  // bytes of chunk per workgroup
-constexpr uint32_t kMaxSegBatch = kBlock;     // segment rows staged in LDS at once
+constexpr uint32_t kDefaultTile = 8u << 10;  // bytes of chunk per workgroup (<= kMaxTile)
+constexpr uint32_t kMaxCopyStreams = 2;       // host-to-device copy streams of a ring
 
 struct Runtime;  // device-side state (runtime.hip)
 
@@ -72,6 +72,7 @@ struct ii_plan_s {
     // runtime configuration
     uint32_t ring_depth = 3;
     uint32_t host_threads = 8;
+    uint32_t copy_streams = 2;
     // device state, created by the first load
     ii::Runtime* rt = nullptr;
     std::atomic<int> busy{0};

@@ -215,7 +215,7 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         if (S >= (1ull << 32)) return fail(II_EINVAL, "ii_plan: more than 2^32 segments");
 
         // 5. tiles: per chunk, windows of tile_bytes and the segments meeting them
-        uint32_t T = env_u32("II_TILE_BYTES", kDefaultTile, 1024, 1u << 24) & ~15u;
+        uint32_t T = env_u32("II_TILE_BYTES", kDefaultTile, 1024, kMaxTile) & ~15u;
         p->tile_bytes = T;
         p->tiles_per_chunk = (uint32_t)((C + T - 1) / T);
         p->tiles.assign(p->num_chunks * p->tiles_per_chunk, TileDev{0, 0});
@@ -242,6 +242,7 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
     }
 
     p->ring_depth = env_u32("II_RING_DEPTH", 3, 1, 8);
+    p->copy_streams = std::min(p->ring_depth, env_u32("II_COPY_STREAMS", 2, 1, kMaxCopyStreams));
     {
         long cores = sysconf(_SC_NPROCESSORS_ONLN);
         uint32_t dflt = (uint32_t)std::max(1L, std::min(8L, cores));

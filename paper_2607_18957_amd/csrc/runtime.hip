@@ -134,6 +134,7 @@ struct Runtime {
     bool tables_used = false, uploaded = false;
     std::vector<uint64_t> cached_dst;   // destination addresses d_segs was built for
     bool cached_valid = false;
+    uint64_t image_b = 0, image_e = 0;  // source image range last checked against them
     // scrub ranges
     RangeDev* d_ranges = nullptr;
     RangeDev* h_ranges = nullptr;
@@ -145,7 +146,8 @@ struct Runtime {
     std::vector<uint8_t*> hslot, dslot;
     std::vector<hipEvent_t> copy_done, scatter_done;
     std::vector<char> copy_rec, scatter_rec;
-    hipStream_t copy_s = nullptr, scatter_s = nullptr;
+    hipStream_t copy_s[kMaxCopyStreams] = {}, scatter_s = nullptr;
+    uint32_t ncopy = 1;
     hipEvent_t entry = nullptr, done = nullptr;
     CopyPool* pool = nullptr;
 };
@@ -164,11 +166,13 @@ static void free_ring(Runtime* r) {
     r->scatter_done.clear();
     r->copy_rec.clear();
     r->scatter_rec.clear();
-    if (r->copy_s) (void)hipStreamDestroy(r->copy_s);
+    for (auto& c : r->copy_s)
+        if (c) (void)hipStreamDestroy(c);
     if (r->scatter_s) (void)hipStreamDestroy(r->scatter_s);
     if (r->entry) (void)hipEventDestroy(r->entry);
     if (r->done) (void)hipEventDestroy(r->done);
-    r->copy_s = r->scatter_s = nullptr;
+    for (auto& c : r->copy_s) c = nullptr;
+    r->scatter_s = nullptr;
     r->entry = r->done = nullptr;
     delete r->pool;
     r->pool = nullptr;
@@ -181,7 +185,8 @@ static void destroy(Runtime* r) {
     (void)hipGetDevice(&cur);
     if (r->device >= 0 && cur != r->device) (void)hipSetDevice(r->device);
     // drain everything the plan may still have in flight
-    if (r->copy_s) (void)hipStreamSynchronize(r->copy_s);
+    for (auto c : r->copy_s)
+        if (c) (void)hipStreamSynchronize(c);
     if (r->scatter_s) (void)hipStreamSynchronize(r->scatter_s);
     if (r->tables_idle && r->tables_used) (void)hipEventSynchronize(r->tables_idle);
     if (r->upload_done && r->uploaded) (void)hipEventSynchronize(r->upload_done);
@@ -264,7 +269,9 @@ static int ensure_ring(ii_plan_t* p) {
         II_RING(hipEventCreateWithFlags(&r->copy_done[i], hipEventDisableTiming));
         II_RING(hipEventCreateWithFlags(&r->scatter_done[i], hipEventDisableTiming));
     }
-    II_RING(hipStreamCreateWithFlags(&r->copy_s, hipStreamNonBlocking));
+    r->ncopy = p->copy_streams;
+    for (uint32_t i = 0; i < r->ncopy; ++i)
+        II_RING(hipStreamCreateWithFlags(&r->copy_s[i], hipStreamNonBlocking));
     II_RING(hipStreamCreateWithFlags(&r->scatter_s, hipStreamNonBlocking));
     II_RING(hipEventCreateWithFlags(&r->entry, hipEventDisableTiming));
     II_RING(hipEventCreateWithFlags(&r->done, hipEventDisableTiming));
@@ -282,9 +289,8 @@ struct DstRange {
     size_t i;
 };
 
-// Check destination addresses: present, aligned, pairwise disjoint, and
-// disjoint from [avoid_b, avoid_e) (a device-resident source image).
-static int check_dst(const ii_plan_t* p, const uint64_t* dst, uint64_t avoid_b, uint64_t avoid_e) {
+// Check destination addresses: present, aligned and pairwise disjoint.
+static int check_dst(const ii_plan_t* p, const uint64_t* dst) {
     const size_t n = p->nbytes.size();
     std::vector<DstRange> v;
     v.reserve(n);
@@ -297,8 +303,6 @@ static int check_dst(const ii_plan_t* p, const uint64_t* dst, uint64_t avoid_b, 
         uint64_t e;
         if (__builtin_add_overflow(dst[i], p->nbytes[i], &e))
             return fail(II_EOVERFLOW, "dst_ptrs[%zu] + nbytes overflows", i);
-        if (dst[i] < avoid_e && avoid_b < e)
-            return fail(II_EOVERLAP, "tensor %zu's destination overlaps the source image", i);
         v.push_back({dst[i], e, i});
     }
     std::sort(v.begin(), v.end(), [](const DstRange& a, const DstRange& b) { return a.b < b.b; });
@@ -309,23 +313,36 @@ static int check_dst(const ii_plan_t* p, const uint64_t* dst, uint64_t avoid_b, 
     return II_OK;
 }
 
+// No destination may overlap the source image [b, e) (one linear pass).
+static int check_image(const ii_plan_t* p, const uint64_t* dst, uint64_t b, uint64_t e) {
+    for (size_t i = 0; i < p->nbytes.size(); ++i)
+        if (p->nbytes[i] && dst[i] < e && b < dst[i] + p->nbytes[i])
+            return fail(II_EOVERLAP, "tensor %zu's destination overlaps the source image", i);
+    return II_OK;
+}
+
 // Make d_segs hold this load's resolved destination addresses. The upload is
-// ordered on `s`, after every kernel that read the previous table.
-static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, uint64_t avoid_b,
-                            uint64_t avoid_e) {
+// ordered on `s`, after every kernel that read the previous table. Checks run
+// only for destinations (and a source image range) not seen before.
+static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, uint64_t image_b,
+                            uint64_t image_e) {
     Runtime* r = p->rt;
     const size_t n = p->nbytes.size(), S = p->seg_len.size();
-    if (r->cached_valid && r->cached_dst.size() == n &&
-        (n == 0 || memcmp(r->cached_dst.data(), dst, n * sizeof(uint64_t)) == 0)) {
-        // same destinations as the table on the device: only the image check remains
-        if (avoid_e > avoid_b) {
-            int rc = check_dst(p, dst, avoid_b, avoid_e);
-            if (rc) return rc;
-        }
+    const bool same = r->cached_valid && r->cached_dst.size() == n &&
+                      (n == 0 || memcmp(r->cached_dst.data(), dst, n * sizeof(uint64_t)) == 0);
+    if (!same) {
+        int rc = check_dst(p, dst);
+        if (rc) return rc;
+    }
+    if (image_e > image_b && !(same && r->image_b == image_b && r->image_e == image_e)) {
+        int rc = check_image(p, dst, image_b, image_e);
+        if (rc) return rc;
+    }
+    if (same) {
+        r->image_b = image_b;
+        r->image_e = image_e;
         return II_OK;
     }
-    int rc = check_dst(p, dst, avoid_b, avoid_e);
-    if (rc) return rc;
     if (S) {
         if (r->uploaded) II_HIP(hipEventSynchronize(r->upload_done));  // h_segs free again
         for (size_t i = 0; i < S; ++i)
@@ -338,6 +355,8 @@ static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, ui
     }
     r->cached_dst.assign(dst, dst + n);
     r->cached_valid = true;
+    r->image_b = image_b;
+    r->image_e = image_e;
     return II_OK;
 }
 
@@ -390,7 +409,8 @@ static bool is_device_ptr(const void* ptr) {
 // failed call still touches caller memory.
 static int drain(ii_plan_t* p, hipStream_t caller, int rc) {
     if (p->rt) {
-        if (p->rt->copy_s) (void)hipStreamSynchronize(p->rt->copy_s);
+        for (auto c : p->rt->copy_s)
+            if (c) (void)hipStreamSynchronize(c);
         if (p->rt->scatter_s) (void)hipStreamSynchronize(p->rt->scatter_s);
     }
     (void)hipStreamSynchronize(caller);
@@ -445,9 +465,10 @@ static int run_ring(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst, hipS
             from = r->hslot[slot];
         }
         // InMem -> InGPU, once the device slot's previous scatter is done
-        if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(r->copy_s, r->scatter_done[slot], 0));
-        II_HIP(hipMemcpyAsync(r->dslot[slot], from, len, hipMemcpyHostToDevice, r->copy_s));
-        II_HIP(hipEventRecord(r->copy_done[slot], r->copy_s));
+        hipStream_t cs = r->copy_s[k % r->ncopy];
+        if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(cs, r->scatter_done[slot], 0));
+        II_HIP(hipMemcpyAsync(r->dslot[slot], from, len, hipMemcpyHostToDevice, cs));
+        II_HIP(hipEventRecord(r->copy_done[slot], cs));
         r->copy_rec[slot] = 1;
         // InGPU -> tensors Loaded, then the slot is released
         II_HIP(hipStreamWaitEvent(r->scatter_s, r->copy_done[slot], 0));
@@ -579,13 +600,17 @@ extern "C" int ii_switch(const ii_plan_t* po, ii_plan_t* pn, void* arena, uint64
     return rc ? drain(pn, stream, rc) : II_OK;
 }
 
-extern "C" int ii_plan_set_ring(ii_plan_t* p, uint32_t depth, uint32_t host_threads) {
+extern "C" int ii_plan_set_ring(ii_plan_t* p, uint32_t depth, uint32_t host_threads,
+                                uint32_t copy_streams) {
     if (!p) return fail(II_EINVAL, "ii_plan_set_ring: plan is NULL");
-    if (depth < 1 || depth > 8 || host_threads < 1 || host_threads > 64)
-        return fail(II_EINVAL, "ii_plan_set_ring: depth must be 1..8, host_threads 1..64");
+    if (depth < 1 || depth > 8 || host_threads < 1 || host_threads > 64 || copy_streams < 1 ||
+        copy_streams > kMaxCopyStreams || copy_streams > depth)
+        return fail(II_EINVAL, "ii_plan_set_ring: depth must be 1..8, host_threads 1..64, "
+                               "copy_streams 1..min(2, depth)");
     if (p->rt && p->rt->depth) return fail(II_EBUSY, "ii_plan_set_ring: ring already allocated");
     p->ring_depth = depth;
     p->host_threads = host_threads;
+    p->copy_streams = copy_streams;
     return II_OK;
 }
 

@@ -84,8 +84,6 @@ __device__ __forceinline__ uint32_t wave_scan(uint32_t v) {
     return v;
 }
 
-constexpr int kUnroll = 4;  // units in flight per lane
-
 }  // namespace
 
 // One workgroup's share of the scatter: tile t of chunk k, whose bytes start

@@ -19,6 +19,11 @@
 
 namespace ii {
 
+constexpr uint32_t kBlock = 256;           // threads per scatter workgroup
+constexpr int kUnroll = 4;                 // units in flight per lane
+constexpr uint32_t kMaxSegBatch = kBlock;  // segment rows staged in LDS at once
+constexpr uint32_t kMaxTile = 64u << 10;   // largest tile a workgroup takes
+
 struct SegRow {
     uint64_t delta;  // source address minus destination address
     uint64_t dbeg;   // destination range [dbeg, dend)

@@ -53,7 +53,7 @@ _sig("ii_plan_free", None, _vp)
 _sig("ii_load", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_load_device", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_switch", _c.c_int, _vp, _vp, _vp, _u64, _vp, _u64, _vp)
-_sig("ii_plan_set_ring", _c.c_int, _vp, _u32, _u32)
+_sig("ii_plan_set_ring", _c.c_int, _vp, _u32, _u32, _u32)
 _sig("ii_plan_release", _c.c_int, _vp)
 for _n in ("ii_plan_num_tensors", "ii_plan_num_chunks", "ii_plan_num_segments"):
     _sig(_n, _sz, _vp)
@@ -247,8 +247,9 @@ class Plan:
         return _lib.ii_plan_tensor_name(self.handle, i).decode()
 
     # configuration ----------------------------------------------------------
-    def set_ring(self, depth: int, host_threads: int) -> None:
-        _check(_lib.ii_plan_set_ring(self.handle, depth, host_threads), "ii_plan_set_ring")
+    def set_ring(self, depth: int, host_threads: int, copy_streams: int = 2) -> None:
+        _check(_lib.ii_plan_set_ring(self.handle, depth, host_threads, min(copy_streams, depth)),
+               "ii_plan_set_ring")
 
     def release(self) -> None:
         _check(_lib.ii_plan_release(self.handle), "ii_plan_release")

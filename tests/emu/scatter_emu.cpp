@@ -23,6 +23,9 @@ using namespace ii;
 
 namespace {
 
+constexpr uint32_t kBlockE = kBlock;  // the kernel's workgroup size
+constexpr int kUnrollE = kUnroll;     // the kernel's units per lane
+
 struct EmuMem {
     // source: chunk bytes, addressed as src_base + (k * C) + off
     const uint8_t* blob = nullptr;
@@ -118,6 +121,7 @@ int emu_scatter(uint64_t num_chunks, uint64_t chunk_bytes, uint64_t lo, uint64_t
     m.writes = &writes;
     uint64_t units = 0, max_rows = 0;
     std::vector<SegRow> rows(batch);
+    if (batch > kMaxSegBatch) batch = kMaxSegBatch;
     std::vector<uint32_t> pre(batch), cnt(batch), srow(batch);
 
     for (uint64_t k = 0; k < num_chunks && m.err.empty(); ++k) {
@@ -142,28 +146,38 @@ int emu_scatter(uint64_t num_chunks, uint64_t chunk_bytes, uint64_t lo, uint64_t
                     rows[i].ubase -= pre[i];
                     srow[i] = s;
                 }
-                for (uint32_t u = 0; u < total && m.err.empty(); ++u) {
-                    const uint32_t r = find_row(pre.data(), ns, u);
-                    if (!(pre[r] <= u && u < pre[r] + cnt[r])) {
-                        m.bad("lane mapped to a row that does not own its unit", u);
-                        break;
+                // lanes exactly as the kernel runs them: kBlock lanes, each with
+                // kUnroll units at stride kBlock, rows found in lock step
+                for (uint32_t base = 0; base < total && m.err.empty(); base += kBlockE * kUnrollE) {
+                    for (uint32_t tid = 0; tid < kBlockE && m.err.empty(); ++tid) {
+                        for (int j = 0; j < kUnrollE; ++j) {
+                            const uint32_t u = base + (uint32_t)j * kBlockE + tid;
+                            if (u >= total || !m.err.empty()) continue;
+                            const uint32_t r = find_row(pre.data(), ns, u);
+                            if (r >= ns) m.bad("row index out of range", r);
+                            if (!(pre[r] <= u && u < pre[r] + cnt[r])) {
+                                m.bad("lane mapped to a row that does not own its unit", u);
+                                break;
+                            }
+                            const uint32_t s = srow[r];
+                            m.row_src_b = cbase + seg_off[s];
+                            m.row_src_e = m.row_src_b + seg_len[s];
+                            m.row_dst_b = rows[r].dbeg;
+                            m.row_dst_e = rows[r].dend;
+                            const UnitIO io = unit_io(rows[r], u);
+                            // the unit's anchor must lie in this tile
+                            const uint64_t first_src = io.d + io.c0 + rows[r].delta - cbase;
+                            if (first_src < w0 || first_src >= w1)
+                                m.bad("unit anchored outside its tile", io.d);
+                            U4 x0{0, 0, 0, 0}, x1{0, 0, 0, 0};
+                            if (io.need0) x0 = m.ld16(io.A);
+                            if (io.need1) x1 = m.ld16(io.A + 16);
+                            const U4 v = funnel16(x0, x1, io.p);
+                            if (io.c1 > io.c0) store_unit(m, io.d, v, io.c0, io.c1);
+                            else m.bad("unit with no bytes", io.d);
+                            ++units;
+                        }
                     }
-                    const uint32_t s = srow[r];
-                    m.row_src_b = cbase + seg_off[s];
-                    m.row_src_e = m.row_src_b + seg_len[s];
-                    m.row_dst_b = rows[r].dbeg;
-                    m.row_dst_e = rows[r].dend;
-                    const UnitIO io = unit_io(rows[r], u);
-                    // the unit's anchor must lie in this tile
-                    const uint64_t first_src = io.d + io.c0 + rows[r].delta - cbase;
-                    if (first_src < w0 || first_src >= w1) m.bad("unit anchored outside its tile", io.d);
-                    U4 x0{0, 0, 0, 0}, x1{0, 0, 0, 0};
-                    if (io.need0) x0 = m.ld16(io.A);
-                    if (io.need1) x1 = m.ld16(io.A + 16);
-                    const U4 v = funnel16(x0, x1, io.p);
-                    if (io.c1 > io.c0) store_unit(m, io.d, v, io.c0, io.c1);
-                    else m.bad("unit with no bytes", io.d);
-                    ++units;
                 }
             }
         }

@@ -45,12 +45,12 @@ def _expect_arena(orc, table, blob, canary_slice):
 
 
 def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=None,
-                stream=None, chunk=None):
+                stream=None, chunk=None, copy_streams=2):
     """Load `table` into a canary-filled arena (plan layout) and compare the
     whole buffer, guard bands included, with the oracle."""
     plan = ii.ii_plan(table, chunk or table.chunk_bytes)
     if depth:
-        plan.set_ring(depth, threads or 4)
+        plan.set_ring(depth, threads or 4, copy_streams)
     nb, off = plan.tensors()
     total = plan.arena_bytes + 2 * GUARD
     buf, can = _canary_buffer(total)
@@ -100,11 +100,12 @@ def test_stress_full(orc, mode):
     _load_arena(orc, synth.stress(), mode=mode)
 
 
-@pytest.mark.parametrize("depth", [1, 2, 3])
-def test_ring_depths_small_chunks(orc, depth):
+@pytest.mark.parametrize("depth,copy_streams", [(1, 1), (2, 1), (2, 2), (3, 1), (3, 2), (8, 2)])
+def test_ring_depths_small_chunks(orc, depth, copy_streams):
     """4 KiB chunks: hundreds of slot reuses per load."""
     t = synth.stress(n=3000, chunk=4096, dst_align=16)
-    _load_arena(orc, t, depth=depth, threads=2)
+    _load_arena(orc, t, depth=depth, threads=2, copy_streams=copy_streams)
+    _load_arena(orc, t, mode="pinned", depth=depth, threads=2, copy_streams=copy_streams)
 
 
 def test_separate_tensor_buffers(orc):
@@ -131,7 +132,7 @@ def test_back_to_back_loads_no_sync(orc):
     them: slot reuse carries across calls."""
     t = synth.stress(n=8000, chunk=1 << 16)
     plan = ii.ii_plan(t)
-    plan.set_ring(2, 2)
+    plan.set_ring(2, 2, 2)
     nb, off = plan.tensors()
     blob_a = synth.blob(t)
     blob_b = synth.blob(t.blob_bytes, seed=77)
