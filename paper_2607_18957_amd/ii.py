@@ -30,6 +30,15 @@ if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                       "(python -m paper_2607_18957_amd.build)")
 
+# One HIP runtime per process. PyTorch ships its own libamdhip64 and loads it
+# by a different name than the soname libii.so asks for; if libii.so were
+# loaded first, the process would end up with two runtimes and the second one
+# would see no device. Loading PyTorch first makes libii.so bind to its copy.
+try:
+    import torch  # noqa: F401
+except ImportError:
+    pass
+
 _lib = ctypes.CDLL(LIB_PATH)
 
 OK, EINVAL, EOVERFLOW, EOVERLAP, EALIGN, ENOMEM, EARENA, EBUSY, EHIP, ERANGE = range(10)

@@ -110,3 +110,20 @@ def test_null_arguments():
     lib.ii_load.argtypes = [ctypes.c_void_p] * 2 + [ctypes.c_uint64] + [ctypes.c_void_p] * 2
     assert lib.ii_load(None, None, 0, None, None) == ii.EINVAL
     assert "NULL" in ii.ii_last_error()
+
+
+def test_single_hip_runtime_in_process():
+    """Importing the binding first, before anything else touches HIP, must not
+    leave two different HIP runtimes (PyTorch's bundled one and the system
+    one) in the process: the second would see no device."""
+    import subprocess
+    import sys
+    code = ("import os\n"
+            "from paper_2607_18957_amd import ii\n"
+            "import torch\n"
+            "libs = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+            "print(len({os.path.realpath(p) for p in libs}))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip().splitlines()[-1] == "1", r.stdout
