@@ -344,6 +344,37 @@ def main() -> int:
     e2e["host_threads"] = int(os.environ.get("II_HOST_THREADS", min(8, os.cpu_count() or 1)))
     pinned.free()
 
+    # ---- what merging saves: the same loads through the naive per-tensor pipeline
+    merge = {}
+    for name in ("llama8b", "stress"):
+        t2 = table if name == "llama8b" else synth.stress()
+        p2 = plan if name == "llama8b" else ii.ii_plan(t2)
+        b2 = blob if name == "llama8b" else synth.blob(t2)
+        nb2, off2 = p2.tensors()
+        a2 = arena if name == "llama8b" else torch.empty(p2.arena_bytes, dtype=torch.uint8,
+                                                           device=dev)
+        d2 = a2.data_ptr() + off2
+        row = {"tensors": t2.n, "payload_bytes": p2.payload_bytes}
+        for label, fn in (("merged", ii.ii_load), ("per_tensor", ii.ii_load_pertensor)):
+            fn(p2, b2, d2, stream)
+            torch.cuda.synchronize(dev)
+            times = []
+            for _ in range(3):
+                t1 = time.perf_counter()
+                fn(p2, b2, d2, stream)
+                torch.cuda.synchronize(dev)
+                times.append(time.perf_counter() - t1)
+            tm = statistics.median(times)
+            row[label] = {"GBps": p2.payload_bytes / tm / 1e9, "tensors_per_s": t2.n / tm}
+        row["speedup"] = row["merged"]["GBps"] / row["per_tensor"]["GBps"]
+        merge[name] = row
+        log(f"{name}: merged {row['merged']['GBps']:.1f} GB/s, per-tensor "
+            f"{row['per_tensor']['GBps']:.1f} GB/s ({row['speedup']:.2f}x)")
+        if name != "llama8b":
+            del a2
+            p2.free()
+    e2e["merged_vs_per_tensor"] = merge
+
     cpu = cpu_baseline(table, blob)
     log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core")
 

@@ -168,6 +168,20 @@ int ii_load_device(ii_plan_t* plan, const void* dev_image, uint64_t image_bytes,
                    void* const* dst_ptrs, hipStream_t stream);
 
 /*
+ * ii_load_pertensor -- the same result as ii_load by the naive per-tensor
+ * pipeline of Sec. 4.2 ("Naive CFA Model"): one host-to-device copy per
+ * tensor (a tensor larger than chunk_bytes is copied in chunk_bytes pieces),
+ * in table order, straight into its destination; the host staging of tensor
+ * i+1 into the plan's pinned ring overlaps the copy of tensor i, and the
+ * copies run one after another on one copy stream ((T_i,InMem) ->
+ * (T_i+1,InDisk) and (T_i,InGPU) -> (T_i+1,InMem)). No scatter kernel runs.
+ * It exists to measure what merging saves; arguments, ordering, ownership
+ * and errors are exactly those of ii_load.
+ */
+int ii_load_pertensor(ii_plan_t* plan, const void* host_blob, uint64_t blob_bytes,
+                      void* const* dst_ptrs, hipStream_t stream);
+
+/*
  * ii_switch -- reuse a device arena that holds plan_old's tensors (at
  * plan_old's layout offsets) for plan_new's tensors (at plan_new's offsets),
  * following the model-switch dependency (Sec. 4.3): the new model's

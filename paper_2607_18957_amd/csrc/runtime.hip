@@ -502,9 +502,93 @@ static int run_device(ii_plan_t* p, const uint8_t* image, const uint64_t* dst, h
     return II_OK;
 }
 
+// The naive per-tensor pipeline of Sec. 4.2 ("Naive CFA Model"), kept as the
+// comparison path for the merged loader: tensors in table order, one
+// host-to-device copy per tensor (pieces of at most one slot for tensors
+// larger than a slot), two stages with one item in each -- the host copy of
+// tensor i+1 into the pinned ring overlaps the DMA of tensor i, and the DMAs
+// run back to back on one copy stream, straight into the destinations. A
+// slot is packed with consecutive pieces until full; it is refilled once the
+// copy stream has finished reading it. A pinned blob is copied tensor by
+// tensor without staging.
+static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
+                         hipStream_t stream) {
+    int rc = ensure_tables(p);
+    if (rc) return rc;
+    rc = ensure_ring(p);
+    if (rc) return rc;
+    Runtime* r = p->rt;
+    rc = check_dst(p, dst);
+    if (rc) return rc;
+    const bool pinned = is_pinned_host(blob);
+    hipStream_t cs = r->copy_s[0];
+    II_HIP(hipEventRecord(r->entry, stream));
+    II_HIP(hipStreamWaitEvent(cs, r->entry, 0));
+    const uint64_t C = p->chunk_bytes;
+    const uint32_t D = r->depth;
+    uint32_t slot = 0;
+    uint64_t used = 0;  // bytes of the current slot already packed
+    auto close_slot = [&]() -> int {
+        II_HIP(hipEventRecord(r->copy_done[slot], cs));
+        r->copy_rec[slot] = 1;
+        slot = (slot + 1) % D;
+        used = 0;
+        if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
+        return II_OK;
+    };
+    if (!pinned && r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
+    for (size_t i = 0; i < p->nbytes.size(); ++i) {
+        const uint64_t n = p->nbytes[i];
+        const uint8_t* src = blob + p->src_offset[i];
+        if (pinned) {
+            if (n) II_HIP(hipMemcpyAsync(reinterpret_cast<void*>(dst[i]), src, n,
+                                         hipMemcpyHostToDevice, cs));
+            continue;
+        }
+        for (uint64_t x = 0; x < n;) {
+            if (used == C) {
+                rc = close_slot();
+                if (rc) return rc;
+            }
+            const uint64_t len = std::min(n - x, C - used);
+            uint8_t* stage = r->hslot[slot] + used;
+            r->pool->copy(stage, src + x, len);
+            II_HIP(hipMemcpyAsync(reinterpret_cast<void*>(dst[i] + x), stage, len,
+                                  hipMemcpyHostToDevice, cs));
+            used += len;
+            x += len;
+        }
+    }
+    if (!pinned && used) {
+        II_HIP(hipEventRecord(r->copy_done[slot], cs));
+        r->copy_rec[slot] = 1;
+    }
+    II_HIP(hipEventRecord(r->done, cs));
+    II_HIP(hipStreamWaitEvent(stream, r->done, 0));
+    return II_OK;
+}
+
 }  // namespace ii
 
 using namespace ii;
+
+extern "C" int ii_load_pertensor(ii_plan_t* p, const void* host_blob, uint64_t blob_bytes,
+                                 void* const* dst_ptrs, hipStream_t stream) {
+    if (!p) return fail(II_EINVAL, "ii_load_pertensor: plan is NULL");
+    const size_t n = p->nbytes.size();
+    if (n && !dst_ptrs) return fail(II_EINVAL, "ii_load_pertensor: dst_ptrs is NULL");
+    if (p->num_chunks && !host_blob) return fail(II_EINVAL, "ii_load_pertensor: host_blob is NULL");
+    if (blob_bytes < p->hi)
+        return fail(II_ERANGE, "ii_load_pertensor: blob has %llu bytes, plan needs %llu",
+                    (unsigned long long)blob_bytes, (unsigned long long)p->hi);
+    if (p->num_chunks && is_device_ptr(host_blob))
+        return fail(II_EINVAL, "ii_load_pertensor: host_blob is device memory");
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_load_pertensor: plan in use");
+    int rc = run_pertensor(p, static_cast<const uint8_t*>(host_blob),
+                           reinterpret_cast<const uint64_t*>(dst_ptrs), stream);
+    return rc ? drain(p, stream, rc) : II_OK;
+}
 
 extern "C" int ii_load(ii_plan_t* p, const void* host_blob, uint64_t blob_bytes,
                        void* const* dst_ptrs, hipStream_t stream) {

@@ -61,6 +61,7 @@ _sig("ii_plan", _c.c_int, _vp, _sz, _u64, _P(_vp))
 _sig("ii_plan_free", None, _vp)
 _sig("ii_load", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_load_device", _c.c_int, _vp, _vp, _u64, _vp, _vp)
+_sig("ii_load_pertensor", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_switch", _c.c_int, _vp, _vp, _vp, _u64, _vp, _u64, _vp)
 _sig("ii_plan_set_ring", _c.c_int, _vp, _u32, _u32, _u32)
 _sig("ii_plan_release", _c.c_int, _vp)
@@ -320,6 +321,14 @@ def ii_load(plan: Plan, blob, dst_ptrs, stream=None) -> None:
     d = _ptrs(dst_ptrs)
     _check(_lib.ii_load(plan.handle, ptr or None, nbytes, d.ctypes.data if d.size else None,
                         _stream(stream)), "ii_load")
+
+
+def ii_load_pertensor(plan: Plan, blob, dst_ptrs, stream=None) -> None:
+    ptr, nbytes = _host(blob)
+    d = _ptrs(dst_ptrs)
+    _check(_lib.ii_load_pertensor(plan.handle, ptr or None, nbytes,
+                                  d.ctypes.data if d.size else None, _stream(stream)),
+           "ii_load_pertensor")
 
 
 def ii_load_device(plan: Plan, image, dst_ptrs, stream=None) -> None:

@@ -69,6 +69,12 @@ def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=N
     elif mode == "image":
         img = torch.from_numpy(blob).to(DEV)
         ii.ii_load_device(plan, img, base + off, s)
+    elif mode == "pertensor":
+        ii.ii_load_pertensor(plan, blob, base + off, s)
+    elif mode == "pertensor-pinned":
+        hb = ii.ii_host_alloc(blob.size)
+        hb.numpy()[:] = blob
+        ii.ii_load_pertensor(plan, hb, base + off, s)
     s.synchronize()
     got = buf.cpu().numpy()
     want = can.copy()
@@ -106,6 +112,15 @@ def test_ring_depths_small_chunks(orc, depth, copy_streams):
     t = synth.stress(n=3000, chunk=4096, dst_align=16)
     _load_arena(orc, t, depth=depth, threads=2, copy_streams=copy_streams)
     _load_arena(orc, t, mode="pinned", depth=depth, threads=2, copy_streams=copy_streams)
+
+
+@pytest.mark.parametrize("mode", ["pertensor", "pertensor-pinned"])
+def test_pertensor_path(orc, mode):
+    """The naive per-tensor pipeline gives the same bytes: tiny and stress
+    sets, and 4 KiB slots so that large tensors go in pieces."""
+    _load_arena(orc, synth.tiny(), mode=mode)
+    _load_arena(orc, synth.stress(n=20000), mode=mode)
+    _load_arena(orc, synth.tiny(chunk=4096, dst_align=1, header=3), mode=mode, depth=2, threads=2)
 
 
 def test_separate_tensor_buffers(orc):
