@@ -218,6 +218,22 @@ int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint6
 int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads,
                      uint32_t copy_streams);
 
+/*
+ * Pipeline timeline. With tracing on (ii_plan_set_trace(plan, 1) or
+ * $II_TRACE=1), every later ii_load / ii_switch on the plan records four
+ * timing events per chunk k: before and after its host-to-device copy (on
+ * the copy stream) and before and after its scatter (on the scatter stream).
+ * ii_plan_trace waits for the last traced load to finish and writes, for
+ * each chunk, the times in milliseconds since that load's first scatter-
+ * stream event into arrays of num_chunks entries (NULL skips one). The
+ * dependency edges can be read off them: copy_end[k] <= scatter_start[k] and
+ * scatter_end[k] <= copy_start[k + depth]. Errors: II_EINVAL (tracing off or
+ * no traced load), II_EBUSY, II_EHIP.
+ */
+int ii_plan_set_trace(ii_plan_t* plan, int on);
+int ii_plan_trace(ii_plan_t* plan, float* copy_start, float* copy_end, float* scatter_start,
+                  float* scatter_end);
+
 /* Free the plan's staging ring and device tables after waiting for its
  * outstanding work (the paper frees its I/O buffers as soon as loading
  * completes, Sec. 6.6). The plan stays valid; the next load reallocates. */

@@ -73,6 +73,7 @@ struct ii_plan_s {
     uint32_t ring_depth = 3;
     uint32_t host_threads = 8;
     uint32_t copy_streams = 2;
+    bool trace = false;
     // device state, created by the first load
     ii::Runtime* rt = nullptr;
     std::atomic<int> busy{0};

@@ -243,6 +243,7 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
 
     p->ring_depth = env_u32("II_RING_DEPTH", 3, 1, 8);
     p->copy_streams = std::min(p->ring_depth, env_u32("II_COPY_STREAMS", 2, 1, kMaxCopyStreams));
+    p->trace = env_u32("II_TRACE", 0, 0, 1) != 0;
     {
         long cores = sysconf(_SC_NPROCESSORS_ONLN);
         uint32_t dflt = (uint32_t)std::max(1L, std::min(8L, cores));

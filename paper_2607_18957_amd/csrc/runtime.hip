@@ -150,7 +150,22 @@ struct Runtime {
     uint32_t ncopy = 1;
     hipEvent_t entry = nullptr, done = nullptr;
     CopyPool* pool = nullptr;
+    // optional per-chunk timeline of the last ring load (timing events)
+    std::vector<hipEvent_t> tr_cs, tr_ce, tr_ss, tr_se;
+    hipEvent_t tr_t0 = nullptr;
+    size_t tr_chunks = 0;  // chunks recorded by the last traced load (0 = none)
 };
+
+static void free_trace(Runtime* r) {
+    for (auto* v : {&r->tr_cs, &r->tr_ce, &r->tr_ss, &r->tr_se}) {
+        for (auto e : *v)
+            if (e) (void)hipEventDestroy(e);
+        v->clear();
+    }
+    if (r->tr_t0) (void)hipEventDestroy(r->tr_t0);
+    r->tr_t0 = nullptr;
+    r->tr_chunks = 0;
+}
 
 // ---------------------------------------------------------------------------
 // state management
@@ -192,6 +207,7 @@ static void destroy(Runtime* r) {
     if (r->upload_done && r->uploaded) (void)hipEventSynchronize(r->upload_done);
     if (r->ranges_idle && r->ranges_used) (void)hipEventSynchronize(r->ranges_idle);
     free_ring(r);
+    free_trace(r);
     if (r->d_segs) (void)hipFree(r->d_segs);
     if (r->h_segs) (void)hipHostFree(r->h_segs);
     if (r->d_tiles) (void)hipFree(r->d_tiles);
@@ -278,6 +294,18 @@ static int ensure_ring(ii_plan_t* p) {
 #undef II_RING
     r->pool = new (std::nothrow) CopyPool(p->host_threads);
     if (!r->pool) return bail(fail(II_ENOMEM, "host copy pool allocation failed"));
+    return II_OK;
+}
+
+// Timing events for a traced load of K chunks.
+static int ensure_trace(Runtime* r, size_t K) {
+    if (r->tr_cs.size() >= K && r->tr_t0) return II_OK;
+    free_trace(r);
+    for (auto* v : {&r->tr_cs, &r->tr_ce, &r->tr_ss, &r->tr_se}) {
+        v->assign(K, nullptr);
+        for (auto& e : *v) II_HIP(hipEventCreate(&e));
+    }
+    II_HIP(hipEventCreate(&r->tr_t0));
     return II_OK;
 }
 
@@ -442,9 +470,16 @@ static int run_ring(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst, hipS
     Runtime* r = p->rt;
     const bool pinned = is_pinned_host(blob);
 
+    const bool trace = p->trace;
+    if (trace) {
+        rc = ensure_trace(r, p->num_chunks);
+        if (rc) return rc;
+        r->tr_chunks = 0;
+    }
     // entry edge: destination writes start after the caller's prior work
     II_HIP(hipEventRecord(r->entry, stream));
     II_HIP(hipStreamWaitEvent(r->scatter_s, r->entry, 0));
+    if (trace) II_HIP(hipEventRecord(r->tr_t0, r->scatter_s));
     rc = prepare_segments(p, dst, r->scatter_s, 0, 0);
     if (rc) return rc;
     if (scrub) {
@@ -467,16 +502,21 @@ static int run_ring(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst, hipS
         // InMem -> InGPU, once the device slot's previous scatter is done
         hipStream_t cs = r->copy_s[k % r->ncopy];
         if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(cs, r->scatter_done[slot], 0));
+        if (trace) II_HIP(hipEventRecord(r->tr_cs[k], cs));
         II_HIP(hipMemcpyAsync(r->dslot[slot], from, len, hipMemcpyHostToDevice, cs));
         II_HIP(hipEventRecord(r->copy_done[slot], cs));
+        if (trace) II_HIP(hipEventRecord(r->tr_ce[k], cs));
         r->copy_rec[slot] = 1;
         // InGPU -> tensors Loaded, then the slot is released
         II_HIP(hipStreamWaitEvent(r->scatter_s, r->copy_done[slot], 0));
+        if (trace) II_HIP(hipEventRecord(r->tr_ss[k], r->scatter_s));
         II_HIP(launch_scatter_slot(r->dslot[slot], k, r->d_segs, r->d_tiles, C, last_len, K,
                                    p->tiles_per_chunk, p->tile_bytes, r->scatter_s));
         II_HIP(hipEventRecord(r->scatter_done[slot], r->scatter_s));
+        if (trace) II_HIP(hipEventRecord(r->tr_se[k], r->scatter_s));
         r->scatter_rec[slot] = 1;
     }
+    if (trace) r->tr_chunks = K;
     II_HIP(hipEventRecord(r->tables_idle, r->scatter_s));
     r->tables_used = true;
     II_HIP(hipEventRecord(r->done, r->scatter_s));
@@ -695,6 +735,37 @@ extern "C" int ii_plan_set_ring(ii_plan_t* p, uint32_t depth, uint32_t host_thre
     p->ring_depth = depth;
     p->host_threads = host_threads;
     p->copy_streams = copy_streams;
+    return II_OK;
+}
+
+extern "C" int ii_plan_set_trace(ii_plan_t* p, int on) {
+    if (!p) return fail(II_EINVAL, "ii_plan_set_trace: plan is NULL");
+    p->trace = on != 0;
+    return II_OK;
+}
+
+extern "C" int ii_plan_trace(ii_plan_t* p, float* copy_start, float* copy_end,
+                             float* scatter_start, float* scatter_end) {
+    if (!p) return fail(II_EINVAL, "ii_plan_trace: plan is NULL");
+    Runtime* r = p->rt;
+    if (!r || !r->tr_chunks || r->tr_chunks != p->num_chunks)
+        return fail(II_EINVAL, "ii_plan_trace: no traced ring load on record");
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_plan_trace: plan in use");
+    const size_t K = r->tr_chunks;
+    II_HIP(hipEventSynchronize(r->tr_se[K - 1]));
+    for (size_t k = 0; k < K; ++k) {
+        const struct {
+            float* out;
+            hipEvent_t e;
+        } items[4] = {{copy_start, r->tr_cs[k]}, {copy_end, r->tr_ce[k]},
+                      {scatter_start, r->tr_ss[k]}, {scatter_end, r->tr_se[k]}};
+        for (const auto& it : items) {
+            if (!it.out) continue;
+            II_HIP(hipEventSynchronize(it.e));
+            II_HIP(hipEventElapsedTime(&it.out[k], r->tr_t0, it.e));
+        }
+    }
     return II_OK;
 }
 

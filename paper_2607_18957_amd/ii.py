@@ -65,6 +65,8 @@ _sig("ii_load_pertensor", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_switch", _c.c_int, _vp, _vp, _vp, _u64, _vp, _u64, _vp)
 _sig("ii_plan_set_ring", _c.c_int, _vp, _u32, _u32, _u32)
 _sig("ii_plan_release", _c.c_int, _vp)
+_sig("ii_plan_set_trace", _c.c_int, _vp, _c.c_int)
+_sig("ii_plan_trace", _c.c_int, _vp, _vp, _vp, _vp, _vp)
 for _n in ("ii_plan_num_tensors", "ii_plan_num_chunks", "ii_plan_num_segments"):
     _sig(_n, _sz, _vp)
 for _n in ("ii_plan_chunk_bytes", "ii_plan_payload_bytes", "ii_plan_arena_bytes"):
@@ -260,6 +262,19 @@ class Plan:
     def set_ring(self, depth: int, host_threads: int, copy_streams: int = 2) -> None:
         _check(_lib.ii_plan_set_ring(self.handle, depth, host_threads, min(copy_streams, depth)),
                "ii_plan_set_ring")
+
+    def set_trace(self, on: bool = True) -> None:
+        _check(_lib.ii_plan_set_trace(self.handle, int(bool(on))), "ii_plan_set_trace")
+
+    def trace(self) -> dict:
+        """Per-chunk stage times (ms) of the last traced ring load."""
+        k = self.num_chunks
+        out = {f: np.zeros(k, np.float32) for f in ("copy_start", "copy_end", "scatter_start",
+                                                    "scatter_end")}
+        _check(_lib.ii_plan_trace(self.handle, *(out[f].ctypes.data for f in
+                                                 ("copy_start", "copy_end", "scatter_start",
+                                                  "scatter_end"))), "ii_plan_trace")
+        return out
 
     def release(self) -> None:
         _check(_lib.ii_plan_release(self.handle), "ii_plan_release")

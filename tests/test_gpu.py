@@ -45,12 +45,13 @@ def _expect_arena(orc, table, blob, canary_slice):
 
 
 def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=None,
-                stream=None, chunk=None, copy_streams=2):
+                stream=None, chunk=None, copy_streams=2, plan=None):
     """Load `table` into a canary-filled arena (plan layout) and compare the
     whole buffer, guard bands included, with the oracle."""
-    plan = ii.ii_plan(table, chunk or table.chunk_bytes)
-    if depth:
-        plan.set_ring(depth, threads or 4, copy_streams)
+    if plan is None:
+        plan = ii.ii_plan(table, chunk or table.chunk_bytes)
+        if depth:
+            plan.set_ring(depth, threads or 4, copy_streams)
     nb, off = plan.tensors()
     total = plan.arena_bytes + 2 * GUARD
     buf, can = _canary_buffer(total)
@@ -121,6 +122,34 @@ def test_pertensor_path(orc, mode):
     _load_arena(orc, synth.tiny(), mode=mode)
     _load_arena(orc, synth.stress(n=20000), mode=mode)
     _load_arena(orc, synth.tiny(chunk=4096, dst_align=1, header=3), mode=mode, depth=2, threads=2)
+
+
+@pytest.mark.parametrize("depth,copy_streams", [(1, 1), (2, 1), (3, 1), (3, 2)])
+def test_pipeline_order_from_trace(orc, depth, copy_streams):
+    """The dependency edges of the chunk pipeline, read off GPU timestamps:
+    a chunk is scattered only after its copy ended (C_k,InGPU)->(T,Alloc); a
+    slot is refilled only after the scatter that read it ended (Destroyed
+    before reuse); scatters run in chunk order; with one copy stream the
+    copies also run one after another in chunk order ((C_k,InGPU) ->
+    (C_k+1,InMem)); and with two or more slots copies do overlap scatters."""
+    t = synth.stress(n=20000, chunk=1 << 18)
+    plan = ii.ii_plan(t)
+    plan.set_ring(depth, 4, copy_streams)
+    plan.set_trace(True)
+    _load_arena(orc, t, depth=depth, threads=4, copy_streams=copy_streams, plan=plan)
+    tr = plan.trace()
+    eps = 1e-3  # ms
+    cs, ce, ss, se = tr["copy_start"], tr["copy_end"], tr["scatter_start"], tr["scatter_end"]
+    K = plan.num_chunks
+    _say(f"depth {depth} copy streams {copy_streams}: {K} chunks in {se[-1]:.3f} ms")
+    assert (ce <= ss + eps).all()
+    assert (cs <= ce + eps).all() and (ss <= se + eps).all()
+    assert (se[:-1] <= ss[1:] + eps).all()
+    assert (se[:K - depth] <= cs[depth:] + eps).all()
+    if copy_streams == 1:
+        assert (ce[:-1] <= cs[1:] + eps).all()
+    if depth >= 2:
+        assert (cs[1:] < se[:-1] - eps).any()
 
 
 def test_separate_tensor_buffers(orc):
