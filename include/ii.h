@@ -23,7 +23,10 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include <hip/hip_runtime_api.h>
+/* The HIP stream handle, declared exactly as the HIP runtime declares it, so
+ * this header needs no ROCm include path; repeating the typedef alongside
+ * <hip/hip_runtime_api.h> is harmless. */
+typedef struct ihipStream_t* hipStream_t;
 
 #ifdef __cplusplus
 extern "C" {

@@ -12,7 +12,7 @@
 #include <cstdint>
 
 #if defined(__HIPCC__)
-#define II_HD __host__ __device__ __forceinline__
+#define II_HD __host__ __device__ inline __attribute__((always_inline))
 #else
 #define II_HD inline
 #endif

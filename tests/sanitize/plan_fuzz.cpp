@@ -1,0 +1,133 @@
+// Planner under AddressSanitizer + UndefinedBehaviorSanitizer (host only).
+//
+// Builds random tables -- including zero-size tensors, scalars, huge
+// extents that overflow, overlapping and touching ranges, every dtype and
+// alignment -- plans them with several chunk sizes, reads every getter and
+// checks the structural invariants that need no oracle: segments tile each
+// tensor exactly, lie inside their chunk, and are ordered; tile windows are
+// consistent. Any sanitizer report or failed check exits non-zero.
+#include <cstdint>
+#include <cstdio>
+#include <cstdlib>
+#include <vector>
+
+#include "ii.h"
+
+namespace ii {
+struct ii_unused;
+}
+struct ii_plan_s;
+namespace ii {
+void runtime_destroy(ii_plan_s*) {}  // no device state in a host-only build
+}
+
+static uint64_t rng_state = 88172645463325252ull;
+static uint64_t rnd() {  // xorshift64
+    rng_state ^= rng_state << 13;
+    rng_state ^= rng_state >> 7;
+    rng_state ^= rng_state << 17;
+    return rng_state;
+}
+static uint64_t pick(uint64_t n) { return rnd() % n; }
+
+#define CHECK(c)                                                         \
+    do {                                                                 \
+        if (!(c)) {                                                      \
+            fprintf(stderr, "check failed: %s (line %d)\n", #c, __LINE__); \
+            exit(2);                                                     \
+        }                                                                \
+    } while (0)
+
+int main(int argc, char** argv) {
+    const int iters = argc > 1 ? atoi(argv[1]) : 3000;
+    int ok_plans = 0, errors = 0;
+    for (int it = 0; it < iters; ++it) {
+        const size_t n = pick(40);
+        std::vector<std::vector<int64_t>> shapes(n);
+        std::vector<ii_tensor_desc> t(n);
+        uint64_t pos = pick(64);
+        for (size_t i = 0; i < n; ++i) {
+            const int nd = (int)pick(4);
+            for (int d = 0; d < nd; ++d) shapes[i].push_back(pick(10) ? (int64_t)pick(50) : 0);
+            t[i].name = (i % 3) ? "w" : nullptr;
+            t[i].dtype = 1 + (int32_t)pick(10);
+            t[i].ndim = (int32_t)shapes[i].size();
+            t[i].shape = shapes[i].empty() ? nullptr : shapes[i].data();
+            t[i].dst_align = 1ull << pick(13);
+            t[i].src_offset = pos;
+            static const uint64_t width[11] = {0, 1, 1, 1, 1, 2, 2, 4, 4, 8, 8};
+            uint64_t numel = 1;
+            for (int64_t x : shapes[i]) numel *= (uint64_t)x;
+            pos += numel * width[t[i].dtype] + (pick(3) ? 0 : pick(40));
+        }
+        // one table in four gets one bad row of a random kind
+        if (n && pick(4) == 0) {
+            const size_t i = pick(n);
+            switch (pick(7)) {
+            case 0: t[i].dtype = pick(2) ? 0 : 11; break;                   // unknown dtype
+            case 1: shapes[i].push_back(-1); break;                           // negative extent
+            case 2: shapes[i].push_back((int64_t)(1ull << 40));               // size overflows
+                    shapes[i].push_back((int64_t)(1ull << 40)); break;
+            case 3: t[i].dst_align = 3; break;                                // not a power of two
+            case 4: t[i].src_offset = ~0ull - pick(100); break;               // end overflows
+            case 5: if (i) t[i].src_offset = t[i - 1].src_offset; break;      // overlap (if non-empty)
+            case 6: t[i].ndim = -1; break;
+            }
+            t[i].shape = shapes[i].empty() ? nullptr : shapes[i].data();
+            if (t[i].ndim >= 0) t[i].ndim = (int32_t)shapes[i].size();
+        }
+        const uint64_t chunks[] = {16, 32, 48, 64, 4096, 1 << 16, 0, 17};
+        for (uint64_t C : chunks) {
+            ii_plan_t* p = nullptr;
+            int rc = ii_plan(t.data(), n, C, &p);
+            if (rc) {
+                CHECK(p == nullptr);
+                CHECK(ii_last_error()[0] != 0);
+                ++errors;
+                continue;
+            }
+            ++ok_plans;
+            const size_t N = ii_plan_num_tensors(p), K = ii_plan_num_chunks(p),
+                         S = ii_plan_num_segments(p);
+            CHECK(N == n);
+            std::vector<uint64_t> nb(N), off(N), cb(K), cl(K), sb(K + 1);
+            std::vector<uint32_t> sc(S), so(S), st(S), sl(S);
+            std::vector<uint64_t> sto(S);
+            CHECK(ii_plan_tensors(p, nb.data(), off.data()) == 0);
+            CHECK(ii_plan_chunks(p, cb.data(), cl.data(), sb.data()) == 0);
+            CHECK(ii_plan_segments(p, sc.data(), so.data(), st.data(), sto.data(), sl.data()) == 0);
+            uint32_t tb = 0, tpc = 0;
+            CHECK(ii_plan_tiles(p, &tb, &tpc, nullptr, nullptr) == 0);
+            std::vector<uint32_t> tf((size_t)K * tpc), tl((size_t)K * tpc);
+            CHECK(ii_plan_tiles(p, &tb, &tpc, tf.data(), tl.data()) == 0);
+            for (size_t i = 0; i < N; ++i) (void)ii_plan_tensor_name(p, i);
+            uint64_t lo, hi;
+            ii_plan_span(p, &lo, &hi);
+            // segments: inside their chunk, ordered, and tiling each tensor
+            std::vector<uint64_t> covered(N, 0);
+            uint64_t total = 0;
+            for (size_t s = 0; s < S; ++s) {
+                CHECK(sc[s] < K && st[s] < N && sl[s] > 0);
+                CHECK((uint64_t)so[s] + sl[s] <= cl[sc[s]]);
+                CHECK(cb[sc[s]] + so[s] == t[st[s]].src_offset + sto[s]);
+                CHECK(sto[s] == covered[st[s]]);  // source order = offset order within a tensor
+                covered[st[s]] += sl[s];
+                total += sl[s];
+                if (s && sc[s] == sc[s - 1]) CHECK(so[s] >= so[s - 1] + sl[s - 1]);
+                if (s) CHECK(sc[s] >= sc[s - 1]);
+            }
+            for (size_t i = 0; i < N; ++i) CHECK(covered[i] == nb[i]);
+            CHECK(total == ii_plan_payload_bytes(p));
+            for (size_t k = 0; k < K; ++k) {
+                CHECK(sb[k] <= sb[k + 1]);
+                for (uint32_t x = 0; x < tpc; ++x) {
+                    const size_t g = k * tpc + x;
+                    CHECK(tf[g] <= tl[g] && tl[g] <= S);
+                }
+            }
+            ii_plan_free(p);
+        }
+    }
+    printf("OK plans=%d rejected=%d\n", ok_plans, errors);
+    return 0;
+}
