@@ -109,6 +109,80 @@ def d2d_ceiling(torch, dev, nbytes: int = 4 << 30, reps: int = 10) -> dict:
     return {"GBps": 2 * nbytes / (ms * 1e-3) / 1e9, "bytes": nbytes, "median_ms": ms}
 
 
+def raw_direct_read(path: str, nbytes: int, threads: int = 8, block: int = 64 << 20) -> float:
+    """Parallel O_DIRECT read of the whole file into page-aligned buffers,
+    no device involved: a measure of the storage read rate the loader is
+    bound by (the better of two reader shapes is reported)."""
+    import mmap
+    import threading
+    fd = os.open(path, os.O_RDONLY | os.O_DIRECT)
+    bufs = [mmap.mmap(-1, block) for _ in range(threads)]
+    nblocks = (nbytes + block - 1) // block
+    nxt = [0]
+    lock = threading.Lock()
+
+    def work(i):
+        while True:
+            with lock:
+                b = nxt[0]
+                nxt[0] += 1
+            if b >= nblocks:
+                return
+            os.preadv(fd, [bufs[i]], b * block)
+
+    t0 = time.perf_counter()
+    ts = [threading.Thread(target=work, args=(i,)) for i in range(threads)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join()
+    dt = time.perf_counter() - t0
+    os.close(fd)
+    return nbytes / dt / 1e9
+
+
+def from_file(torch, dev, ii, plan, table, blob, dst, stream) -> dict:
+    """ii_load_file from the blob written to tmpfs (read through the page
+    cache) and to the local disk (read with O_DIRECT)."""
+    import tempfile
+    out = {}
+    payload = plan.payload_bytes
+    for label, root, direct in (("tmpfs", "/dev/shm", False),
+                                ("disk_direct", tempfile.gettempdir(), True)):
+        if not os.path.isdir(root):
+            continue
+        fd, path = tempfile.mkstemp(dir=root, prefix="ii_bench_")
+        try:
+            with os.fdopen(fd, "wb") as fh:
+                fh.write(memoryview(blob))
+                fh.flush()
+                os.fsync(fh.fileno())
+            rd = os.open(path, os.O_RDONLY | (os.O_DIRECT if direct else 0))
+            try:
+                times = []
+                for rep in range(3):
+                    t1 = time.perf_counter()
+                    ii.ii_load_file(plan, rd, dst, stream)
+                    torch.cuda.synchronize(dev)
+                    times.append(time.perf_counter() - t1)
+            finally:
+                os.close(rd)
+            t = statistics.median(times)
+            row = {"GBps": payload / t / 1e9, "tensors_per_s": table.n / t, "median_s": t,
+                   "runs": len(times)}
+            if direct:
+                raw = max(raw_direct_read(path, blob.size, 8, 64 << 20),
+                          raw_direct_read(path, blob.size, 16, 16 << 20))
+                row["raw_direct_read_GBps"] = raw
+                row["frac_of_raw_read"] = row["GBps"] / raw
+            out[label] = row
+            log(f"from file ({label}): {row['GBps']:.2f} GB/s"
+                + (f", raw O_DIRECT read {row['raw_direct_read_GBps']:.2f} GB/s" if direct else ""))
+        finally:
+            os.unlink(path)
+    return out
+
+
 def cpu_baseline(table, blob, budget_s: float = 12.0, max_passes: int = 4) -> dict:
     """The CPU oracle (sequential allocate-and-copy loader), pinned to one
     core, on the whole table; passes until the budget is used."""
@@ -343,6 +417,9 @@ def main() -> int:
     e2e["ring"] = {"depth": 3, "copy_streams": 2, "chunk_bytes": plan.chunk_bytes}
     e2e["host_threads"] = int(os.environ.get("II_HOST_THREADS", min(8, os.cpu_count() or 1)))
     pinned.free()
+
+    # ---- from a file: tmpfs (in-memory storage) and disk with O_DIRECT
+    e2e["from_file"] = from_file(torch, dev, ii, plan, table, blob, dst, stream)
 
     # ---- what merging saves: the same loads through the naive per-tensor pipeline
     merge = {}

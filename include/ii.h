@@ -43,7 +43,8 @@ enum {
     II_EARENA = 6,    /* the arena is smaller than the new plan's arena_bytes */
     II_EBUSY = 7,     /* the plan is in use by another call */
     II_EHIP = 8,      /* any other HIP runtime error (detail in ii_last_error) */
-    II_ERANGE = 9     /* the blob or image is shorter than the plan's span end */
+    II_ERANGE = 9,    /* the blob, image or file is shorter than the plan's span end */
+    II_EIO = 10       /* reading the model file failed (detail in ii_last_error) */
 };
 
 /* ---- element types (storage width in brackets) ---------------------------- */
@@ -152,6 +153,24 @@ void ii_plan_free(ii_plan_t* plan);
  */
 int ii_load(ii_plan_t* plan, const void* host_blob, uint64_t blob_bytes, void* const* dst_ptrs,
             hipStream_t stream);
+
+/*
+ * ii_load_file -- the same materialisation with the blob read from a file
+ * (the model file on storage or on tmpfs; Sec. 4.2 InDisk -> InMem, Sec. 5):
+ * the host threads read each chunk's bytes with pread straight into a pinned
+ * slot, then the copy and scatter steps run as in ii_load. If fd was opened
+ * with O_DIRECT, every read starts and ends on a 4096-byte boundary and
+ * bypasses the page cache; those reads land in a page-aligned host buffer
+ * (device-pinned pages cannot be targets of direct I/O) from which the host
+ * threads copy the chunk into the pinned slot.
+ *   fd          open for reading; file byte x is blob byte x. Read during the
+ *               call only; the call returns once every chunk has been read.
+ *   file_bytes  size of the file; must be >= the plan's span end hi.
+ *   dst_ptrs, stream   as for ii_load.
+ * Errors: as ii_load, plus II_EIO when a read fails or the file ends early.
+ */
+int ii_load_file(ii_plan_t* plan, int fd, uint64_t file_bytes, void* const* dst_ptrs,
+                 hipStream_t stream);
 
 /*
  * ii_load_device -- the same materialisation from a blob image that is

@@ -1,22 +1,28 @@
-// Host thread pool that splits one large memcpy between its threads: the
-// host stage of the load pipeline (pageable blob -> pinned staging slot).
-// Plain C++ so that it can be tested on its own under ThreadSanitizer.
+// Host thread pool that splits one large transfer between its threads: the
+// host stage of the load pipeline (pageable blob -> pinned staging slot, or
+// file -> pinned staging slot). Plain C++ so that it can be tested on its own
+// under ThreadSanitizer.
 #pragma once
 
+#include <unistd.h>
+
 #include <algorithm>
+#include <atomic>
+#include <cerrno>
 #include <condition_variable>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
+#include <functional>
 #include <mutex>
 #include <thread>
 #include <vector>
 
 namespace ii {
 
-// Fixed set of host threads that split one large memcpy between them.
 class CopyPool {
    public:
-    explicit CopyPool(uint32_t n) : n_(n) {
+    explicit CopyPool(uint32_t n) : n_(n ? n : 1) {
         for (uint32_t i = 1; i < n_; ++i) threads_.emplace_back([this, i] { worker(i); });
     }
     ~CopyPool() {
@@ -27,17 +33,58 @@ class CopyPool {
         cv_.notify_all();
         for (auto& t : threads_) t.join();
     }
+    CopyPool(const CopyPool&) = delete;
+    CopyPool& operator=(const CopyPool&) = delete;
+
     // Copy len bytes from src to dst using every thread of the pool.
     void copy(void* dst, const void* src, uint64_t len) {
+        uint8_t* d = static_cast<uint8_t*>(dst);
+        const uint8_t* s = static_cast<const uint8_t*>(src);
         if (n_ <= 1 || len < (4u << 20)) {
-            memcpy(dst, src, len);
+            if (len) memcpy(d, s, len);
             return;
         }
+        split(len, 4096, [d, s](uint64_t b, uint64_t e) { memcpy(d + (b), s + (b), e - b); });
+    }
+
+    // Read file bytes [off, off + len) of fd into dst using every thread of
+    // the pool; piece boundaries are multiples of `align` from off (so an
+    // aligned request stays aligned for direct I/O). Only the first `need`
+    // bytes must exist: a request rounded up past the end of the file may end
+    // early there. Returns 0, or the errno of the first failing read (EIO if
+    // the file ends before `need` bytes).
+    int read(int fd, void* dst, uint64_t off, uint64_t len, uint64_t align, uint64_t need) {
+        uint8_t* d = static_cast<uint8_t*>(dst);
+        std::atomic<int> err{0};
+        auto piece = [&](uint64_t b, uint64_t e) {
+            while (b < e && !err.load(std::memory_order_relaxed)) {
+                const ssize_t got = ::pread(fd, d + b, e - b, (off_t)(off + b));
+                if (got < 0) {
+                    if (errno == EINTR) continue;
+                    err.store(errno ? errno : EIO);
+                    return;
+                }
+                if (got == 0) {
+                    if (b < need) err.store(EIO);  // end of file before the needed bytes
+                    return;
+                }
+                b += (uint64_t)got;
+            }
+        };
+        if (n_ <= 1 || len < (4u << 20)) piece(0, len);
+        else split(len, std::max<uint64_t>(align, 4096), piece);
+        return err.load();
+    }
+
+   private:
+    // Run fn over [0, len) cut into one piece per thread, pieces aligned to
+    // `align`; the calling thread takes piece 0.
+    void split(uint64_t len, uint64_t align, const std::function<void(uint64_t, uint64_t)>& fn) {
         {
             std::lock_guard<std::mutex> g(m_);
-            dst_ = static_cast<uint8_t*>(dst);
-            src_ = static_cast<const uint8_t*>(src);
+            fn_ = &fn;
             len_ = len;
+            align_ = align;
             pending_ = n_ - 1;
             ++gen_;
         }
@@ -45,13 +92,12 @@ class CopyPool {
         part(0);
         std::unique_lock<std::mutex> l(m_);
         done_.wait(l, [this] { return pending_ == 0; });
+        fn_ = nullptr;
     }
-
-   private:
     void part(uint32_t i) {
-        const uint64_t per = ((len_ + n_ - 1) / n_ + 4095) & ~4095ull;
+        const uint64_t per = ((len_ + n_ - 1) / n_ + align_ - 1) / align_ * align_;
         const uint64_t b = std::min(len_, (uint64_t)i * per), e = std::min(len_, b + per);
-        if (e > b) memcpy(dst_ + b, src_ + b, e - b);
+        if (e > b) (*fn_)(b, e);
     }
     void worker(uint32_t i) {
         uint64_t seen = 0;
@@ -76,9 +122,123 @@ class CopyPool {
     bool stop_ = false;
     uint64_t gen_ = 0;
     uint32_t pending_ = 0;
-    uint8_t* dst_ = nullptr;
-    const uint8_t* src_ = nullptr;
-    uint64_t len_ = 0;
+    const std::function<void(uint64_t, uint64_t)>* fn_ = nullptr;
+    uint64_t len_ = 0, align_ = 4096;
+};
+
+}  // namespace ii
+
+namespace ii {
+
+// Read-ahead for direct-I/O files: R reader threads, each owning one
+// page-aligned buffer; thread j reads chunks j, j + R, j + 2R, ... in turn,
+// each as one block-aligned range, and refills its buffer as soon as the
+// consumer has released the chunk in it. The consumer takes chunks in order
+// with wait(k) / release(k). R whole-chunk reads stay in flight, which keeps a
+// storage device's queue full the way a plain parallel reader does.
+class ReadAhead {
+   public:
+    struct Range {
+        uint64_t begin, end, need;  // file bytes to read; bytes that must exist
+    };
+    ReadAhead(int fd, uint32_t nthreads, uint64_t buf_bytes, uint32_t nchunks,
+              std::function<Range(uint32_t)> range_of)
+        : fd_(fd), n_(nthreads ? nthreads : 1), nchunks_(nchunks), range_of_(std::move(range_of)) {
+        slots_.resize(n_);
+        for (uint32_t j = 0; j < n_; ++j) {
+            slots_[j].buf = static_cast<uint8_t*>(aligned_alloc(4096, (buf_bytes + 4095) & ~4095ull));
+            if (!slots_[j].buf) alloc_failed_ = true;
+        }
+        if (!alloc_failed_)
+            for (uint32_t j = 0; j < n_ && j < nchunks_; ++j)
+                threads_.emplace_back([this, j] { reader(j); });
+    }
+    ~ReadAhead() {
+        {
+            std::lock_guard<std::mutex> g(m_);
+            stop_ = true;
+        }
+        cv_.notify_all();
+        for (auto& t : threads_) t.join();
+        for (auto& s : slots_) free(s.buf);
+    }
+    ReadAhead(const ReadAhead&) = delete;
+    ReadAhead& operator=(const ReadAhead&) = delete;
+
+    bool ok() const { return !alloc_failed_; }
+
+    // Wait until chunk k is in memory; returns its buffer (file byte
+    // range_of(k).begin at offset 0), or nullptr with *err set.
+    const uint8_t* wait(uint32_t k, int* err) {
+        Slot& s = slots_[k % n_];
+        std::unique_lock<std::mutex> l(m_);
+        cv_.wait(l, [&] { return s.ready == (int64_t)k || s.err; });
+        if (s.err) {
+            *err = s.err;
+            return nullptr;
+        }
+        *err = 0;
+        return s.buf;
+    }
+    // The consumer is done with chunk k's buffer.
+    void release(uint32_t k) {
+        {
+            std::lock_guard<std::mutex> g(m_);
+            slots_[k % n_].released = (int64_t)k;
+        }
+        cv_.notify_all();
+    }
+
+   private:
+    struct Slot {
+        uint8_t* buf = nullptr;
+        int64_t ready = -1;     // chunk whose bytes the buffer holds
+        int64_t released = -1;  // last chunk the consumer gave back
+        int err = 0;
+    };
+    void reader(uint32_t j) {
+        Slot& s = slots_[j];
+        for (uint64_t k = j; k < nchunks_; k += n_) {
+            if (k >= n_) {  // the buffer still holds chunk k - n_ until it is released
+                std::unique_lock<std::mutex> l(m_);
+                cv_.wait(l, [&] { return stop_ || s.released == (int64_t)(k - n_); });
+                if (stop_) return;
+            }
+            const Range r = range_of_((uint32_t)k);
+            int e = 0;
+            uint64_t b = 0;
+            while (b < r.end - r.begin) {
+                const ssize_t got =
+                    ::pread(fd_, s.buf + b, r.end - r.begin - b, (off_t)(r.begin + b));
+                if (got < 0) {
+                    if (errno == EINTR) continue;
+                    e = errno ? errno : EIO;
+                    break;
+                }
+                if (got == 0) {
+                    if (b < r.need) e = EIO;
+                    break;
+                }
+                b += (uint64_t)got;
+            }
+            {
+                std::lock_guard<std::mutex> g(m_);
+                if (e) s.err = e;
+                else s.ready = (int64_t)k;
+            }
+            cv_.notify_all();
+            if (e) return;
+        }
+    }
+    int fd_;
+    uint32_t n_, nchunks_;
+    std::function<Range(uint32_t)> range_of_;
+    std::vector<Slot> slots_;
+    std::vector<std::thread> threads_;
+    std::mutex m_;
+    std::condition_variable cv_;
+    bool stop_ = false;
+    bool alloc_failed_ = false;
 };
 
 }  // namespace ii

@@ -37,6 +37,7 @@ struct RangeDev {
 
 constexpr uint32_t kDefaultTile = 8u << 10;  // bytes of chunk per workgroup (<= kMaxTile)
 constexpr uint32_t kMaxCopyStreams = 2;       // host-to-device copy streams of a ring
+constexpr uint64_t kIoAlign = 4096;           // block alignment of direct-I/O file reads
 
 struct Runtime;  // device-side state (runtime.hip)
 

@@ -332,7 +332,8 @@ extern "C" const char* ii_strerror(int status) {
     case II_EARENA: return "arena too small";
     case II_EBUSY: return "plan in use by another call";
     case II_EHIP: return "HIP runtime error";
-    case II_ERANGE: return "blob or image shorter than the plan's span";
+    case II_ERANGE: return "blob, image or file shorter than the plan's span";
+    case II_EIO: return "reading the model file failed";
     default: return "unknown status";
     }
 }

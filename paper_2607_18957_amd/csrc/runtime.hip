@@ -23,7 +23,11 @@
 // on it like any other stream work.
 #include <hip/hip_runtime.h>
 
+#include <fcntl.h>
+
 #include <algorithm>
+#include <cerrno>
+#include <memory>
 #include <cstring>
 #include <vector>
 
@@ -390,14 +394,26 @@ struct BusyGuard {
 // ---------------------------------------------------------------------------
 // the pipeline
 
-static int run_ring(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst, hipStream_t stream,
+// Where the chunk bytes come from: a host blob (pageable: copied into the
+// pinned slot by the host threads; pinned: copied by DMA straight from it) or
+// a file (read into the pinned slot by the host threads; with O_DIRECT the
+// reads start and end on kIoAlign boundaries and the chunk sits `shift`
+// bytes into the slot).
+struct Source {
+    const uint8_t* blob = nullptr;
+    int fd = -1;
+    bool direct = false;
+};
+
+static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStream_t stream,
                     const std::vector<RangeDev>* scrub) {
     int rc = ensure_tables(p);
     if (rc) return rc;
     rc = ensure_ring(p);
     if (rc) return rc;
     Runtime* r = p->rt;
-    const bool pinned = is_pinned_host(blob);
+    const uint8_t* blob = src.blob;
+    const bool pinned = src.fd < 0 && is_pinned_host(blob);
 
     const bool trace = p->trace;
     if (trace) {
@@ -418,15 +434,53 @@ static int run_ring(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst, hipS
 
     const uint32_t D = r->depth, K = (uint32_t)p->num_chunks;
     const uint64_t C = p->chunk_bytes, last_len = K ? p->chunk_len(K - 1) : 0;
+    std::unique_ptr<ReadAhead> ahead;
+    if (src.fd >= 0 && src.direct && K) {
+        const uint64_t lo = p->lo;
+        try {
+            ahead.reset(new ReadAhead(
+            src.fd, std::min<uint32_t>(p->host_threads, 8), C + 2 * kIoAlign, K,
+            [p, lo, C](uint32_t k) {
+                const uint64_t at = lo + (uint64_t)k * C, len = p->chunk_len(k);
+                const uint64_t a = at & ~(kIoAlign - 1);
+                const uint64_t e = (at + len + kIoAlign - 1) & ~(kIoAlign - 1);
+                return ReadAhead::Range{a, e, at + len - a};
+            }));
+        } catch (const std::exception&) {
+            return fail(II_ENOMEM, "read-ahead threads could not be started");
+        }
+        if (!ahead->ok()) return fail(II_ENOMEM, "read-ahead buffer allocation failed");
+    }
     for (uint32_t k = 0; k < K; ++k) {
         const uint32_t slot = k % D;
         const uint64_t len = p->chunk_len(k);
-        const uint8_t* from = blob + p->lo + (uint64_t)k * C;
+        const uint64_t at = p->lo + (uint64_t)k * C;  // blob / file offset of the chunk
+        const uint8_t* from = blob ? blob + at : nullptr;
         if (!pinned) {
             // InDisk -> InMem: the pinned slot is free once its last copy finished
             if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
-            r->pool->copy(r->hslot[slot], from, len);
-            from = r->hslot[slot];
+            if (src.fd < 0) {
+                r->pool->copy(r->hslot[slot], from, len);
+                from = r->hslot[slot];
+            } else if (!src.direct) {
+                const int err = r->pool->read(src.fd, r->hslot[slot], at, len, 1, len);
+                if (err)
+                    return fail(II_EIO, "reading chunk %u (file bytes %llu..%llu): %s", k,
+                                (unsigned long long)at, (unsigned long long)(at + len),
+                                strerror(err));
+                from = r->hslot[slot];
+            } else {
+                // direct I/O: whole blocks, read ahead into aligned buffers;
+                // the chunk's bytes are then copied into the pinned slot
+                int err = 0;
+                const uint8_t* b = ahead->wait(k, &err);
+                if (!b)
+                    return fail(II_EIO, "reading chunk %u (file bytes from %llu): %s", k,
+                                (unsigned long long)(at & ~(kIoAlign - 1)), strerror(err));
+                r->pool->copy(r->hslot[slot], b + (at & (kIoAlign - 1)), len);
+                ahead->release(k);
+                from = r->hslot[slot];
+            }
         }
         // InMem -> InGPU, once the device slot's previous scatter is done
         hipStream_t cs = r->copy_s[k % r->ncopy];
@@ -572,8 +626,31 @@ extern "C" int ii_load(ii_plan_t* p, const void* host_blob, uint64_t blob_bytes,
         return fail(II_EINVAL, "ii_load: host_blob is device memory (use ii_load_device)");
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_load: plan in use");
-    int rc = run_ring(p, static_cast<const uint8_t*>(host_blob),
-                      reinterpret_cast<const uint64_t*>(dst_ptrs), stream, nullptr);
+    Source src;
+    src.blob = static_cast<const uint8_t*>(host_blob);
+    int rc = run_ring(p, src, reinterpret_cast<const uint64_t*>(dst_ptrs), stream, nullptr);
+    return rc ? drain(p, stream, rc) : II_OK;
+}
+
+extern "C" int ii_load_file(ii_plan_t* p, int fd, uint64_t file_bytes, void* const* dst_ptrs,
+                            hipStream_t stream) {
+    if (!p) return fail(II_EINVAL, "ii_load_file: plan is NULL");
+    const size_t n = p->nbytes.size();
+    if (n && !dst_ptrs) return fail(II_EINVAL, "ii_load_file: dst_ptrs is NULL");
+    if (p->num_chunks && fd < 0) return fail(II_EINVAL, "ii_load_file: bad file descriptor");
+    if (file_bytes < p->hi)
+        return fail(II_ERANGE, "ii_load_file: file has %llu bytes, plan needs %llu",
+                    (unsigned long long)file_bytes, (unsigned long long)p->hi);
+    Source src;
+    src.fd = fd;
+    if (p->num_chunks) {
+        const int fl = fcntl(fd, F_GETFL);
+        if (fl < 0) return fail(II_EINVAL, "ii_load_file: fcntl: %s", strerror(errno));
+        src.direct = (fl & O_DIRECT) != 0;
+    }
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_load_file: plan in use");
+    int rc = run_ring(p, src, reinterpret_cast<const uint64_t*>(dst_ptrs), stream, nullptr);
     return rc ? drain(p, stream, rc) : II_OK;
 }
 
@@ -649,7 +726,9 @@ extern "C" int ii_switch(const ii_plan_t* po, ii_plan_t* pn, void* arena, uint64
     std::vector<uint64_t> dst(pn->nbytes.size());
     for (size_t i = 0; i < dst.size(); ++i) dst[i] = a + pn->dst_offset[i];
     std::vector<RangeDev> scrub = scrub_ranges(po, pn, a);
-    int rc = run_ring(pn, static_cast<const uint8_t*>(host_blob_new), dst.data(), stream, &scrub);
+    Source src;
+    src.blob = static_cast<const uint8_t*>(host_blob_new);
+    int rc = run_ring(pn, src, dst.data(), stream, &scrub);
     return rc ? drain(pn, stream, rc) : II_OK;
 }
 

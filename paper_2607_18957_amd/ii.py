@@ -41,9 +41,10 @@ except ImportError:
 
 _lib = ctypes.CDLL(LIB_PATH)
 
-OK, EINVAL, EOVERFLOW, EOVERLAP, EALIGN, ENOMEM, EARENA, EBUSY, EHIP, ERANGE = range(10)
+OK, EINVAL, EOVERFLOW, EOVERLAP, EALIGN, ENOMEM, EARENA, EBUSY, EHIP, ERANGE, EIO = range(11)
 ERRNAMES = {0: "II_OK", 1: "II_EINVAL", 2: "II_EOVERFLOW", 3: "II_EOVERLAP", 4: "II_EALIGN",
-            5: "II_ENOMEM", 6: "II_EARENA", 7: "II_EBUSY", 8: "II_EHIP", 9: "II_ERANGE"}
+            5: "II_ENOMEM", 6: "II_EARENA", 7: "II_EBUSY", 8: "II_EHIP", 9: "II_ERANGE",
+            10: "II_EIO"}
 
 _c = ctypes
 _vp, _sz, _u32, _u64, _i32 = _c.c_void_p, _c.c_size_t, _c.c_uint32, _c.c_uint64, _c.c_int32
@@ -62,6 +63,7 @@ _sig("ii_plan_free", None, _vp)
 _sig("ii_load", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_load_device", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_load_pertensor", _c.c_int, _vp, _vp, _u64, _vp, _vp)
+_sig("ii_load_file", _c.c_int, _vp, _c.c_int, _u64, _vp, _vp)
 _sig("ii_switch", _c.c_int, _vp, _vp, _vp, _u64, _vp, _u64, _vp)
 _sig("ii_plan_set_ring", _c.c_int, _vp, _u32, _u32, _u32)
 _sig("ii_plan_release", _c.c_int, _vp)
@@ -344,6 +346,15 @@ def ii_load_pertensor(plan: Plan, blob, dst_ptrs, stream=None) -> None:
     _check(_lib.ii_load_pertensor(plan.handle, ptr or None, nbytes,
                                   d.ctypes.data if d.size else None, _stream(stream)),
            "ii_load_pertensor")
+
+
+def ii_load_file(plan: Plan, fd: int, dst_ptrs, stream=None, file_bytes: int | None = None) -> None:
+    """Load from an open file descriptor (file byte x = blob byte x)."""
+    if file_bytes is None:
+        file_bytes = os.fstat(fd).st_size
+    d = _ptrs(dst_ptrs)
+    _check(_lib.ii_load_file(plan.handle, fd, file_bytes, d.ctypes.data if d.size else None,
+                             _stream(stream)), "ii_load_file")
 
 
 def ii_load_device(plan: Plan, image, dst_ptrs, stream=None) -> None:

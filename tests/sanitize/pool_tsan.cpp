@@ -4,7 +4,9 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <unistd.h>
 #include <vector>
+#include <algorithm>
 
 #include "copy_pool.h"
 
@@ -31,6 +33,77 @@ int main() {
                 }
             }
     }
+    // file reads: whole, unaligned, past the end of the file (allowed beyond
+    // `need`), and an early end (EIO)
+    char path[] = "/tmp/ii_pool_tsanXXXXXX";
+    const int fd = mkstemp(path);
+    if (fd < 0) return 3;
+    const uint64_t fsz = (9u << 20) + 123;
+    if (write(fd, src.data(), fsz) != (ssize_t)fsz) return 3;
+    for (uint32_t threads : {1u, 3u, 8u}) {
+        ii::CopyPool pool(threads);
+        struct Case { uint64_t off, len, need; int want; } cases[] = {
+            {0, fsz, fsz, 0}, {4096, 8u << 20, 8u << 20, 0}, {17, (5u << 20) + 5, (5u << 20) + 5, 0},
+            {8u << 20, 2u << 20, fsz - (8u << 20), 0}, {8u << 20, 2u << 20, 2u << 20, EIO}};
+        for (const Case& c : cases) {
+            std::fill(dst.begin(), dst.end(), 0xEE);
+            const int err = pool.read(fd, dst.data(), c.off, c.len, 4096, c.need);
+            if (err != c.want) {
+                fprintf(stderr, "read(%llu, %llu): err %d, want %d\n", (unsigned long long)c.off,
+                        (unsigned long long)c.len, err, c.want);
+                return 2;
+            }
+            const uint64_t have = std::min(c.len, fsz - c.off);
+            if (!err && memcmp(dst.data(), src.data() + c.off, have) != 0) {
+                fprintf(stderr, "read mismatch off=%llu\n", (unsigned long long)c.off);
+                return 2;
+            }
+        }
+    }
+    // read-ahead: all chunks in order (several thread counts), stopping
+    // halfway, and a file that ends early
+    const uint64_t C = 1u << 20;
+    const uint32_t K = (uint32_t)((fsz + C - 1) / C);
+    auto range = [&](uint32_t k) {
+        const uint64_t at = (uint64_t)k * C, len = std::min(C, fsz - at);
+        return ii::ReadAhead::Range{at, at + len, len};
+    };
+    for (uint32_t threads : {1u, 2u, 5u, 8u}) {
+        for (int stop_early = 0; stop_early < 2; ++stop_early) {
+            ii::ReadAhead ra(fd, threads, C, K, range);
+            if (!ra.ok()) return 3;
+            for (uint32_t k = 0; k < K; ++k) {
+                if (stop_early && k == K / 2) break;
+                int err = 0;
+                const uint8_t* b = ra.wait(k, &err);
+                const uint64_t len = std::min(C, fsz - (uint64_t)k * C);
+                if (!b || err || memcmp(b, src.data() + (uint64_t)k * C, len) != 0) {
+                    fprintf(stderr, "read-ahead chunk %u wrong (threads %u)\n", k, threads);
+                    return 2;
+                }
+                ra.release(k);
+            }
+        }
+    }
+    {
+        auto past = [&](uint32_t k) {  // asks for one chunk more than the file has
+            const uint64_t at = (uint64_t)k * C;
+            return ii::ReadAhead::Range{at, at + C, C};
+        };
+        ii::ReadAhead ra(fd, 3, C, K + 1, past);
+        int err = 0;
+        for (uint32_t k = 0; k <= K; ++k) {
+            const uint8_t* b = ra.wait(k, &err);
+            if (!b) break;
+            ra.release(k);
+        }
+        if (err != EIO) {
+            fprintf(stderr, "read-ahead past the end: err %d, want EIO\n", err);
+            return 2;
+        }
+    }
+    close(fd);
+    unlink(path);
     printf("OK\n");
     return 0;
 }

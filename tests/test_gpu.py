@@ -152,6 +152,55 @@ def test_pipeline_order_from_trace(orc, depth, copy_streams):
         assert (cs[1:] < se[:-1] - eps).any()
 
 
+def _file_modes():
+    import tempfile
+    return [("tmpfs", "/dev/shm", False), ("disk-direct", tempfile.gettempdir(), True),
+            ("disk-buffered", tempfile.gettempdir(), False)]
+
+
+@pytest.mark.parametrize("where,root,direct", _file_modes(), ids=[m[0] for m in _file_modes()])
+def test_load_from_file(orc, where, root, direct):
+    """The blob read from a file (storage stage): tmpfs, and a disk file read
+    through the page cache and with O_DIRECT, including spans that start off
+    a block boundary and chunks that are not a multiple of the block size."""
+    import tempfile
+    if not os.path.isdir(root):
+        pytest.skip(f"{root} missing")
+    cases = [synth.tiny(header=1000), synth.tiny(chunk=65552, header=4099, dst_align=1),
+             synth.stress(n=30000, chunk=1 << 20)]
+    for t in cases:
+        blob = synth.blob(t)
+        fd, path = tempfile.mkstemp(dir=root)
+        os.close(fd)
+        try:
+            blob.tofile(path)
+            flags = os.O_RDONLY | (os.O_DIRECT if direct else 0)
+            fd = os.open(path, flags)
+            try:
+                plan = ii.ii_plan(t)
+                nb, off = plan.tensors()
+                buf, can = _canary_buffer(plan.arena_bytes + 2 * GUARD)
+                base = buf.data_ptr() + GUARD
+                ii.ii_load_file(plan, fd, base + off)
+                torch.cuda.synchronize()
+                want = can.copy()
+                orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob,
+                          want[GUARD:GUARD + plan.arena_bytes])
+                assert np.array_equal(buf.cpu().numpy(), want), (where, t.name)
+                # a file that ends before the span does: an I/O error, plan still usable
+                with pytest.raises(ii.IIError) as e:
+                    plan2 = ii.ii_plan(t)
+                    short = os.open(path, os.O_RDONLY)
+                    os.truncate(path, blob.size // 2)
+                    ii.ii_load_file(plan2, short, base + off, file_bytes=blob.size)
+                os.close(short)
+                assert e.value.name == "II_EIO"
+            finally:
+                os.close(fd)
+        finally:
+            os.unlink(path)
+
+
 def test_separate_tensor_buffers(orc):
     """Destinations are independent allocations, not an arena."""
     for table in (synth.tiny(), synth.stress(n=5000)):
