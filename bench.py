@@ -421,6 +421,30 @@ def main() -> int:
     # ---- from a file: tmpfs (in-memory storage) and disk with O_DIRECT
     e2e["from_file"] = from_file(torch, dev, ii, plan, table, blob, dst, stream)
 
+    # ---- model switch: the 8B arena reused for the Mistral-7B-shaped set
+    new_t = synth.mistral7b()
+    new_plan = ii.ii_plan(new_t)
+    new_blob = synth.blob(new_t)
+    sw_times = []
+    for rep in range(4):
+        ii.ii_load(plan, blob, dst, stream)  # the arena holds the old set again
+        torch.cuda.synchronize(dev)
+        t1 = time.perf_counter()
+        ii.ii_switch(plan, new_plan, arena, plan.arena_bytes, new_blob, stream)
+        torch.cuda.synchronize(dev)
+        if rep:
+            sw_times.append(time.perf_counter() - t1)
+    tsw = statistics.median(sw_times)
+    e2e["switch"] = {"from": table.name, "to": new_t.name,
+                     "new_payload_bytes": new_plan.payload_bytes,
+                     "scrubbed_bytes": plan.arena_bytes - new_plan.arena_bytes,
+                     "GBps": new_plan.payload_bytes / tsw / 1e9, "median_s": tsw,
+                     "frac_of_h2d_peak": new_plan.payload_bytes / tsw / 1e9 / h2d["GBps"]}
+    log(f"switch {table.name} -> {new_t.name}: {e2e['switch']['GBps']:.2f} GB/s "
+        f"({100 * e2e['switch']['frac_of_h2d_peak']:.1f}% of H2D peak)")
+    del new_blob
+    new_plan.free()
+
     # ---- what merging saves: the same loads through the naive per-tensor pipeline
     merge = {}
     for name in ("llama8b", "stress"):
