@@ -20,6 +20,8 @@ Reported beside it, never as value:
                 the 8 TB/s HBM peak; traffic from rocprofv3 counters when a
                 profile of the current kernel source is on record;
   cpu_baseline  the CPU oracle (one core) on the same table.
+With --compare-per-tensor it also times the naive per-tensor pipeline
+(ii_load_pertensor) against the merged loader on the 8B and stress sets.
 """
 from __future__ import annotations
 
@@ -183,6 +185,41 @@ def from_file(torch, dev, ii, plan, table, blob, dst, stream) -> dict:
     return out
 
 
+def merged_vs_per_tensor(torch, dev, ii, synth, table, plan, blob, arena, dst, stream) -> dict:
+    """The same host-blob loads through ii_load and through the naive
+    per-tensor pipeline (ii_load_pertensor), on the 8B and stress sets: what
+    merging saves. Opt-in (--compare-per-tensor)."""
+    merge = {}
+    for name in ("llama8b", "stress"):
+        t2 = table if name == "llama8b" else synth.stress()
+        p2 = plan if name == "llama8b" else ii.ii_plan(t2)
+        b2 = blob if name == "llama8b" else synth.blob(t2)
+        nb2, off2 = p2.tensors()
+        a2 = arena if name == "llama8b" else torch.empty(p2.arena_bytes, dtype=torch.uint8,
+                                                           device=dev)
+        d2 = a2.data_ptr() + off2
+        row = {"tensors": t2.n, "payload_bytes": p2.payload_bytes}
+        for label, fn in (("merged", ii.ii_load), ("per_tensor", ii.ii_load_pertensor)):
+            fn(p2, b2, d2, stream)
+            torch.cuda.synchronize(dev)
+            times = []
+            for _ in range(3):
+                t1 = time.perf_counter()
+                fn(p2, b2, d2, stream)
+                torch.cuda.synchronize(dev)
+                times.append(time.perf_counter() - t1)
+            tm = statistics.median(times)
+            row[label] = {"GBps": p2.payload_bytes / tm / 1e9, "tensors_per_s": t2.n / tm}
+        row["speedup"] = row["merged"]["GBps"] / row["per_tensor"]["GBps"]
+        merge[name] = row
+        log(f"{name}: merged {row['merged']['GBps']:.1f} GB/s, per-tensor "
+            f"{row['per_tensor']['GBps']:.1f} GB/s ({row['speedup']:.2f}x)")
+        if name != "llama8b":
+            del a2
+            p2.free()
+    return merge
+
+
 def cpu_baseline(table, blob, budget_s: float = 12.0, max_passes: int = 4) -> dict:
     """The CPU oracle (sequential allocate-and-copy loader), pinned to one
     core, on the whole table; passes until the budget is used."""
@@ -317,6 +354,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--e2e-reps", type=int, default=5)
+    ap.add_argument("--compare-per-tensor", action="store_true",
+                    help="also time the naive per-tensor pipeline on the 8B and stress sets")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -445,36 +484,9 @@ def main() -> int:
     del new_blob
     new_plan.free()
 
-    # ---- what merging saves: the same loads through the naive per-tensor pipeline
-    merge = {}
-    for name in ("llama8b", "stress"):
-        t2 = table if name == "llama8b" else synth.stress()
-        p2 = plan if name == "llama8b" else ii.ii_plan(t2)
-        b2 = blob if name == "llama8b" else synth.blob(t2)
-        nb2, off2 = p2.tensors()
-        a2 = arena if name == "llama8b" else torch.empty(p2.arena_bytes, dtype=torch.uint8,
-                                                           device=dev)
-        d2 = a2.data_ptr() + off2
-        row = {"tensors": t2.n, "payload_bytes": p2.payload_bytes}
-        for label, fn in (("merged", ii.ii_load), ("per_tensor", ii.ii_load_pertensor)):
-            fn(p2, b2, d2, stream)
-            torch.cuda.synchronize(dev)
-            times = []
-            for _ in range(3):
-                t1 = time.perf_counter()
-                fn(p2, b2, d2, stream)
-                torch.cuda.synchronize(dev)
-                times.append(time.perf_counter() - t1)
-            tm = statistics.median(times)
-            row[label] = {"GBps": p2.payload_bytes / tm / 1e9, "tensors_per_s": t2.n / tm}
-        row["speedup"] = row["merged"]["GBps"] / row["per_tensor"]["GBps"]
-        merge[name] = row
-        log(f"{name}: merged {row['merged']['GBps']:.1f} GB/s, per-tensor "
-            f"{row['per_tensor']['GBps']:.1f} GB/s ({row['speedup']:.2f}x)")
-        if name != "llama8b":
-            del a2
-            p2.free()
-    e2e["merged_vs_per_tensor"] = merge
+    if args.compare_per_tensor:
+        e2e["merged_vs_per_tensor"] = merged_vs_per_tensor(torch, dev, ii, synth, table, plan,
+                                                           blob, arena, dst, stream)
 
     cpu = cpu_baseline(table, blob)
     log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core")
