@@ -88,6 +88,49 @@ def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=N
     return plan
 
 
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_llama70b_full_sampled(orc):
+    """The Llama-70B-shaped set at full size: 141 GB blob, 256 MiB chunks,
+    141 GB of destinations in HBM. The blob is pageable host memory staged
+    through the pinned ring (a single 141 GB pinned allocation exceeds what
+    the host lets one process pin). The oracle cannot hold a second copy, so
+    it runs on a sub-table (24 whole tensors, every kind and both ends of the
+    file) and every other tensor is checked in random 4 KiB windows plus its
+    first and last bytes."""
+    import time
+    t = synth.llama70b()
+    plan = ii.ii_plan(t)
+    nb, off = plan.tensors()
+    assert plan.payload_bytes == 141_107_412_992 and plan.num_chunks == 526
+    _say("llama70b: blob")
+    blob = np.empty(t.blob_bytes, np.uint8)
+    synth.fill(blob.ctypes.data, 0, t.blob_bytes, t.seed, threads=16)
+    arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=DEV)
+    _say("llama70b: load")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ii.ii_load(plan, blob, arena.data_ptr() + off)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    _say(f"llama70b: {plan.payload_bytes / dt / 1e9:.1f} GB/s end to end (pageable, first load)")
+    rng = np.random.default_rng(70)
+    whole = sorted(set([0, 1, 2, 3, 4, 5, 6, 7, 8, 9, t.n - 3, t.n - 2, t.n - 1] +
+                       list(rng.choice(t.n, size=11, replace=False))))
+    outs = orc.load(orc.nbytes(t)[whole], t.src_offset[whole], blob)
+    for i, o in zip(whole, outs):
+        got = arena[int(off[i]):int(off[i]) + o.size].cpu().numpy()
+        assert np.array_equal(got, o), f"tensor {i} ({t.names[i]})"
+    for i in range(t.n):
+        n, s, d = int(nb[i]), int(t.src_offset[i]), int(off[i])
+        for j in [0, max(0, n - 4096)] + [int(x) for x in rng.integers(0, max(1, n - 4096), 2)]:
+            m = min(4096, n - j)
+            got = arena[d + j:d + j + m].cpu().numpy()
+            assert np.array_equal(got, blob[s + j:s + j + m]), (i, j)
+    _say(f"llama70b: {len(whole)} whole tensors and {t.n} sampled tensors bit-exact")
+    del arena
+
+
 @pytest.mark.parametrize("mode", ["pageable", "pinned", "image"])
 def test_tiny(orc, mode):
     _load_arena(orc, synth.tiny(), mode=mode)
@@ -419,46 +462,3 @@ def test_switch_llama8b_to_mistral7b(orc):
                blob_n, before)
     assert np.array_equal(got, before)
     assert (got[pn.arena_bytes:] == 0).all()
-
-
-@pytest.mark.slow
-@pytest.mark.timeout(900)
-def test_llama70b_full_sampled(orc):
-    """The Llama-70B-shaped set at full size: 141 GB blob, 256 MiB chunks,
-    141 GB of destinations in HBM. The blob is pageable host memory staged
-    through the pinned ring (a single 141 GB pinned allocation exceeds what
-    the host lets one process pin). The oracle cannot hold a second copy, so
-    it runs on a sub-table (24 whole tensors, every kind and both ends of the
-    file) and every other tensor is checked in random 4 KiB windows plus its
-    first and last bytes."""
-    import time
-    t = synth.llama70b()
-    plan = ii.ii_plan(t)
-    nb, off = plan.tensors()
-    assert plan.payload_bytes == 141_107_412_992 and plan.num_chunks == 526
-    _say("llama70b: blob")
-    blob = np.empty(t.blob_bytes, np.uint8)
-    synth.fill(blob.ctypes.data, 0, t.blob_bytes, t.seed, threads=16)
-    arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=DEV)
-    _say("llama70b: load")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ii.ii_load(plan, blob, arena.data_ptr() + off)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    _say(f"llama70b: {plan.payload_bytes / dt / 1e9:.1f} GB/s end to end (pageable, first load)")
-    rng = np.random.default_rng(70)
-    whole = sorted(set([0, 1, 2, 3, 4, 5, 6, 7, 8, 9, t.n - 3, t.n - 2, t.n - 1] +
-                       list(rng.choice(t.n, size=11, replace=False))))
-    outs = orc.load(orc.nbytes(t)[whole], t.src_offset[whole], blob)
-    for i, o in zip(whole, outs):
-        got = arena[int(off[i]):int(off[i]) + o.size].cpu().numpy()
-        assert np.array_equal(got, o), f"tensor {i} ({t.names[i]})"
-    for i in range(t.n):
-        n, s, d = int(nb[i]), int(t.src_offset[i]), int(off[i])
-        for j in [0, max(0, n - 4096)] + [int(x) for x in rng.integers(0, max(1, n - 4096), 2)]:
-            m = min(4096, n - j)
-            got = arena[d + j:d + j + m].cpu().numpy()
-            assert np.array_equal(got, blob[s + j:s + j + m]), (i, j)
-    _say(f"llama70b: {len(whole)} whole tensors and {t.n} sampled tensors bit-exact")
-    del arena
