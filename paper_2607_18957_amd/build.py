@@ -20,6 +20,7 @@ ARCH = os.environ.get("II_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wall",
+    "-Wl,-soname,libii.so",
     # packed fp32 instructions are disabled for all device code built here
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
