@@ -76,8 +76,22 @@ class Oracle:
                                   ctypes.c_uint64]
         lib.orc_switch.argtypes = [_sz, _u64p, _u64p, _sz, _u64p, _u64p, _u64p, _vp,
                                    ctypes.c_uint64, _vp, ctypes.c_uint64]
+        lib.orc_rows.argtypes = [_sz, _i32p, _vp, _i64p, _u64p, _u64p, _u64p]
+        lib.orc_check_rows.argtypes = [_sz, _u64p, _u64p, _u64p, _u64p, _u64p]
+        lib.orc_span_rows.argtypes = [_sz, _u64p, _u64p, _u64p, _u64p,
+                                      ctypes.POINTER(ctypes.c_uint64),
+                                      ctypes.POINTER(ctypes.c_uint64)]
+        lib.orc_span_rows.restype = None
+        lib.orc_plan_rows.argtypes = [_sz, _u64p, _u64p, _u64p, _u64p, ctypes.c_uint64,
+                                      ctypes.POINTER(_sz), ctypes.POINTER(_sz),
+                                      _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+        lib.orc_load_rows_into.argtypes = [_sz, _u64p, _u64p, _u64p, _u64p, _vp, ctypes.c_uint64,
+                                           _vp]
+        lib.orc_arena_rows.argtypes = [_sz, _u64p, _u64p, _u64p, _u64p, _u64p, _vp,
+                                       ctypes.c_uint64, _vp, ctypes.c_uint64]
         for f in ("orc_sizes", "orc_check", "orc_layout", "orc_plan", "orc_load_into",
-                  "orc_load_alloc", "orc_arena", "orc_switch"):
+                  "orc_load_alloc", "orc_arena", "orc_switch", "orc_rows", "orc_check_rows",
+                  "orc_plan_rows", "orc_load_rows_into", "orc_arena_rows"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
         self.path = so_path
@@ -179,6 +193,73 @@ class Oracle:
                                  arena.ctypes.data, arena.size)
         if rc:
             raise OracleError(rc, "switch")
+
+
+    # -- tables given as rows (tensor-parallel shards) ---------------------
+    def rows(self, table, nbytes=None) -> np.ndarray:
+        """Rows per tensor of a table with src_row_stride (0 = contiguous)."""
+        nb = self.nbytes(table) if nbytes is None else _u64(nbytes)
+        flat, start = table.shape_flat()
+        flat = np.ascontiguousarray(flat, dtype=np.int64)
+        out = np.zeros(table.n, dtype=np.uint64)
+        rc = self.lib.orc_rows(table.n, np.ascontiguousarray(table.ndim(), np.int32),
+                               flat.ctypes.data if flat.size else None,
+                               np.ascontiguousarray(start, np.int64),
+                               _u64(table.src_row_stride), nb, out)
+        if rc:
+            raise OracleError(rc, "rows")
+        return out
+
+    def check_rows(self, nbytes, src_offset, rows, stride, dst_align) -> int:
+        return self.lib.orc_check_rows(len(nbytes), _u64(nbytes), _u64(src_offset), _u64(rows),
+                                       _u64(stride), _u64(dst_align))
+
+    def span_rows(self, nbytes, src_offset, rows, stride) -> tuple[int, int]:
+        lo, hi = ctypes.c_uint64(0), ctypes.c_uint64(0)
+        self.lib.orc_span_rows(len(nbytes), _u64(nbytes), _u64(src_offset), _u64(rows),
+                               _u64(stride), ctypes.byref(lo), ctypes.byref(hi))
+        return int(lo.value), int(hi.value)
+
+    def plan_rows(self, nbytes, src_offset, rows, stride, chunk_bytes: int) -> dict:
+        a = (_u64(nbytes), _u64(src_offset), _u64(rows), _u64(stride))
+        K, S = _sz(0), _sz(0)
+        rc = self.lib.orc_plan_rows(len(a[0]), *a, chunk_bytes, ctypes.byref(K), ctypes.byref(S),
+                                    None, None, None, None, None, None, None)
+        if rc:
+            raise OracleError(rc, "plan_rows")
+        k, s = K.value, S.value
+        out = dict(chunk_begin=np.zeros(k, np.uint64), chunk_len=np.zeros(k, np.uint64),
+                   seg_chunk=np.zeros(s, np.uint32), seg_chunk_off=np.zeros(s, np.uint64),
+                   seg_tensor=np.zeros(s, np.uint32), seg_tensor_off=np.zeros(s, np.uint64),
+                   seg_len=np.zeros(s, np.uint64))
+        p = lambda x: x.ctypes.data if x.size else None  # noqa: E731
+        rc = self.lib.orc_plan_rows(len(a[0]), *a, chunk_bytes, ctypes.byref(K), ctypes.byref(S),
+                                    p(out["chunk_begin"]), p(out["chunk_len"]),
+                                    p(out["seg_chunk"]), p(out["seg_chunk_off"]),
+                                    p(out["seg_tensor"]), p(out["seg_tensor_off"]),
+                                    p(out["seg_len"]))
+        if rc:
+            raise OracleError(rc, "plan_rows")
+        return out
+
+    def load_rows(self, nbytes, src_offset, rows, stride, blob: np.ndarray) -> list:
+        nb = _u64(nbytes)
+        outs = [np.empty(int(x), dtype=np.uint8) for x in nb]
+        ptrs = (ctypes.c_void_p * max(1, len(nb)))(*[o.ctypes.data for o in outs])
+        rc = self.lib.orc_load_rows_into(len(nb), nb, _u64(src_offset), _u64(rows), _u64(stride),
+                                         blob.ctypes.data, blob.size,
+                                         ctypes.cast(ptrs, ctypes.c_void_p))
+        if rc:
+            raise OracleError(rc, "load_rows")
+        return outs
+
+    def arena_rows(self, nbytes, src_offset, rows, stride, dst_align, blob: np.ndarray,
+                   arena: np.ndarray) -> None:
+        rc = self.lib.orc_arena_rows(len(nbytes), _u64(nbytes), _u64(src_offset), _u64(rows),
+                                     _u64(stride), _u64(dst_align), blob.ctypes.data, blob.size,
+                                     arena.ctypes.data, arena.size)
+        if rc:
+            raise OracleError(rc, "arena_rows")
 
 
 def _u64(a) -> np.ndarray:

@@ -30,6 +30,15 @@
  *     tensor are zeroed, new-tensor bytes hold the new model's bytes and all
  *     other bytes are untouched. -> orc_switch.
  *
+ *   - Tensor-parallel shards. A rank's shard of a weight sharded along its
+ *     inner dimension is not contiguous in the model file: each of its
+ *     shape[0] rows is a run of row bytes at a fixed stride (the paper notes
+ *     that tensor parallelism fragments transfers, Sec. 2.2). The *_rows
+ *     functions below take, per tensor, a row count and a source stride; a
+ *     contiguous tensor is one row. The result is tensor i's rows, in order,
+ *     back to back. -> orc_rows, orc_check_rows, orc_span_rows,
+ *     orc_plan_rows, orc_load_rows_into, orc_arena_rows.
+ *
  * Readings where the paper is silent (also listed in the design notes):
  *   R1 chunk windows start at lo = min source offset over non-empty tensors
  *      and end at hi = max source end; bytes outside [lo, hi) are never read;
@@ -381,4 +390,203 @@ int orc_switch(size_t n_old, const uint64_t* nbytes_old, const uint64_t* dst_ali
         return rc;
     return orc_arena(n_new, nbytes_new, src_new, dst_align_new, blob_new, blob_len, arena,
                      arena_len);
+}
+
+/* ---- tensors given as rows (tensor-parallel shards) ------------------- */
+
+/* Rows of each tensor: 0 if it is empty; 1 if its stride is 0 (contiguous);
+ * otherwise shape[0] rows of nbytes / shape[0] bytes each, which needs
+ * ndim >= 1. */
+int orc_rows(size_t n, const int32_t* ndim, const int64_t* shape_flat, const int64_t* shape_start,
+             const uint64_t* stride, const uint64_t* nbytes, uint64_t* rows)
+{
+    for (size_t i = 0; i < n; ++i) {
+        if (nbytes[i] == 0) {
+            rows[i] = 0;
+        } else if (stride[i] == 0) {
+            rows[i] = 1;
+        } else {
+            if (ndim[i] < 1)
+                return ORC_EINVAL;
+            rows[i] = (uint64_t)shape_flat[shape_start[i]];
+        }
+    }
+    return ORC_OK;
+}
+
+/* bytes per row, and the stride actually used (a single row has no stride) */
+static uint64_t row_bytes(const uint64_t* nbytes, const uint64_t* rows, size_t i)
+{
+    return rows[i] ? nbytes[i] / rows[i] : 0;
+}
+
+/* Validity: every row fits in 64 bits, rows of one tensor do not overlap
+ * each other (stride >= row bytes), and no byte belongs to two rows of any
+ * tensors. */
+int orc_check_rows(size_t n, const uint64_t* nbytes, const uint64_t* src_offset,
+                   const uint64_t* rows, const uint64_t* stride, const uint64_t* dst_align)
+{
+    size_t total = 0;
+    for (size_t i = 0; i < n; ++i) {
+        if (!is_pow2(dst_align[i]))
+            return ORC_EINVAL;
+        if (rows[i] > 1 && stride[i] < row_bytes(nbytes, rows, i))
+            return ORC_EINVAL;
+        if (rows[i]) {
+            uint64_t rb = row_bytes(nbytes, rows, i);
+            if (rows[i] > 1 && stride[i] > (UINT64_MAX - src_offset[i]) / (rows[i] - 1))
+                return ORC_EOVERFLOW;
+            uint64_t last = src_offset[i] + (rows[i] > 1 ? (rows[i] - 1) * stride[i] : 0);
+            if (rb > UINT64_MAX - last)
+                return ORC_EOVERFLOW;
+        }
+        total += (size_t)rows[i];
+    }
+    orc_range* r = (orc_range*)malloc((total ? total : 1) * sizeof(orc_range));
+    if (!r)
+        return ORC_EINVAL;
+    size_t m = 0;
+    for (size_t i = 0; i < n; ++i)
+        for (uint64_t q = 0; q < rows[i]; ++q) {
+            r[m].begin = src_offset[i] + q * stride[i];
+            r[m].end = r[m].begin + row_bytes(nbytes, rows, i);
+            ++m;
+        }
+    qsort(r, m, sizeof(orc_range), cmp_range);
+    int rc = ORC_OK;
+    for (size_t j = 1; j < m; ++j)
+        if (r[j].begin < r[j - 1].end)
+            rc = ORC_EOVERLAP;
+    free(r);
+    return rc;
+}
+
+/* R1 for rows: from the first byte of any row to the end of the last. */
+void orc_span_rows(size_t n, const uint64_t* nbytes, const uint64_t* src_offset,
+                   const uint64_t* rows, const uint64_t* stride, uint64_t* lo, uint64_t* hi)
+{
+    uint64_t l = UINT64_MAX, h = 0;
+    for (size_t i = 0; i < n; ++i)
+        for (uint64_t q = 0; q < rows[i]; ++q) {
+            uint64_t b = src_offset[i] + q * stride[i];
+            uint64_t e = b + row_bytes(nbytes, rows, i);
+            if (b < l)
+                l = b;
+            if (e > h)
+                h = e;
+        }
+    if (h == 0)
+        l = 0;
+    *lo = l;
+    *hi = h;
+}
+
+/* orc_plan for rows: every row of every tensor cut at chunk boundaries; a
+ * piece's offset in its tensor is (row index x row bytes) + its offset in the
+ * row. Same two-call protocol as orc_plan. */
+int orc_plan_rows(size_t n, const uint64_t* nbytes, const uint64_t* src_offset,
+                  const uint64_t* rows, const uint64_t* stride, uint64_t chunk_bytes,
+                  size_t* num_chunks, size_t* num_segments, uint64_t* chunk_begin,
+                  uint64_t* chunk_len, uint32_t* seg_chunk, uint64_t* seg_chunk_off,
+                  uint32_t* seg_tensor, uint64_t* seg_tensor_off, uint64_t* seg_len)
+{
+    if (chunk_bytes == 0)
+        return ORC_EINVAL;
+    uint64_t lo, hi;
+    orc_span_rows(n, nbytes, src_offset, rows, stride, &lo, &hi);
+    size_t K = 0;
+    for (uint64_t b = lo; b < hi; b += chunk_bytes) {
+        if (chunk_begin) {
+            chunk_begin[K] = b;
+            chunk_len[K] = (hi - b < chunk_bytes) ? hi - b : chunk_bytes;
+        }
+        ++K;
+        if (b > UINT64_MAX - chunk_bytes)
+            break;
+    }
+    *num_chunks = K;
+    size_t total = 0;
+    for (size_t i = 0; i < n; ++i)
+        total += (size_t)rows[i];
+    orc_seg* tmp = (orc_seg*)malloc((total ? total : 1) * sizeof(orc_seg));
+    if (!tmp)
+        return ORC_EINVAL;
+    size_t S = 0;
+    for (size_t k = 0; k < K; ++k) {
+        uint64_t cb = lo + (uint64_t)k * chunk_bytes;
+        uint64_t ce = (hi - cb < chunk_bytes) ? hi : cb + chunk_bytes;
+        size_t m = 0;
+        for (size_t i = 0; i < n; ++i) {
+            uint64_t rb = row_bytes(nbytes, rows, i);
+            for (uint64_t q = 0; q < rows[i]; ++q) {
+                uint64_t rs = src_offset[i] + q * stride[i], re = rs + rb;
+                uint64_t b = rs > cb ? rs : cb;
+                uint64_t e = re < ce ? re : ce;
+                if (b < e) {
+                    tmp[m].chunk_off = b - cb;
+                    tmp[m].tensor_off = q * rb + (b - rs);
+                    tmp[m].tensor = (uint32_t)i;
+                    tmp[m].len = e - b;
+                    ++m;
+                }
+            }
+        }
+        qsort(tmp, m, sizeof(orc_seg), cmp_seg);
+        for (size_t j = 0; j < m; ++j, ++S) {
+            if (seg_chunk) {
+                seg_chunk[S] = (uint32_t)k;
+                seg_chunk_off[S] = tmp[j].chunk_off;
+                seg_tensor[S] = tmp[j].tensor;
+                seg_tensor_off[S] = tmp[j].tensor_off;
+                seg_len[S] = tmp[j].len;
+            }
+        }
+    }
+    free(tmp);
+    *num_segments = S;
+    return ORC_OK;
+}
+
+/* The sequential loader for rows: tensor by tensor, row by row, each row
+ * appended to the tensor's buffer. */
+int orc_load_rows_into(size_t n, const uint64_t* nbytes, const uint64_t* src_offset,
+                       const uint64_t* rows, const uint64_t* stride, const uint8_t* blob,
+                       uint64_t blob_len, uint8_t* const* out)
+{
+    for (size_t i = 0; i < n; ++i) {
+        uint64_t rb = row_bytes(nbytes, rows, i);
+        for (uint64_t q = 0; q < rows[i]; ++q) {
+            uint64_t s = src_offset[i] + q * stride[i];
+            if (s > blob_len || rb > blob_len - s)
+                return ORC_ERANGE;
+            memcpy(out[i] + q * rb, blob + s, rb);
+        }
+    }
+    return ORC_OK;
+}
+
+/* Expected arena after a load of a table given as rows (layout R4). */
+int orc_arena_rows(size_t n, const uint64_t* nbytes, const uint64_t* src_offset,
+                   const uint64_t* rows, const uint64_t* stride, const uint64_t* dst_align,
+                   const uint8_t* blob, uint64_t blob_len, uint8_t* arena, uint64_t arena_len)
+{
+    uint64_t* off = (uint64_t*)malloc((n ? n : 1) * sizeof(uint64_t));
+    uint8_t** out = (uint8_t**)malloc((n ? n : 1) * sizeof(uint8_t*));
+    if (!off || !out) {
+        free(off);
+        free(out);
+        return ORC_EINVAL;
+    }
+    uint64_t need;
+    int rc = orc_layout(n, nbytes, dst_align, off, &need);
+    if (rc == ORC_OK && need > arena_len)
+        rc = ORC_ERANGE;
+    if (rc == ORC_OK) {
+        for (size_t i = 0; i < n; ++i)
+            out[i] = arena + off[i];
+        rc = orc_load_rows_into(n, nbytes, src_offset, rows, stride, blob, blob_len, out);
+    }
+    free(off);
+    free(out);
+    return rc;
 }

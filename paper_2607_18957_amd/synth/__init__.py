@@ -56,6 +56,13 @@ class Table:
     seed: int
     chunk_bytes: int
     meta: dict = field(default_factory=dict)
+    # per tensor: 0 = contiguous; else the source distance between the starts
+    # of consecutive rows (shape[0] rows of nbytes / shape[0] bytes each)
+    src_row_stride: np.ndarray = None
+
+    def __post_init__(self):
+        if self.src_row_stride is None:
+            self.src_row_stride = np.zeros(len(self.names), dtype=np.uint64)
 
     @property
     def n(self) -> int:
@@ -119,6 +126,51 @@ def transformer(setname: str, layers: int, hidden: int, ffn: int, kv: int, vocab
                    setname, meta=dict(layers=layers, hidden=hidden, ffn=ffn, kv=kv, vocab=vocab))
 
 
+def transformer_tp(setname: str, layers: int, hidden: int, ffn: int, kv: int, vocab: int,
+                   rank: int, size: int, *, dtype: str = "bf16", seed: int = 0,
+                   chunk: int = 64 * MiB, dst_align: int = 256) -> Table:
+    """One tensor-parallel rank's table over the full model file of
+    transformer(...): the file (and so the blob) is the unsharded model,
+    packed in table order; the table lists only rank `rank` of `size`'s
+    shards (Megatron-style). Column-parallel weights (q, k, v, gate, up) and
+    the vocab-sharded embed and lm_head take a contiguous block of rows; the
+    row-parallel weights (o, down) take a block of columns, i.e. every row
+    contributes a run of in/size elements at a stride of one full row; norms
+    are replicated."""
+    full = transformer(setname, layers, hidden, ffn, kv, vocab, dtype=dtype, seed=seed,
+                       chunk=chunk, dst_align=dst_align)
+    w = DTYPE_WIDTH[dtype]
+    names, shapes, src, stride = [], [], [], []
+    for name, shp, off in zip(full.names, full.shapes, full.src_offset.tolist()):
+        kind = name.rsplit(".", 1)[-1]
+        if len(shp) == 1:                                   # norms: whole
+            names.append(name), shapes.append(shp), src.append(off), stride.append(0)
+        elif kind in ("o", "down"):                          # column block, strided rows
+            out, inn = shp
+            assert inn % size == 0
+            part = inn // size
+            names.append(f"{name}@{rank}/{size}")
+            shapes.append((out, part))
+            src.append(off + rank * part * w)
+            stride.append(inn * w)
+        else:                                                # row block, contiguous
+            out, inn = shp
+            assert out % size == 0
+            part = out // size
+            names.append(f"{name}@{rank}/{size}")
+            shapes.append((part, inn))
+            src.append(off + rank * part * inn * w)
+            stride.append(0)
+    n = len(names)
+    return Table(name=f"{setname}-tp{rank}of{size}", names=names,
+                 dtype=np.full(n, DTYPE_CODES[dtype], dtype=np.int32), shapes=shapes,
+                 src_offset=np.array(src, dtype=np.uint64),
+                 dst_align=np.full(n, dst_align, dtype=np.uint64), blob_bytes=full.blob_bytes,
+                 seed=seed, chunk_bytes=chunk,
+                 meta=dict(full.meta, tp_rank=rank, tp_size=size, full=full),
+                 src_row_stride=np.array(stride, dtype=np.uint64))
+
+
 def tiny(**kw) -> Table:
     """4 layers, hidden 256, FFN 1024, 4 heads (kv 256), vocab 8192; 39 bf16 tensors."""
     kw.setdefault("seed", 0)
@@ -172,6 +224,18 @@ def stress(n: int = 100_000, *, rng_seed: int = 2, seed: int = 2, chunk: int = 1
 
 SETS = {"tiny": tiny, "llama8b": llama8b, "stress": stress, "llama70b": llama70b,
         "mistral7b": mistral7b}
+
+
+def tiny_tp(rank: int, size: int, **kw) -> Table:
+    kw.setdefault("seed", 0)
+    kw.setdefault("chunk", 4 * MiB)
+    return transformer_tp("tiny", 4, 256, 1024, 256, 8192, rank, size, **kw)
+
+
+def llama8b_tp(rank: int, size: int, **kw) -> Table:
+    kw.setdefault("seed", 1)
+    kw.setdefault("chunk", 64 * MiB)
+    return transformer_tp("llama8b", 32, 4096, 14336, 1024, 128256, rank, size, **kw)
 
 
 # ---------------------------------------------------------------------------

@@ -24,7 +24,14 @@ What pins what (InstantInfer, arXiv 2607.18957):
                           blob (Theorem 2: the result equals the sequential
                           program's; a dense same-order table is one copy);
   * switch             -- degenerate cases that reduce to a plain load, to
-                          no change, or to pure clearing (Sec. 4.3 reading).
+                          no change, or to pure clearing (Sec. 4.3 reading);
+  * tables given as rows (tensor-parallel shards, Sec. 2.2 / Sec. 6.1) --
+                          stride 0 and stride = row bytes reproduce the
+                          contiguous results; each shard equals numpy's own
+                          2-D slice of the unsharded tensor; segments derived
+                          byte by byte from numpy's strided view of the
+                          source; closed-form chunk and piece counts; the
+                          validity rules on hand-made cases.
 """
 from __future__ import annotations
 
@@ -421,8 +428,248 @@ def pin_empty(orc):
         assert orc.span(sizes, [5] * len(sizes)) == (0, 0)
 
 
+# -- tables given as rows -----------------------------------------------------
+
+def _merge_runs(tuples):
+    """Join segments that continue each other (same chunk and tensor, next
+    chunk offset and next tensor offset)."""
+    out = []
+    for k, co, i, to, n in tuples:
+        if out and out[-1][0] == k and out[-1][2] == i and out[-1][1] + out[-1][4] == co \
+                and out[-1][3] + out[-1][4] == to:
+            out[-1][4] += n
+        else:
+            out.append([k, co, i, to, n])
+    return [tuple(x) for x in out]
+
+
+def pin_rows_contiguous(orc):
+    """stride 0 (one row) and stride = row bytes (rows back to back) give the
+    contiguous table's chunks, segments (up to joins at row ends), load and
+    arena."""
+    rng = random.Random(5)
+    for sizes, src, C in _random_tables(rng, 60):
+        n = len(sizes)
+        align = [1 << rng.randint(0, 9) for _ in range(n)]
+        rows1 = [1 if s else 0 for s in sizes]
+        assert orc.check_rows(sizes, src, rows1, [0] * n, align) == orc.check(sizes, src, align)
+        if orc.check(sizes, src, align):
+            continue
+        a, b = orc.plan(sizes, src, C), orc.plan_rows(sizes, src, rows1, [0] * n, C)
+        assert _plan_tuples(a) == _plan_tuples(b)
+        assert np.array_equal(a["chunk_begin"], b["chunk_begin"])
+        assert np.array_equal(a["chunk_len"], b["chunk_len"])
+        # the same bytes cut into rows of 1, 2, 4 ... bytes laid back to back
+        rows = [rng.choice([d for d in (1, 2, 4, s) if s % d == 0]) if s else 0 for s in sizes]
+        stride = [s // r if r else 0 for s, r in zip(sizes, rows)]
+        assert orc.span_rows(sizes, src, rows, stride) == orc.span(sizes, src)
+        c = orc.plan_rows(sizes, src, rows, stride, C)
+        assert _merge_runs(_plan_tuples(c)) == _plan_tuples(a), (sizes, src, rows, C)
+        blob = np.frombuffer(rng.randbytes(max([src[i] + sizes[i] for i in range(n)] + [0]) + 3),
+                             dtype=np.uint8).copy()
+        want = orc.load(sizes, src, blob)
+        got = orc.load_rows(sizes, src, rows, stride, blob)
+        assert all(np.array_equal(x, y) for x, y in zip(want, got))
+        _, ab = orc.layout(sizes, align)
+        x, y = np.full(ab, 7, np.uint8), np.full(ab, 7, np.uint8)
+        orc.arena(sizes, src, align, blob, x)
+        orc.arena_rows(sizes, src, rows, stride, align, blob, y)
+        assert np.array_equal(x, y)
+
+
+def _shard_view(full2d: np.ndarray, full_shape, shard_shape, rank: int, width: int):
+    """numpy's own slice of an [out, in] tensor (as bytes, [out, in*width])
+    for a shard of the given shape."""
+    if len(full_shape) == 1:
+        return full2d
+    if shard_shape[1] == full_shape[1]:                 # block of rows
+        p = shard_shape[0]
+        return full2d[rank * p:(rank + 1) * p, :]
+    p = shard_shape[1] * width                          # block of columns
+    return full2d[:, rank * p:(rank + 1) * p]
+
+
+def pin_rows_numpy_shards(orc):
+    """Every tensor-parallel shard loaded by the oracle equals numpy's 2-D
+    slice of the unsharded tensor in the blob, for every rank of 1, 2 and 4;
+    the arena holds them at the layout's offsets."""
+    blob = synth.blob(synth.tiny_tp(0, 1))   # the unsharded model file, same for every rank
+    for size in (1, 2, 4):
+        for rank in range(size):
+            t = synth.tiny_tp(rank, size)
+            full = t.meta["full"]
+            nb = orc.nbytes(t)
+            rows = orc.rows(t)
+            assert orc.check_rows(nb, t.src_offset, rows, t.src_row_stride, t.dst_align) == 0
+            got = orc.load_rows(nb, t.src_offset, rows, t.src_row_stride, blob)
+            fnb = orc.nbytes(full)
+            w = 2
+            for i, name in enumerate(t.names):
+                j = full.names.index(name.split("@")[0])
+                fshape = full.shapes[j]
+                f = blob[int(full.src_offset[j]):int(full.src_offset[j]) + int(fnb[j])]
+                f2 = f.reshape(fshape[0], -1) if len(fshape) == 2 else f
+                want = _shard_view(f2, fshape, t.shapes[i], rank, w)
+                assert got[i].tobytes() == np.ascontiguousarray(want).tobytes(), (name, rank, size)
+            off, ab = orc.layout(nb, t.dst_align)
+            arena = np.zeros(ab, np.uint8)
+            orc.arena_rows(nb, t.src_offset, rows, t.src_row_stride, t.dst_align, blob, arena)
+            for i in range(t.n):
+                assert arena[int(off[i]):int(off[i]) + int(nb[i])].tobytes() == got[i].tobytes()
+    # the shards of all ranks tile their unsharded tensor exactly once
+    t0 = [synth.tiny_tp(r, 4) for r in range(4)]
+    for name in ("layers.0.o", "layers.3.down", "layers.1.q", "embed"):
+        cols = []
+        for r, t in enumerate(t0):
+            i = t.names.index(f"{name}@{r}/4")
+            nb = orc.nbytes(t)
+            cols.append((int(t.src_offset[i]), int(nb[i]), t.shapes[i], int(t.src_row_stride[i])))
+        full = t0[0].meta["full"]
+        j = full.names.index(name)
+        fb = int(orc.nbytes(full)[j])
+        s0 = int(full.src_offset[j])
+        covered = np.zeros(fb, np.int32)            # bytes of the unsharded tensor
+        pos = np.arange(fb, dtype=np.int64)
+        for so, n, shp, st in cols:
+            rows = shp[0] if st else 1
+            rb = n // rows
+            idx = np.lib.stride_tricks.as_strided(pos[so - s0:], shape=(rows, rb),
+                                                  strides=(st * pos.itemsize, pos.itemsize))
+            np.add.at(covered, idx.ravel(), 1)
+        assert (covered == 1).all(), name
+
+
+def _row_owner_map(sizes, src, rows, stride):
+    """source byte -> (tensor, byte index in the tensor), from numpy's
+    strided view of an index array over the blob."""
+    owner = {}
+    span = max([src[i] + (rows[i] - 1) * stride[i] + sizes[i] // rows[i]
+                for i in range(len(sizes)) if rows[i]] + [1])
+    pos = np.arange(span + 1, dtype=np.int64)
+    for i, (n, s, r, st) in enumerate(zip(sizes, src, rows, stride)):
+        if not r:
+            continue
+        rb = n // r
+        view = np.lib.stride_tricks.as_strided(pos[s:], shape=(r, rb),
+                                               strides=(st * pos.itemsize, pos.itemsize))
+        for j, x in enumerate(view.ravel().tolist()):
+            owner[x] = (i, j)
+    return owner
+
+
+def _row_segments_by_bytes(owner, C):
+    xs = sorted(owner)
+    if not xs:
+        return [], 0, 0
+    lo, hi = xs[0], xs[-1] + 1
+    segs, cur = [], None
+    for x in range(lo, hi):
+        o = owner.get(x)
+        if o is None:
+            cur = None
+            continue
+        k = (x - lo) // C
+        if cur is not None and cur[0] == k and cur[2] == o[0] and cur[3] + cur[4] == o[1] \
+                and cur[5] == x:
+            cur[4] += 1
+            cur[5] += 1
+        else:
+            cur = [k, x - (lo + k * C), o[0], o[1], 1, x + 1]
+            segs.append(cur)
+    return [tuple(c[:5]) for c in segs], lo, hi
+
+
+def pin_rows_bytewise(orc):
+    """Tiny random strided tables (interleaved column blocks, gaps, rows that
+    straddle chunk ends): the oracle's segments, joined at row ends, equal
+    the runs of equal (chunk, tensor, consecutive tensor byte) tags; the
+    counts follow the closed forms K = ceil((hi - lo) / C) and
+    S = sum over rows of the chunk indices each row spans."""
+    rng = random.Random(23)
+    done = 0
+    while done < 300:
+        # column blocks of one [R, full_row] byte matrix, plus contiguous
+        # tensors after it
+        n = rng.randint(1, 4)
+        R = rng.randint(1, 6)
+        widths = [rng.randint(1, 9) for _ in range(n)]
+        sizes, src, rows, stride = [], [], [], []
+        base = rng.randint(0, 9)
+        full_row = sum(widths) + rng.randint(0, 3)
+        col = 0
+        for i in range(n):
+            r = R if rng.random() < 0.8 else 1
+            if r == 1:
+                sizes.append(widths[i] * rng.randint(1, 3))
+                src.append(base + R * full_row + 5 + 40 * i)
+                rows.append(1)
+                stride.append(0)
+            else:
+                sizes.append(widths[i] * R)
+                src.append(base + col)
+                rows.append(R)
+                stride.append(full_row)
+                col += widths[i]
+            if rng.random() < 0.1:
+                sizes[-1], rows[-1] = 0, 0
+        align = [16] * n
+        if orc.check_rows(sizes, src, rows, stride, align):
+            continue
+        C = rng.choice((8, 16, 32, 48))
+        owner = _row_owner_map(sizes, src, rows, stride)
+        want, lo, hi = _row_segments_by_bytes(owner, C)
+        p = orc.plan_rows(sizes, src, rows, stride, C)
+        assert _merge_runs(_plan_tuples(p)) == want, (sizes, src, rows, stride, C)
+        K = -(-(hi - lo) // C) if hi > lo else 0
+        assert len(p["chunk_begin"]) == K
+        S = sum((s + q * st + n // r - 1 - lo) // C - (s + q * st - lo) // C + 1
+                for n, s, r, st in zip(sizes, src, rows, stride) if r for q in range(r))
+        assert len(p["seg_len"]) == S, (sizes, src, rows, stride, C)
+        assert orc.span_rows(sizes, src, rows, stride) == ((lo, hi) if K else (0, 0))
+        blob = np.frombuffer(rng.randbytes(hi + 2), dtype=np.uint8).copy()
+        got = orc.load_rows(sizes, src, rows, stride, blob)
+        for i in range(n):
+            exp = bytes(blob[x] for x, o in sorted(owner.items(), key=lambda kv: kv[1])
+                        if o[0] == i)
+            assert got[i].tobytes() == exp
+        done += 1
+
+
+def pin_rows_check(orc):
+    """Validity of tables given as rows, on hand-made cases."""
+    A = [256]
+    # two column blocks of one [4, 8] byte matrix interleave without overlap
+    assert orc.check_rows([16, 16], [0, 4], [4, 4], [8, 8], A * 2) == 0
+    # shifted by one byte they collide
+    assert orc.check_rows([16, 16], [0, 3], [4, 4], [8, 8], A * 2) == EOVERLAP
+    # rows of one tensor closer than a row: invalid, not an overlap
+    assert orc.check_rows([16], [0], [4], [3], A) == EINVAL
+    # the same bytes as one row: fine, stride unused
+    assert orc.check_rows([16], [0], [1], [3], A) == 0
+    # a contiguous tensor that lands in a gap between rows, and one that does not
+    assert orc.check_rows([16, 4], [0, 4], [4, 1], [8, 0], A * 2) == 0
+    assert orc.check_rows([16, 5], [0, 4], [4, 1], [8, 0], A * 2) == EOVERLAP
+    # the last row's end does not fit in 64 bits
+    assert orc.check_rows([8], [0], [2], [2 ** 64 - 2], A) == EOVERFLOW
+    assert orc.check_rows([8], [2 ** 63], [4], [2 ** 62], A) == EOVERFLOW
+    assert orc.check_rows([8], [0], [4], [2], [3]) == EINVAL
+    # rows(): shape[0] for strided tensors, 1 for contiguous, 0 for empty
+    t = _T([5, 5, 5, 5], [(4, 8), (4, 8), (0, 8), (3, 2, 2)], [0, 1000, 0, 2000], A * 4)
+    t.src_row_stride = np.array([32, 0, 32, 64], np.uint64)
+    assert orc.rows(t).tolist() == [4, 1, 0, 3]
+    s = _T([5], [()], [0], A)
+    s.src_row_stride = np.array([8], np.uint64)
+    try:
+        orc.rows(s)
+    except Exception as e:  # noqa: BLE001
+        assert getattr(e, "code", None) == EINVAL
+    else:
+        raise AssertionError("a strided scalar must be rejected")
+
+
 PINS = [pin_esize, pin_sizes, pin_chunks, pin_appendix_counts, pin_segments_bytewise,
-        pin_coverage, pin_layout, pin_check, pin_load, pin_arena, pin_switch, pin_empty]
+        pin_coverage, pin_layout, pin_check, pin_load, pin_arena, pin_switch, pin_empty,
+        pin_rows_contiguous, pin_rows_numpy_shards, pin_rows_bytewise, pin_rows_check]
 
 
 def run_all(so_path: str, quick: bool = True) -> list[str]:

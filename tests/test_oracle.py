@@ -24,7 +24,8 @@ def test_pin(orc, pin):
     pin(orc)
 
 
-# (description, text in ii_oracle.c, replacement)
+# (description, text in ii_oracle.c, replacement -- or one replacement per
+# occurrence where the text occurs in a contiguous and a row-wise function)
 MUTANTS = [
     ("bf16 width 4", "case 5: case 6: return 2;", "case 5: case 6: return 4;"),
     ("sum dims instead of product", "numel *= x;", "numel += x;"),
@@ -34,11 +35,12 @@ MUTANTS = [
     ("arena rounded to smallest alignment", "if (a > maxal)", "if (a < maxal)"),
     ("last chunk never partial", "chunk_len[K] = (hi - b < chunk_bytes) ? hi - b : chunk_bytes;",
      "chunk_len[K] = chunk_bytes;"),
-    ("chunk offset measured from tensor", "tmp[m].chunk_off = b - cb;", "tmp[m].chunk_off = b - tb;"),
+    ("chunk offset measured from tensor", "tmp[m].chunk_off = b - cb;",
+     ("tmp[m].chunk_off = b - tb;", "tmp[m].chunk_off = b - rs;")),
     ("tensor offset measured from chunk", "tmp[m].tensor_off = b - tb;", "tmp[m].tensor_off = b - cb;"),
     ("segment not clipped at chunk end", "uint64_t e = te < ce ? te : ce;", "uint64_t e = te;"),
     ("segment not clipped at chunk start", "uint64_t b = tb > cb ? tb : cb;", "uint64_t b = tb;"),
-    ("empty segments kept", "if (b < e) {", "if (b <= e && b < te) {"),
+    ("empty segments kept", "if (b < e) {", ("if (b <= e && b < te) {", "if (b <= e && b < re) {")),
     ("segments left in table order", "qsort(tmp, m, sizeof(orc_seg), cmp_seg);", ""),
     ("chunk windows from zero", "uint64_t cb = lo + (uint64_t)k * chunk_bytes;",
      "uint64_t cb = (uint64_t)k * chunk_bytes;"),
@@ -55,17 +57,58 @@ MUTANTS = [
     ("touching ranges called overlapping", "if (r[j].begin < r[j - 1].end)",
      "if (r[j].begin <= r[j - 1].end)"),
     ("span ignores the smallest offset", "if (src_offset[i] < l)", "if (src_offset[i] > l)"),
+    # tables given as rows
+    ("rows taken from the last dimension", "rows[i] = (uint64_t)shape_flat[shape_start[i]];",
+     "rows[i] = (uint64_t)shape_flat[shape_start[i] + ndim[i] - 1];"),
+    ("row piece offset uses the source stride", "tmp[m].tensor_off = q * rb + (b - rs);",
+     "tmp[m].tensor_off = q * stride[i] + (b - rs);"),
+    ("row piece offset from the tensor's first row", "tmp[m].tensor_off = q * rb + (b - rs);",
+     "tmp[m].tensor_off = q * rb + (b - src_offset[i]);"),
+    ("row pieces not clipped at chunk end", "uint64_t e = re < ce ? re : ce;", "uint64_t e = re;"),
+    ("row load ignores the stride", "uint64_t s = src_offset[i] + q * stride[i];",
+     "uint64_t s = src_offset[i] + q * rb;"),
+    ("row load packs rows at the stride", "memcpy(out[i] + q * rb, blob + s, rb);",
+     "memcpy(out[i] + (q ? rb : 0), blob + s, rb);"),
+    ("rows span stops at the first row", "            if (e > h)\n                h = e;\n        }\n    if (h == 0)\n        l = 0;\n    *lo = l;\n    *hi = h;\n}\n\n/* orc_plan for rows",
+     "            if (q == 0 && e > h)\n                h = e;\n        }\n    if (h == 0)\n        l = 0;\n    *lo = l;\n    *hi = h;\n}\n\n/* orc_plan for rows"),
+    ("rows closer than a row allowed",
+     "if (rows[i] > 1 && stride[i] < row_bytes(nbytes, rows, i))\n            return ORC_EINVAL;", ""),
+    ("row overlap check sees first rows only",
+     "r[m].begin = src_offset[i] + q * stride[i];", "r[m].begin = src_offset[i] + (q ? 1 : 0) * stride[i];"),
+    ("row arena ignores alignment", "rc = orc_load_rows_into(n, nbytes, src_offset, rows, stride, blob, blob_len, out);",
+     "for (size_t i = 0; i < n; ++i)\n            out[i] = arena + (i ? off[i] - off[i] % 64 : 0);\n        rc = orc_load_rows_into(n, nbytes, src_offset, rows, stride, blob, blob_len, out);"),
 ]
 
 
-@pytest.mark.parametrize("desc,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
-def test_pins_catch_mutant(desc, old, new):
+def _cases():
+    """One case per occurrence of each mutation site: where the row-wise
+    functions repeat a step of the contiguous ones, the slip is planted in
+    each copy separately."""
     src = open(oracle.SRC).read()
-    assert src.count(old) == 1, f"mutation site not unique: {old!r}"
+    out = []
+    for desc, old, new in MUTANTS:
+        count = src.count(old)
+        for k in range(max(count, 1)):
+            out.append(pytest.param(desc, old, new, k, count,
+                                    id=desc if count == 1 else f"{desc} #{k + 1}"))
+    return out
+
+
+def _replace_nth(text, old, new, k):
+    at = -1
+    for _ in range(k + 1):
+        at = text.index(old, at + 1)
+    return text[:at] + new + text[at + len(old):]
+
+
+@pytest.mark.parametrize("desc,old,new,k,count", _cases())
+def test_pins_catch_mutant(desc, old, new, k, count):
+    src = open(oracle.SRC).read()
+    assert count >= 1, f"mutation site not found: {old!r}"
     with tempfile.TemporaryDirectory() as d:
         c = os.path.join(d, "mut.c")
         so = os.path.join(d, "libmut.so")
-        open(c, "w").write(src.replace(old, new))
+        open(c, "w").write(_replace_nth(src, old, new[k] if isinstance(new, tuple) else new, k))
         oracle.build(c, so)
         env = dict(os.environ, PYTHONPATH=ROOT + os.pathsep + os.path.join(ROOT, "tests"))
         r = subprocess.run([sys.executable, os.path.join(ROOT, "tests", "oracle_pins.py"), so],
