@@ -73,6 +73,18 @@ enum {
  *   src_offset  byte offset of the tensor's first byte in the blob.
  *   dst_align   required alignment (power of two) of the tensor's
  *               destination address.
+ *   src_row_stride
+ *               0: the tensor's bytes are contiguous in the blob. Otherwise
+ *               the tensor is shape[0] rows of nbytes / shape[0] bytes each,
+ *               row q starting at blob byte src_offset + q * src_row_stride
+ *               (a column block of a larger row-major matrix, as a
+ *               tensor-parallel rank holds its shard of a row-parallel weight
+ *               in an unsharded model file; Sec. 2.2, Sec. 6.1). The
+ *               destination is always contiguous: row q lands at tensor byte
+ *               q * (nbytes / shape[0]). Requires ndim >= 1 and, when
+ *               shape[0] > 1, src_row_stride >= the row's bytes; ignored for
+ *               zero-size tensors. Rows of different tensors may interleave
+ *               but no blob byte may belong to two rows.
  */
 typedef struct ii_tensor_desc {
     const char* name;
@@ -81,6 +93,7 @@ typedef struct ii_tensor_desc {
     const int64_t* shape;
     uint64_t src_offset;
     uint64_t dst_align;
+    uint64_t src_row_stride;
 } ii_tensor_desc;
 
 typedef struct ii_plan_s ii_plan_t; /* opaque */
@@ -93,8 +106,13 @@ typedef struct ii_plan_s ii_plan_t; /* opaque */
  *
  * Chunks are windows of chunk_bytes over the span [lo, hi) of the table's
  * source bytes (lo = smallest source offset, hi = largest source end over
- * non-empty tensors); chunk k covers [lo + k*chunk_bytes, min(lo +
- * (k+1)*chunk_bytes, hi)). A segment is one tensor's piece of one chunk.
+ * non-empty tensors, or over their rows for tensors given with a row
+ * stride); chunk k covers [lo + k*chunk_bytes, min(lo + (k+1)*chunk_bytes,
+ * hi)). A segment is one tensor's piece of one chunk (for a tensor given as
+ * rows, one row's piece of one chunk), ordered by offset in the chunk.
+ * The ring loads move, per chunk, only the bytes from its first segment's
+ * start to its last segment's end (rounded out to 256 bytes), and skip chunks
+ * that hold no segment; the total is ii_plan_copy_bytes.
  * Destination layout (used by ii_switch and by callers carving an arena): in
  * table order, tensor i starts at the smallest multiple of dst_align[i] at or
  * after the end of tensor i-1; arena_bytes is the end rounded up to the
@@ -106,8 +124,10 @@ typedef struct ii_plan_s ii_plan_t; /* opaque */
  *   out          receives the plan; release with ii_plan_free.
  * Host only: touches no device. Errors: II_EINVAL (NULL out, NULL table with
  * n > 0, bad chunk_bytes, unknown dtype, negative ndim or extent, dst_align
- * not a power of two), II_EOVERFLOW, II_EOVERLAP (two non-empty source
- * ranges share a byte), II_ENOMEM.
+ * not a power of two, a row stride on a scalar or shorter than its row, more
+ * than 2^31 rows in all), II_EOVERFLOW (a size or a source end, including a
+ * last row's end, does not fit in 64 bits), II_EOVERLAP (two non-empty
+ * source ranges or rows share a byte), II_ENOMEM.
  */
 int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_bytes, ii_plan_t** out);
 
@@ -247,10 +267,11 @@ int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads,
  * the copy stream) and before and after its scatter (on the scatter stream).
  * ii_plan_trace waits for the last traced load to finish and writes, for
  * each chunk, the times in milliseconds since that load's first scatter-
- * stream event into arrays of num_chunks entries (NULL skips one). The
- * dependency edges can be read off them: copy_end[k] <= scatter_start[k] and
- * scatter_end[k] <= copy_start[k + depth]. Errors: II_EINVAL (tracing off or
- * no traced load), II_EBUSY, II_EHIP.
+ * stream event into arrays of num_chunks entries (NULL skips one); chunks
+ * that hold no segment are not moved and get NaN. The dependency edges can be
+ * read off them: copy_end[k] <= scatter_start[k], and scatter_end of the i-th
+ * moved chunk <= copy_start of the (i + depth)-th. Errors: II_EINVAL (tracing
+ * off or no traced load), II_EBUSY, II_EHIP.
  */
 int ii_plan_set_trace(ii_plan_t* plan, int on);
 int ii_plan_trace(ii_plan_t* plan, float* copy_start, float* copy_end, float* scatter_start,
@@ -268,6 +289,11 @@ size_t ii_plan_num_segments(const ii_plan_t* plan);
 uint64_t ii_plan_chunk_bytes(const ii_plan_t* plan);
 uint64_t ii_plan_payload_bytes(const ii_plan_t* plan); /* sum of nbytes */
 uint64_t ii_plan_arena_bytes(const ii_plan_t* plan);
+/* bytes one ii_load / ii_load_file moves from host to device: per chunk
+ * that holds segments, its first segment's start to its last segment's end,
+ * rounded out to 256-byte boundaries inside the chunk (hi - lo for a table
+ * whose tensors tile their span) */
+uint64_t ii_plan_copy_bytes(const ii_plan_t* plan);
 /* span [lo, hi) of source bytes; both 0 when every tensor is empty */
 void ii_plan_span(const ii_plan_t* plan, uint64_t* lo, uint64_t* hi);
 /* per tensor (arrays of num_tensors; NULL skips a field) */

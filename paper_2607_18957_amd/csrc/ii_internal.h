@@ -1,6 +1,7 @@
 // Internal declarations shared by the planner, the runtime and the kernels.
 #pragma once
 
+#include <algorithm>
 #include <atomic>
 #include <cstdint>
 #include <memory>
@@ -38,6 +39,7 @@ struct RangeDev {
 constexpr uint32_t kDefaultTile = 8u << 10;  // bytes of chunk per workgroup (<= kMaxTile)
 constexpr uint32_t kMaxCopyStreams = 2;       // host-to-device copy streams of a ring
 constexpr uint64_t kIoAlign = 4096;           // block alignment of direct-I/O file reads
+constexpr uint64_t kCopyAlign = 256;          // host-to-device copies start and end on these
 
 struct Runtime;  // device-side state (runtime.hip)
 
@@ -55,11 +57,14 @@ struct ii_plan_s {
     std::vector<uint64_t> shape_start;
     std::vector<uint64_t> src_offset;
     std::vector<uint64_t> dst_align;
+    std::vector<uint64_t> row_stride;  // 0 for contiguous tensors
     // derived
     std::vector<uint64_t> nbytes;
+    std::vector<uint64_t> rows;        // 1 for contiguous tensors, 0 for empty ones
     std::vector<uint64_t> dst_offset;
     uint64_t payload = 0, arena_bytes = 0, max_align = 1;
     uint64_t lo = 0, hi = 0;
+    uint64_t copy_bytes = 0;  // host-to-device bytes per load (used range of each chunk)
     uint64_t chunk_bytes = 0;
     size_t num_chunks = 0;
     std::vector<uint64_t> chunk_seg_begin;  // num_chunks + 1
@@ -81,6 +86,21 @@ struct ii_plan_s {
 
     uint64_t chunk_len(size_t k) const {
         return k + 1 < num_chunks ? chunk_bytes : (hi - lo) - chunk_bytes * (num_chunks - 1);
+    }
+    // The bytes of chunk k a load moves: from its first segment's start to
+    // its last segment's end, rounded out to kCopyAlign inside the chunk;
+    // empty if the chunk holds no segment (a gap between the tensors of a
+    // sharded table).
+    void chunk_used(size_t k, uint64_t* b, uint64_t* e) const {
+        const uint64_t s0 = chunk_seg_begin[k], s1 = chunk_seg_begin[k + 1];
+        if (s0 == s1) {
+            *b = *e = 0;
+            return;
+        }
+        const uint64_t a = ii::kCopyAlign;
+        const uint64_t end = (uint64_t)seg_off[s1 - 1] + seg_len[s1 - 1];
+        *b = seg_off[s0] & ~(a - 1);
+        *e = std::min<uint64_t>(chunk_len(k), (end + a - 1) & ~(a - 1));
     }
 };
 

@@ -6,12 +6,14 @@
 // spans. This file computes that association once, on the host, so that the
 // load path only walks precomputed tables.
 //
-// Method: sort the non-empty tensors by source offset (which also finds
-// overlaps), then sweep them in source order and cut each tensor's range at
-// chunk boundaries. Because source ranges are disjoint, the pieces come out
-// already ordered by chunk and by offset inside the chunk: O(N log N + S).
-// The per-tile segment windows used by the kernel come from one more linear
-// sweep per chunk.
+// Method: list every non-empty tensor's source pieces -- the tensor itself,
+// or each of its rows when it is given with a row stride (a tensor-parallel
+// shard read out of an unsharded file) -- sort them by source offset (which
+// also finds overlaps), then sweep them in source order and cut each piece at
+// chunk boundaries. Because pieces are disjoint, the segments come out
+// already ordered by chunk and by offset inside the chunk: O(P log P + S) for
+// P pieces. The per-tile segment windows used by the kernel come from one
+// more linear sweep per chunk.
 #include <algorithm>
 #include <cstdarg>
 #include <cstdio>
@@ -57,6 +59,15 @@ static int width_of(int32_t dtype) {
 
 static bool pow2(uint64_t x) { return x && !(x & (x - 1)); }
 
+// One contiguous run of a tensor's source bytes: the whole tensor, or one
+// row of a tensor given with a row stride.
+struct Piece {
+    uint64_t src;   // blob offset of the first byte
+    uint64_t len;
+    uint64_t toff;  // offset of that byte inside the tensor
+    uint32_t tensor;
+};
+
 static uint32_t env_u32(const char* name, uint32_t dflt, uint32_t lo, uint32_t hi) {
     const char* s = getenv(name);
     if (!s || !*s) return dflt;
@@ -89,6 +100,8 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         p->shape_start.resize(n);
         p->src_offset.resize(n);
         p->dst_align.resize(n);
+        p->row_stride.resize(n);
+        p->rows.resize(n);
         p->nbytes.resize(n);
         p->dst_offset.resize(n);
     } catch (const std::bad_alloc&) {
@@ -127,14 +140,35 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         uint64_t nb;
         if (__builtin_mul_overflow(numel, (uint64_t)w, &nb))
             return fail(II_EOVERFLOW, "ii_plan: row %zu: byte size overflows", i);
-        uint64_t end;
-        if (__builtin_add_overflow(d.src_offset, nb, &end))
+        // rows: a strided tensor is shape[0] rows of rb bytes, row q at
+        // src_offset + q * stride; every other non-empty tensor is one row
+        uint64_t rows = nb ? 1 : 0, rb = nb;
+        if (nb && d.src_row_stride) {
+            if (d.ndim < 1)
+                return fail(II_EINVAL, "ii_plan: row %zu: a row stride needs ndim >= 1", i);
+            rows = (uint64_t)d.shape[0];
+            rb = nb / rows;
+            if (rows > 1 && d.src_row_stride < rb)
+                return fail(II_EINVAL, "ii_plan: row %zu: row stride %llu is shorter than a row "
+                            "(%llu bytes)", i, (unsigned long long)d.src_row_stride,
+                            (unsigned long long)rb);
+        }
+        uint64_t last = d.src_offset, end;
+        if (rows > 1) {
+            uint64_t step;
+            if (__builtin_mul_overflow(rows - 1, d.src_row_stride, &step) ||
+                __builtin_add_overflow(d.src_offset, step, &last))
+                return fail(II_EOVERFLOW, "ii_plan: row %zu: last row's offset overflows", i);
+        }
+        if (__builtin_add_overflow(last, rb, &end))
             return fail(II_EOVERFLOW, "ii_plan: row %zu: source end overflows", i);
         p->names[i] = d.name ? d.name : "";
         p->dtype[i] = d.dtype;
         p->ndim[i] = d.ndim;
         p->src_offset[i] = d.src_offset;
         p->dst_align[i] = d.dst_align;
+        p->row_stride[i] = rows > 1 ? d.src_row_stride : 0;
+        p->rows[i] = rows;
         p->nbytes[i] = nb;
         p->payload += nb;  // cannot overflow: disjoint ranges below 2^64
     }
@@ -159,36 +193,59 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         p->max_align = maxal;
     }
 
-    // 3. source order, overlap check, span
-    std::vector<uint32_t> order;
-    order.reserve(n);
-    for (size_t i = 0; i < n; ++i)
-        if (p->nbytes[i]) order.push_back((uint32_t)i);
-    std::sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) {
-        return p->src_offset[a] < p->src_offset[b];
-    });
-    for (size_t j = 1; j < order.size(); ++j) {
-        uint32_t a = order[j - 1], b = order[j];
-        if (p->src_offset[b] < p->src_offset[a] + p->nbytes[a])
-            return fail(II_EOVERLAP, "ii_plan: source ranges of rows %u and %u overlap", a, b);
+    // 3. source pieces in source order, overlap check, span
+    std::vector<Piece> pieces;
+    try {
+        uint64_t total = 0;
+        for (size_t i = 0; i < n; ++i) {
+            total += p->rows[i];  // rows < 2^63, and the sum stops below 2^32
+            if (total > (1ull << 31))
+                return fail(II_EINVAL, "ii_plan: more than 2^31 rows in all");
+        }
+        pieces.reserve((size_t)total);
+        for (size_t i = 0; i < n; ++i) {
+            const uint64_t rows = p->rows[i];
+            if (!rows) continue;
+            const uint64_t rb = p->nbytes[i] / rows;
+            for (uint64_t q = 0; q < rows; ++q)
+                pieces.push_back(Piece{p->src_offset[i] + q * p->row_stride[i], rb, q * rb,
+                                       (uint32_t)i});
+        }
+    } catch (const std::bad_alloc&) {
+        return fail(II_ENOMEM, "ii_plan: host allocation failed");
     }
-    if (!order.empty()) {
-        p->lo = p->src_offset[order.front()];
-        uint32_t l = order.back();
-        p->hi = p->src_offset[l] + p->nbytes[l];
+    // a table's own order is usually source order already
+    if (!std::is_sorted(pieces.begin(), pieces.end(),
+                        [](const Piece& a, const Piece& b) { return a.src < b.src; }))
+        std::sort(pieces.begin(), pieces.end(),
+                  [](const Piece& a, const Piece& b) { return a.src < b.src; });
+    for (size_t j = 1; j < pieces.size(); ++j) {
+        const Piece& a = pieces[j - 1];
+        const Piece& b = pieces[j];
+        if (b.src < a.src + a.len) {
+            if (a.tensor == b.tensor)
+                return fail(II_EOVERLAP, "ii_plan: rows of table row %u overlap", a.tensor);
+            return fail(II_EOVERLAP, "ii_plan: source ranges of rows %u and %u overlap",
+                        a.tensor, b.tensor);
+        }
+    }
+    if (!pieces.empty()) {
+        p->lo = pieces.front().src;
+        p->hi = pieces.back().src + pieces.back().len;
     }
     const uint64_t C = chunk_bytes, lo = p->lo, span = p->hi - p->lo;
     p->num_chunks = span ? (size_t)((span - 1) / C + 1) : 0;
     if (p->num_chunks >= (1ull << 32))
         return fail(II_EINVAL, "ii_plan: more than 2^32 chunks");
 
-    // 4. cut every tensor at chunk boundaries, in source order
+    // 4. cut every piece at chunk boundaries, in source order
     try {
         size_t S = 0;
-        for (uint32_t i : order) {
-            uint64_t b = p->src_offset[i] - lo, e = b + p->nbytes[i];
+        for (const Piece& pc : pieces) {
+            uint64_t b = pc.src - lo, e = b + pc.len;
             S += (size_t)((e - 1) / C - b / C + 1);
         }
+        if (S >= (1ull << 32)) return fail(II_EINVAL, "ii_plan: more than 2^32 segments");
         p->seg_chunk.resize(S);
         p->seg_off.resize(S);
         p->seg_tensor.resize(S);
@@ -196,23 +253,28 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         p->seg_toff.resize(S);
         p->chunk_seg_begin.assign(p->num_chunks + 1, 0);
         size_t s = 0;
-        for (uint32_t i : order) {
-            uint64_t b = p->src_offset[i] - lo, e = b + p->nbytes[i];
+        for (const Piece& pc : pieces) {
+            uint64_t b = pc.src - lo, e = b + pc.len;
             for (uint64_t x = b; x < e;) {
                 uint64_t k = x / C, cend = std::min(e, (k + 1) * C);
                 p->seg_chunk[s] = (uint32_t)k;
                 p->seg_off[s] = (uint32_t)(x - k * C);
-                p->seg_tensor[s] = i;
+                p->seg_tensor[s] = pc.tensor;
                 p->seg_len[s] = (uint32_t)(cend - x);
-                p->seg_toff[s] = x - b;
+                p->seg_toff[s] = pc.toff + (x - b);
                 p->chunk_seg_begin[k + 1]++;
                 ++s;
                 x = cend;
             }
         }
+        std::vector<Piece>().swap(pieces);
         for (size_t k = 0; k < p->num_chunks; ++k)
             p->chunk_seg_begin[k + 1] += p->chunk_seg_begin[k];
-        if (S >= (1ull << 32)) return fail(II_EINVAL, "ii_plan: more than 2^32 segments");
+        for (size_t k = 0; k < p->num_chunks; ++k) {
+            uint64_t b, e;
+            p->chunk_used(k, &b, &e);
+            p->copy_bytes += e - b;
+        }
 
         // 5. tiles: per chunk, windows of tile_bytes and the segments meeting them
         uint32_t T = env_u32("II_TILE_BYTES", kDefaultTile, 1024, kMaxTile) & ~15u;
@@ -265,6 +327,7 @@ extern "C" size_t ii_plan_num_segments(const ii_plan_t* p) { return p ? p->seg_l
 extern "C" uint64_t ii_plan_chunk_bytes(const ii_plan_t* p) { return p ? p->chunk_bytes : 0; }
 extern "C" uint64_t ii_plan_payload_bytes(const ii_plan_t* p) { return p ? p->payload : 0; }
 extern "C" uint64_t ii_plan_arena_bytes(const ii_plan_t* p) { return p ? p->arena_bytes : 0; }
+extern "C" uint64_t ii_plan_copy_bytes(const ii_plan_t* p) { return p ? p->copy_bytes : 0; }
 
 extern "C" void ii_plan_span(const ii_plan_t* p, uint64_t* lo, uint64_t* hi) {
     if (lo) *lo = p ? p->lo : 0;

@@ -27,6 +27,7 @@
 
 #include <algorithm>
 #include <cerrno>
+#include <cmath>
 #include <memory>
 #include <cstring>
 #include <vector>
@@ -86,7 +87,11 @@ struct Runtime {
     // optional per-chunk timeline of the last ring load (timing events)
     std::vector<hipEvent_t> tr_cs, tr_ce, tr_ss, tr_se;
     hipEvent_t tr_t0 = nullptr;
-    size_t tr_chunks = 0;  // chunks recorded by the last traced load (0 = none)
+    size_t tr_chunks = 0;          // chunks recorded by the last traced load (0 = none)
+    std::vector<uint32_t> tr_id;   // chunk index of each recorded entry
+    // chunks that hold at least one segment, in order (the ring skips the rest)
+    std::vector<uint32_t> live;
+    bool live_ready = false;
 };
 
 static void free_trace(Runtime* r) {
@@ -175,6 +180,12 @@ static int ensure_tables(ii_plan_t* p) {
         II_HIP(hipEventCreateWithFlags(&r->tables_idle, hipEventDisableTiming));
         II_HIP(hipEventCreateWithFlags(&r->upload_done, hipEventDisableTiming));
         II_HIP(hipEventCreateWithFlags(&r->ranges_idle, hipEventDisableTiming));
+    }
+    if (!r->live_ready) {
+        r->live.clear();
+        for (size_t k = 0; k < p->num_chunks; ++k)
+            if (p->chunk_seg_begin[k] < p->chunk_seg_begin[k + 1]) r->live.push_back((uint32_t)k);
+        r->live_ready = true;
     }
     const size_t S = p->seg_len.size();
     if (S && !r->d_segs) {
@@ -434,14 +445,21 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
 
     const uint32_t D = r->depth, K = (uint32_t)p->num_chunks;
     const uint64_t C = p->chunk_bytes, last_len = K ? p->chunk_len(K - 1) : 0;
+    // Chunk j of the ring is chunk live[j] of the plan; only the used range
+    // [u0, u1) of a chunk crosses the link, and it keeps its offsets in the
+    // slot, so the kernel reads the segments where the plan puts them.
+    const std::vector<uint32_t>& live = r->live;
+    const uint32_t L = (uint32_t)live.size();
     std::unique_ptr<ReadAhead> ahead;
-    if (src.fd >= 0 && src.direct && K) {
+    if (src.fd >= 0 && src.direct && L) {
         const uint64_t lo = p->lo;
         try {
             ahead.reset(new ReadAhead(
-            src.fd, std::min<uint32_t>(p->host_threads, 8), C + 2 * kIoAlign, K,
-            [p, lo, C](uint32_t k) {
-                const uint64_t at = lo + (uint64_t)k * C, len = p->chunk_len(k);
+            src.fd, std::min<uint32_t>(p->host_threads, 8), C + 2 * kIoAlign, L,
+            [p, lo, C, &live](uint32_t j) {
+                uint64_t u0, u1;
+                p->chunk_used(live[j], &u0, &u1);
+                const uint64_t at = lo + (uint64_t)live[j] * C + u0, len = u1 - u0;
                 const uint64_t a = at & ~(kIoAlign - 1);
                 const uint64_t e = (at + len + kIoAlign - 1) & ~(kIoAlign - 1);
                 return ReadAhead::Range{a, e, at + len - a};
@@ -451,55 +469,59 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         }
         if (!ahead->ok()) return fail(II_ENOMEM, "read-ahead buffer allocation failed");
     }
-    for (uint32_t k = 0; k < K; ++k) {
-        const uint32_t slot = k % D;
-        const uint64_t len = p->chunk_len(k);
-        const uint64_t at = p->lo + (uint64_t)k * C;  // blob / file offset of the chunk
+    for (uint32_t j = 0; j < L; ++j) {
+        const uint32_t k = live[j], slot = j % D;
+        uint64_t u0, u1;
+        p->chunk_used(k, &u0, &u1);
+        const uint64_t len = u1 - u0;
+        const uint64_t at = p->lo + (uint64_t)k * C + u0;  // blob / file offset of the bytes
         const uint8_t* from = blob ? blob + at : nullptr;
         if (!pinned) {
             // InDisk -> InMem: the pinned slot is free once its last copy finished
             if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
+            uint8_t* stage = r->hslot[slot] + u0;
             if (src.fd < 0) {
-                r->pool->copy(r->hslot[slot], from, len);
-                from = r->hslot[slot];
+                r->pool->copy(stage, from, len);
             } else if (!src.direct) {
-                const int err = r->pool->read(src.fd, r->hslot[slot], at, len, 1, len);
+                const int err = r->pool->read(src.fd, stage, at, len, 1, len);
                 if (err)
                     return fail(II_EIO, "reading chunk %u (file bytes %llu..%llu): %s", k,
                                 (unsigned long long)at, (unsigned long long)(at + len),
                                 strerror(err));
-                from = r->hslot[slot];
             } else {
                 // direct I/O: whole blocks, read ahead into aligned buffers;
                 // the chunk's bytes are then copied into the pinned slot
                 int err = 0;
-                const uint8_t* b = ahead->wait(k, &err);
+                const uint8_t* b = ahead->wait(j, &err);
                 if (!b)
                     return fail(II_EIO, "reading chunk %u (file bytes from %llu): %s", k,
                                 (unsigned long long)(at & ~(kIoAlign - 1)), strerror(err));
-                r->pool->copy(r->hslot[slot], b + (at & (kIoAlign - 1)), len);
-                ahead->release(k);
-                from = r->hslot[slot];
+                r->pool->copy(stage, b + (at & (kIoAlign - 1)), len);
+                ahead->release(j);
             }
+            from = stage;
         }
         // InMem -> InGPU, once the device slot's previous scatter is done
-        hipStream_t cs = r->copy_s[k % r->ncopy];
+        hipStream_t cs = r->copy_s[j % r->ncopy];
         if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(cs, r->scatter_done[slot], 0));
-        if (trace) II_HIP(hipEventRecord(r->tr_cs[k], cs));
-        II_HIP(hipMemcpyAsync(r->dslot[slot], from, len, hipMemcpyHostToDevice, cs));
+        if (trace) II_HIP(hipEventRecord(r->tr_cs[j], cs));
+        II_HIP(hipMemcpyAsync(r->dslot[slot] + u0, from, len, hipMemcpyHostToDevice, cs));
         II_HIP(hipEventRecord(r->copy_done[slot], cs));
-        if (trace) II_HIP(hipEventRecord(r->tr_ce[k], cs));
+        if (trace) II_HIP(hipEventRecord(r->tr_ce[j], cs));
         r->copy_rec[slot] = 1;
         // InGPU -> tensors Loaded, then the slot is released
         II_HIP(hipStreamWaitEvent(r->scatter_s, r->copy_done[slot], 0));
-        if (trace) II_HIP(hipEventRecord(r->tr_ss[k], r->scatter_s));
+        if (trace) II_HIP(hipEventRecord(r->tr_ss[j], r->scatter_s));
         II_HIP(launch_scatter_slot(r->dslot[slot], k, r->d_segs, r->d_tiles, C, last_len, K,
                                    p->tiles_per_chunk, p->tile_bytes, r->scatter_s));
         II_HIP(hipEventRecord(r->scatter_done[slot], r->scatter_s));
-        if (trace) II_HIP(hipEventRecord(r->tr_se[k], r->scatter_s));
+        if (trace) II_HIP(hipEventRecord(r->tr_se[j], r->scatter_s));
         r->scatter_rec[slot] = 1;
     }
-    if (trace) r->tr_chunks = K;
+    if (trace) {
+        r->tr_id = live;
+        r->tr_chunks = L;
+    }
     II_HIP(hipEventRecord(r->tables_idle, r->scatter_s));
     r->tables_used = true;
     II_HIP(hipEventRecord(r->done, r->scatter_s));
@@ -562,10 +584,18 @@ static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
     if (!pinned && r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
     for (size_t i = 0; i < p->nbytes.size(); ++i) {
         const uint64_t n = p->nbytes[i];
+        if (!n) continue;
         const uint8_t* src = blob + p->src_offset[i];
+        // a tensor given as rows is gathered row by row (rb bytes every
+        // `stride` source bytes) into one contiguous destination
+        const uint64_t rb = n / p->rows[i], stride = p->row_stride[i];
         if (pinned) {
-            if (n) II_HIP(hipMemcpyAsync(reinterpret_cast<void*>(dst[i]), src, n,
-                                         hipMemcpyHostToDevice, cs));
+            if (p->rows[i] > 1)
+                II_HIP(hipMemcpy2DAsync(reinterpret_cast<void*>(dst[i]), rb, src, stride, rb,
+                                        p->rows[i], hipMemcpyHostToDevice, cs));
+            else
+                II_HIP(hipMemcpyAsync(reinterpret_cast<void*>(dst[i]), src, n,
+                                      hipMemcpyHostToDevice, cs));
             continue;
         }
         for (uint64_t x = 0; x < n;) {
@@ -573,9 +603,14 @@ static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
                 rc = close_slot();
                 if (rc) return rc;
             }
+            // stage tensor bytes [x, x + len) and copy them with one DMA
             const uint64_t len = std::min(n - x, C - used);
             uint8_t* stage = r->hslot[slot] + used;
-            r->pool->copy(stage, src + x, len);
+            for (uint64_t y = x; y < x + len;) {
+                const uint64_t q = y / rb, c = y % rb, m = std::min(x + len - y, rb - c);
+                r->pool->copy(stage + (y - x), src + q * stride + c, m);
+                y += m;
+            }
             II_HIP(hipMemcpyAsync(reinterpret_cast<void*>(dst[i] + x), stage, len,
                                   hipMemcpyHostToDevice, cs));
             used += len;
@@ -756,18 +791,22 @@ extern "C" int ii_plan_trace(ii_plan_t* p, float* copy_start, float* copy_end,
                              float* scatter_start, float* scatter_end) {
     if (!p) return fail(II_EINVAL, "ii_plan_trace: plan is NULL");
     Runtime* r = p->rt;
-    if (!r || !r->tr_chunks || r->tr_chunks != p->num_chunks)
+    if (!r || !r->tr_chunks)
         return fail(II_EINVAL, "ii_plan_trace: no traced ring load on record");
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_plan_trace: plan in use");
-    const size_t K = r->tr_chunks;
-    II_HIP(hipEventSynchronize(r->tr_se[K - 1]));
-    for (size_t k = 0; k < K; ++k) {
+    const size_t L = r->tr_chunks;
+    II_HIP(hipEventSynchronize(r->tr_se[L - 1]));
+    for (float* out : {copy_start, copy_end, scatter_start, scatter_end})
+        if (out)
+            for (size_t k = 0; k < p->num_chunks; ++k) out[k] = std::nanf("");
+    for (size_t j = 0; j < L; ++j) {
+        const uint32_t k = r->tr_id[j];
         const struct {
             float* out;
             hipEvent_t e;
-        } items[4] = {{copy_start, r->tr_cs[k]}, {copy_end, r->tr_ce[k]},
-                      {scatter_start, r->tr_ss[k]}, {scatter_end, r->tr_se[k]}};
+        } items[4] = {{copy_start, r->tr_cs[j]}, {copy_end, r->tr_ce[j]},
+                      {scatter_start, r->tr_ss[j]}, {scatter_end, r->tr_se[j]}};
         for (const auto& it : items) {
             if (!it.out) continue;
             II_HIP(hipEventSynchronize(it.e));

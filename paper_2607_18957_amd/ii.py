@@ -8,7 +8,8 @@ module raises -- there is no fallback path.
 
 Accepted argument forms:
   table     a ``synth.Table`` (or any object with the same columnar fields:
-            names, dtype, shapes, src_offset, dst_align)
+            names, dtype, shapes, src_offset, dst_align, and optionally
+            src_row_stride)
   blob      a numpy uint8 array, a ``HostBuffer`` from ii_host_alloc, or an
             (address, nbytes) pair
   image     a torch device tensor, or an (address, nbytes) pair
@@ -71,7 +72,8 @@ _sig("ii_plan_set_trace", _c.c_int, _vp, _c.c_int)
 _sig("ii_plan_trace", _c.c_int, _vp, _vp, _vp, _vp, _vp)
 for _n in ("ii_plan_num_tensors", "ii_plan_num_chunks", "ii_plan_num_segments"):
     _sig(_n, _sz, _vp)
-for _n in ("ii_plan_chunk_bytes", "ii_plan_payload_bytes", "ii_plan_arena_bytes"):
+for _n in ("ii_plan_chunk_bytes", "ii_plan_payload_bytes", "ii_plan_arena_bytes",
+           "ii_plan_copy_bytes"):
     _sig(_n, _u64, _vp)
 _sig("ii_plan_span", None, _vp, _P(_u64), _P(_u64))
 _sig("ii_plan_tensors", _c.c_int, _vp, _vp, _vp)
@@ -110,7 +112,8 @@ def ii_last_error() -> str:
 # marshalling helpers
 
 _DESC = np.dtype([("name", "<u8"), ("dtype", "<i4"), ("ndim", "<i4"), ("shape", "<u8"),
-                  ("src_offset", "<u8"), ("dst_align", "<u8")])  # struct ii_tensor_desc
+                  ("src_offset", "<u8"), ("dst_align", "<u8"),
+                  ("src_row_stride", "<u8")])  # struct ii_tensor_desc
 
 
 def _stream(s) -> int:
@@ -219,6 +222,10 @@ class Plan:
         return _lib.ii_plan_arena_bytes(self.handle)
 
     @property
+    def copy_bytes(self) -> int:
+        return _lib.ii_plan_copy_bytes(self.handle)
+
+    @property
     def span(self) -> tuple[int, int]:
         lo, hi = _u64(), _u64()
         _lib.ii_plan_span(self.handle, _c.byref(lo), _c.byref(hi))
@@ -314,6 +321,9 @@ def _desc_array(table) -> tuple[np.ndarray, list]:
         d["shape"] = np.where(d["ndim"] > 0, base + np.asarray(start, np.uint64) * np.uint64(8), 0)
         d["src_offset"] = np.asarray(table.src_offset, dtype=np.uint64)
         d["dst_align"] = np.asarray(table.dst_align, dtype=np.uint64)
+        stride = getattr(table, "src_row_stride", None)
+        if stride is not None:
+            d["src_row_stride"] = np.asarray(stride, dtype=np.uint64)
     keep.append(d)
     return d, keep
 

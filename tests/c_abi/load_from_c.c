@@ -56,6 +56,7 @@ int main(void) {
         t[i].shape = shapes[i];
         t[i].src_offset = pos;
         t[i].dst_align = (i % 2) ? 256 : 4096;
+        t[i].src_row_stride = 0;                                      /* contiguous */
         pos += nb + 8;                                                /* small gaps in the file */
     }
     const uint64_t blob_bytes = pos;

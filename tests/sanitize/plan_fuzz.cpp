@@ -2,10 +2,12 @@
 //
 // Builds random tables -- including zero-size tensors, scalars, huge
 // extents that overflow, overlapping and touching ranges, every dtype and
-// alignment -- plans them with several chunk sizes, reads every getter and
+// alignment, tensors given as strided rows and column blocks whose rows
+// interleave -- plans them with several chunk sizes, reads every getter and
 // checks the structural invariants that need no oracle: segments tile each
-// tensor exactly, lie inside their chunk, and are ordered; tile windows are
-// consistent. Any sanitizer report or failed check exits non-zero.
+// tensor exactly, lie inside their chunk and inside one row, and are
+// ordered; tile windows are consistent; the copied bytes lie between the
+// payload and the span. Any sanitizer report or failed check exits non-zero.
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -44,26 +46,56 @@ int main(int argc, char** argv) {
     for (int it = 0; it < iters; ++it) {
         const size_t n = pick(40);
         std::vector<std::vector<int64_t>> shapes(n);
-        std::vector<ii_tensor_desc> t(n);
+        std::vector<ii_tensor_desc> t(n, ii_tensor_desc{});
+        static const uint64_t width[11] = {0, 1, 1, 1, 1, 2, 2, 4, 4, 8, 8};
         uint64_t pos = pick(64);
-        for (size_t i = 0; i < n; ++i) {
-            const int nd = (int)pick(4);
-            for (int d = 0; d < nd; ++d) shapes[i].push_back(pick(10) ? (int64_t)pick(50) : 0);
-            t[i].name = (i % 3) ? "w" : nullptr;
-            t[i].dtype = 1 + (int32_t)pick(10);
-            t[i].ndim = (int32_t)shapes[i].size();
-            t[i].shape = shapes[i].empty() ? nullptr : shapes[i].data();
-            t[i].dst_align = 1ull << pick(13);
-            t[i].src_offset = pos;
-            static const uint64_t width[11] = {0, 1, 1, 1, 1, 2, 2, 4, 4, 8, 8};
-            uint64_t numel = 1;
-            for (int64_t x : shapes[i]) numel *= (uint64_t)x;
-            pos += numel * width[t[i].dtype] + (pick(3) ? 0 : pick(40));
+        if (pick(3) == 0) {
+            // column blocks of one [R, row] byte matrix: rows of all tensors interleave
+            const uint64_t R = 1 + pick(6);
+            uint64_t col = 0;
+            std::vector<uint64_t> w(n);
+            for (size_t i = 0; i < n; ++i) w[i] = 1 + pick(9);
+            uint64_t row = pick(4);
+            for (size_t i = 0; i < n; ++i) row += w[i];
+            for (size_t i = 0; i < n; ++i) {
+                shapes[i] = {(int64_t)R, (int64_t)w[i]};
+                t[i].name = nullptr;
+                t[i].dtype = 1;
+                t[i].ndim = 2;
+                t[i].shape = shapes[i].data();
+                t[i].dst_align = 1ull << pick(9);
+                t[i].src_offset = pos + col;
+                t[i].src_row_stride = row;
+                col += w[i];
+            }
+        } else {
+            for (size_t i = 0; i < n; ++i) {
+                const int nd = (int)pick(4);
+                for (int d = 0; d < nd; ++d) shapes[i].push_back(pick(10) ? (int64_t)pick(50) : 0);
+                t[i].name = (i % 3) ? "w" : nullptr;
+                t[i].dtype = 1 + (int32_t)pick(10);
+                t[i].ndim = (int32_t)shapes[i].size();
+                t[i].shape = shapes[i].empty() ? nullptr : shapes[i].data();
+                t[i].dst_align = 1ull << pick(13);
+                t[i].src_offset = pos;
+                t[i].src_row_stride = 0;
+                uint64_t numel = 1;
+                for (int64_t x : shapes[i]) numel *= (uint64_t)x;
+                const uint64_t nb = numel * width[t[i].dtype];
+                if (nd >= 1 && nb && pick(3) == 0) {  // strided rows with gaps
+                    const uint64_t rows = (uint64_t)shapes[i][0], rb = nb / rows;
+                    t[i].src_row_stride = rb + pick(20);
+                    pos += (rows - 1) * t[i].src_row_stride + rb;
+                } else {
+                    pos += nb;
+                }
+                pos += pick(3) ? 0 : pick(40);
+            }
         }
         // one table in four gets one bad row of a random kind
         if (n && pick(4) == 0) {
             const size_t i = pick(n);
-            switch (pick(7)) {
+            switch (pick(10)) {
             case 0: t[i].dtype = pick(2) ? 0 : 11; break;                   // unknown dtype
             case 1: shapes[i].push_back(-1); break;                           // negative extent
             case 2: shapes[i].push_back((int64_t)(1ull << 40));               // size overflows
@@ -72,6 +104,9 @@ int main(int argc, char** argv) {
             case 4: t[i].src_offset = ~0ull - pick(100); break;               // end overflows
             case 5: if (i) t[i].src_offset = t[i - 1].src_offset; break;      // overlap (if non-empty)
             case 6: t[i].ndim = -1; break;
+            case 7: t[i].src_row_stride = 1; break;                           // rows overlap (if > 1 row of > 1 byte)
+            case 8: t[i].src_row_stride = ~0ull / 2; break;                   // last row overflows (if > 2 rows)
+            case 9: shapes[i].clear(); t[i].src_row_stride = 8; break;        // strided scalar
             }
             t[i].shape = shapes[i].empty() ? nullptr : shapes[i].data();
             if (t[i].ndim >= 0) t[i].ndim = (int32_t)shapes[i].size();
@@ -103,13 +138,22 @@ int main(int argc, char** argv) {
             for (size_t i = 0; i < N; ++i) (void)ii_plan_tensor_name(p, i);
             uint64_t lo, hi;
             ii_plan_span(p, &lo, &hi);
-            // segments: inside their chunk, ordered, and tiling each tensor
+            // rows of each tensor as the table gives them
+            std::vector<uint64_t> rows(N), rb(N);
+            for (size_t i = 0; i < N; ++i) {
+                rows[i] = nb[i] ? (t[i].src_row_stride ? (uint64_t)shapes[i][0] : 1) : 0;
+                rb[i] = rows[i] ? nb[i] / rows[i] : 0;
+            }
+            // segments: inside their chunk and one row, ordered, and tiling each tensor
             std::vector<uint64_t> covered(N, 0);
             uint64_t total = 0;
             for (size_t s = 0; s < S; ++s) {
                 CHECK(sc[s] < K && st[s] < N && sl[s] > 0);
                 CHECK((uint64_t)so[s] + sl[s] <= cl[sc[s]]);
-                CHECK(cb[sc[s]] + so[s] == t[st[s]].src_offset + sto[s]);
+                const uint64_t q = sto[s] / rb[st[s]], c = sto[s] % rb[st[s]];
+                CHECK(c + sl[s] <= rb[st[s]]);
+                CHECK(cb[sc[s]] + so[s] ==
+                      t[st[s]].src_offset + q * (rows[st[s]] > 1 ? t[st[s]].src_row_stride : 0) + c);
                 CHECK(sto[s] == covered[st[s]]);  // source order = offset order within a tensor
                 covered[st[s]] += sl[s];
                 total += sl[s];
@@ -118,6 +162,7 @@ int main(int argc, char** argv) {
             }
             for (size_t i = 0; i < N; ++i) CHECK(covered[i] == nb[i]);
             CHECK(total == ii_plan_payload_bytes(p));
+            CHECK(ii_plan_copy_bytes(p) >= total && ii_plan_copy_bytes(p) <= hi - lo);
             for (size_t k = 0; k < K; ++k) {
                 CHECK(sb[k] <= sb[k + 1]);
                 for (uint32_t x = 0; x < tpc; ++x) {

@@ -56,12 +56,13 @@ def test_header_constants():
 
 
 def test_struct_layout_matches_binding():
-    # ii_tensor_desc: ptr, i32, i32, ptr, u64, u64
+    # ii_tensor_desc: ptr, i32, i32, ptr, u64, u64, u64
     class Desc(ctypes.Structure):
         _fields_ = [("name", ctypes.c_char_p), ("dtype", ctypes.c_int32),
                     ("ndim", ctypes.c_int32), ("shape", ctypes.c_void_p),
-                    ("src_offset", ctypes.c_uint64), ("dst_align", ctypes.c_uint64)]
-    assert ctypes.sizeof(Desc) == ii._DESC.itemsize == 40
+                    ("src_offset", ctypes.c_uint64), ("dst_align", ctypes.c_uint64),
+                    ("src_row_stride", ctypes.c_uint64)]
+    assert ctypes.sizeof(Desc) == ii._DESC.itemsize == 48
     for f, _ in Desc._fields_:
         assert getattr(Desc, f).offset == ii._DESC.fields[f][1]
 

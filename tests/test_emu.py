@@ -35,10 +35,20 @@ def _run(orc, table, *, chunk=None, arena_phase=0, src_phase=0, batch=256, dst_o
     assert ok, msg
     want = can.copy()
     # the oracle arena, at the same (possibly shifted) offsets
-    if dst_of is None:
-        orc.arena(orc.nbytes(table), table.src_offset, table.dst_align, blob, want)
+    nbo = orc.nbytes(table)
+    stride = getattr(table, "src_row_stride", None)
+    if stride is not None and np.any(stride):
+        rows = orc.rows(table, nbo)
+        if dst_of is None:
+            orc.arena_rows(nbo, table.src_offset, rows, stride, table.dst_align, blob, want)
+        else:
+            outs = orc.load_rows(nbo, table.src_offset, rows, stride, blob)
+            for o, d in zip(outs, dst - base):
+                want[int(d):int(d) + o.size] = o
+    elif dst_of is None:
+        orc.arena(nbo, table.src_offset, table.dst_align, blob, want)
     else:
-        outs = orc.load(orc.nbytes(table), table.src_offset, blob)
+        outs = orc.load(nbo, table.src_offset, blob)
         for o, d in zip(outs, dst - base):
             want[int(d):int(d) + o.size] = o
     assert np.array_equal(got, want), int(np.flatnonzero(got != want)[0])
@@ -126,3 +136,27 @@ def test_random_dst_gaps(orc):
             return np.array(out, dtype=np.uint64)
 
         _run(orc, t, dst_of=dst_of, arena_phase=rng.randint(0, 15), src_phase=rng.randint(0, 15))
+
+
+@pytest.mark.parametrize("size", [2, 4, 8])
+def test_tp_shards(orc, size):
+    """Tensor-parallel shards read out of the unsharded file: column blocks
+    arrive as one segment per row, and rows of 64 B .. 512 B are far below a
+    tile."""
+    for rank in sorted({0, size - 1, size // 2}):
+        t = synth.tiny_tp(rank, size)
+        _run(orc, t)
+        _run(orc, t, chunk=64 << 10, arena_phase=5, src_phase=3)
+
+
+def test_interleaved_column_blocks_misaligned(orc):
+    import test_plan
+    rng = random.Random(4)
+    for _ in range(40):
+        t = test_plan._column_blocks(rng, rng.randint(1, 6), rng.randint(1, 40),
+                                     rng.randint(0, 60), rng.randint(0, 40), rng.randint(0, 3))
+        t.chunk_bytes = 16 * rng.randint(1, 64)
+        nb = orc.nbytes(t)
+        _, hi = orc.span_rows(nb, t.src_offset, orc.rows(t, nb), t.src_row_stride)
+        t.blob = np.frombuffer(rng.randbytes(hi + 64), dtype=np.uint8).copy()
+        _run(orc, t, arena_phase=rng.randint(0, 15), src_phase=rng.randint(0, 15))

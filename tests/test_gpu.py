@@ -38,9 +38,20 @@ def _canary_buffer(nbytes, seed=0xC0FFEE):
     return buf, can
 
 
+def _oracle_arena(orc, table, blob, out):
+    """The oracle's arena for a table, contiguous or given as rows."""
+    nb = orc.nbytes(table)
+    stride = getattr(table, "src_row_stride", None)
+    if stride is not None and np.any(stride):
+        orc.arena_rows(nb, table.src_offset, orc.rows(table, nb), stride, table.dst_align,
+                       blob, out)
+    else:
+        orc.arena(nb, table.src_offset, table.dst_align, blob, out)
+
+
 def _expect_arena(orc, table, blob, canary_slice):
     want = canary_slice.copy()
-    orc.arena(orc.nbytes(table), table.src_offset, table.dst_align, blob, want)
+    _oracle_arena(orc, table, blob, want)
     return want
 
 
@@ -210,7 +221,8 @@ def test_load_from_file(orc, where, root, direct):
     if not os.path.isdir(root):
         pytest.skip(f"{root} missing")
     cases = [synth.tiny(header=1000), synth.tiny(chunk=65552, header=4099, dst_align=1),
-             synth.stress(n=30000, chunk=1 << 20)]
+             synth.stress(n=30000, chunk=1 << 20), synth.tiny_tp(1, 4, chunk=65552),
+             synth.tiny_tp(7, 8, chunk=1 << 16)]
     for t in cases:
         blob = synth.blob(t)
         fd, path = tempfile.mkstemp(dir=root)
@@ -227,8 +239,7 @@ def test_load_from_file(orc, where, root, direct):
                 ii.ii_load_file(plan, fd, base + off)
                 torch.cuda.synchronize()
                 want = can.copy()
-                orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob,
-                          want[GUARD:GUARD + plan.arena_bytes])
+                _oracle_arena(orc, t, blob, want[GUARD:GUARD + plan.arena_bytes])
                 assert np.array_equal(buf.cpu().numpy(), want), (where, t.name)
                 # a file that ends before the span does: an I/O error, plan still usable
                 with pytest.raises(ii.IIError) as e:
@@ -462,3 +473,109 @@ def test_switch_llama8b_to_mistral7b(orc):
                blob_n, before)
     assert np.array_equal(got, before)
     assert (got[pn.arena_bytes:] == 0).all()
+
+
+# -- tensor-parallel shards: tables given as rows ------------------------------
+
+@pytest.mark.parametrize("mode", ["pageable", "pinned", "image", "pertensor",
+                                  "pertensor-pinned"])
+def test_tp_shards_tiny(orc, mode):
+    """Every rank's shard of the unsharded tiny file, in every load mode:
+    column blocks of the row-parallel weights arrive one segment per row,
+    and the ring moves only the used range of each chunk (64 KiB chunks leave
+    most chunks of a rank's table empty)."""
+    for size in (2, 4, 8):
+        for rank in sorted({0, size // 2, size - 1}):
+            t = synth.tiny_tp(rank, size)
+            _load_arena(orc, t, mode=mode)
+            plan = _load_arena(orc, t, mode=mode, chunk=64 << 10, depth=2, threads=2)
+            if mode in ("pageable", "pinned") and size > 1:
+                lo, hi = plan.span
+                assert plan.copy_bytes < hi - lo
+
+
+def test_tp_trace_skips_empty_chunks(orc):
+    """Chunks holding no byte of the rank's table are not moved (NaN in the
+    timeline); the moved ones keep the pipeline's edges."""
+    t = synth.tiny_tp(1, 4)
+    plan = ii.ii_plan(t, 64 << 10)
+    plan.set_ring(2, 2, 1)
+    plan.set_trace(True)
+    _load_arena(orc, t, plan=plan)
+    tr = plan.trace()
+    _, _, sb = plan.chunks()
+    live = np.diff(sb.astype(np.int64)) > 0
+    assert (~live).any() and live.any()
+    for k in ("copy_start", "copy_end", "scatter_start", "scatter_end"):
+        assert np.isnan(tr[k][~live]).all() and not np.isnan(tr[k][live]).any()
+    cs, ce, ss, se = (tr[k][live] for k in ("copy_start", "copy_end", "scatter_start",
+                                            "scatter_end"))
+    eps = 1e-3
+    assert (ce <= ss + eps).all() and (se[:-1] <= ss[1:] + eps).all()
+    assert (se[:-2] <= cs[2:] + eps).all()
+    assert (ce[:-1] <= cs[1:] + eps).all()
+
+
+def test_switch_full_to_tp_shard(orc):
+    """The arena of the whole tiny model reused for one rank's shard table:
+    the shard's bytes at its offsets, the rest of the old tensors cleared,
+    padding untouched."""
+    old, new = synth.tiny(), synth.tiny_tp(2, 4)
+    po, pn = ii.ii_plan(old), ii.ii_plan(new, 64 << 10)
+    blob = synth.blob(old)
+    buf = torch.empty(po.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
+    buf.fill_(0x5A)
+    base = buf.data_ptr() + GUARD
+    _, off_o = po.tensors()
+    ii.ii_load(po, blob, base + off_o)
+    ii.ii_switch(po, pn, base, po.arena_bytes, blob)
+    torch.cuda.synchronize()
+    got = buf.cpu().numpy()[GUARD:GUARD + po.arena_bytes]
+    want = np.empty(po.arena_bytes, np.uint8)
+    orc.arena(orc.nbytes(old), old.src_offset, old.dst_align, blob, want)
+    nbn = orc.nbytes(new)
+    rows = orc.rows(new, nbn)
+    outs = orc.load_rows(nbn, new.src_offset, rows, new.src_row_stride, blob)
+    # R6: zero where an old tensor was, then the new tensors at their offsets
+    nbo = orc.nbytes(old)
+    off_old, _ = orc.layout(nbo, old.dst_align)
+    for o, n in zip(off_old, nbo):
+        want[int(o):int(o) + int(n)] = 0
+    off_new, _ = orc.layout(nbn, new.dst_align)
+    for o, x in zip(off_new, outs):
+        want[int(o):int(o) + x.size] = x
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.slow
+def test_tp_shard_llama8b_full(orc):
+    """Rank 1 of 4 of the Llama-8B-shaped model read out of the unsharded
+    16 GB file: 4.0 GB of shards, 131k row segments for the column blocks of
+    o and down; pageable ring path (only the used range of each chunk
+    crosses the link) and resident-image path, whole arena vs the oracle."""
+    t = synth.llama8b_tp(1, 4)
+    plan = ii.ii_plan(t)
+    nb, off = plan.tensors()
+    blob = synth.blob(t)
+    _say(f"llama8b tp1/4: oracle arena ({plan.payload_bytes} B, S={plan.num_segments}, "
+         f"copy {plan.copy_bytes} of span {plan.span[1] - plan.span[0]})")
+    want = np.empty(plan.arena_bytes, np.uint8)
+    _oracle_arena(orc, t, blob, want)
+    buf = torch.empty(plan.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
+    base = buf.data_ptr() + GUARD
+    for mode in ("pageable", "image"):
+        buf.fill_(0xA5)
+        _say(f"llama8b tp1/4: {mode} load")
+        if mode == "pageable":
+            ii.ii_load(plan, blob, base + off)
+        else:
+            img = torch.from_numpy(blob).to(DEV)
+            ii.ii_load_device(plan, img, base + off)
+        torch.cuda.synchronize()
+        if mode == "image":
+            del img
+        got = buf.cpu().numpy()
+        assert (got[:GUARD] == 0xA5).all() and (got[GUARD + plan.arena_bytes:] == 0xA5).all()
+        assert np.array_equal(got[GUARD:GUARD + plan.arena_bytes], want), mode
+        del got
+    _say("llama8b tp1/4: bit-exact")

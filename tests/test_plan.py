@@ -194,3 +194,153 @@ def test_empty_plan():
     assert (plan.num_tensors, plan.num_chunks, plan.num_segments, plan.arena_bytes) == (0, 0, 0, 0)
     plan = ii.ii_plan(oracle_pins._u8_table([0, 0], [3, 9], [16, 16]), 64)
     assert (plan.num_chunks, plan.num_segments, plan.span) == (0, 0, (0, 0))
+
+
+# -- tables given as rows (tensor-parallel shards) ----------------------------
+
+def _expected_copy_bytes(op, align=256):
+    """Per chunk that holds segments: first segment start to last segment
+    end, rounded out to `align` inside the chunk."""
+    total = 0
+    ch, off, ln = op["seg_chunk"], op["seg_chunk_off"].astype(np.int64), op["seg_len"].astype(np.int64)
+    for k in np.unique(ch):
+        m = ch == k
+        b = int(off[m].min()) // align * align
+        e = min(int(op["chunk_len"][k]), -(-int((off[m] + ln[m]).max()) // align) * align)
+        total += e - b
+    return total
+
+
+def _compare_rows(orc, table, chunk=None):
+    chunk = chunk or table.chunk_bytes
+    plan = ii.ii_plan(table, chunk)
+    nb = orc.nbytes(table)
+    rows = orc.rows(table, nb)
+    stride = np.asarray(table.src_row_stride, np.uint64)
+    assert orc.check_rows(nb, table.src_offset, rows, stride, table.dst_align) == 0
+    op = orc.plan_rows(nb, table.src_offset, rows, stride, chunk)
+    off, arena = orc.layout(nb, table.dst_align)
+    pnb, poff = plan.tensors()
+    assert np.array_equal(pnb, nb) and np.array_equal(poff, off)
+    assert plan.arena_bytes == arena and plan.payload_bytes == int(nb.sum())
+    assert plan.span == orc.span_rows(nb, table.src_offset, rows, stride)
+    b, l, sb = plan.chunks()
+    assert np.array_equal(b, op["chunk_begin"]) and np.array_equal(l, op["chunk_len"])
+    s = plan.segments()
+    assert plan.num_segments == len(op["seg_len"])
+    assert np.array_equal(s["chunk"], op["seg_chunk"])
+    assert np.array_equal(s["chunk_off"].astype(np.uint64), op["seg_chunk_off"])
+    assert np.array_equal(s["tensor"], op["seg_tensor"])
+    assert np.array_equal(s["tensor_off"], op["seg_tensor_off"])
+    assert np.array_equal(s["len"].astype(np.uint64), op["seg_len"])
+    assert sb[0] == 0 and sb[-1] == plan.num_segments
+    assert plan.copy_bytes == _expected_copy_bytes(op)
+    _check_tiles(plan, s, l)
+    return plan
+
+
+@pytest.mark.parametrize("size", [1, 2, 4, 8])
+def test_tp_shards_tiny(orc, size):
+    for rank in range(size):
+        t = synth.tiny_tp(rank, size)
+        for chunk in (t.chunk_bytes, 64 << 10, 4096 + 16):
+            _compare_rows(orc, t, chunk)
+
+
+def test_tp_shard_llama8b(orc):
+    t = synth.llama8b_tp(1, 4)
+    plan = _compare_rows(orc, t)
+    # a quarter of the model's bytes, read out of the unsharded file
+    full = t.meta["full"]
+    assert abs(plan.payload_bytes * 4 - int(orc.nbytes(full).sum())) < 4 * 1024 * 1024
+    assert plan.copy_bytes < plan.span[1] - plan.span[0]
+
+
+def test_contiguous_table_copies_its_span(orc):
+    for t in (synth.tiny(), synth.llama8b(), synth.stress(n=5000)):
+        plan = ii.ii_plan(t)
+        lo, hi = plan.span
+        if t.name.startswith("stress"):
+            assert plan.copy_bytes <= hi - lo
+        else:
+            assert plan.copy_bytes == hi - lo
+
+
+def _column_blocks(rng, n, R, extra, base, contiguous_after=0):
+    """n column blocks of one [R, row] u8 matrix (rows interleave), then
+    `contiguous_after` contiguous tensors past the matrix."""
+    widths = [rng.randint(1, 40) for _ in range(n)]
+    row = sum(widths) + extra
+    shapes, src, stride, col = [], [], [], 0
+    for w in widths:
+        shapes.append((R, w))
+        src.append(base + col)
+        stride.append(row)
+        col += w
+    pos = base + R * row + rng.randint(0, 30)
+    for _ in range(contiguous_after):
+        s = rng.randint(0, 90)
+        shapes.append((s,))
+        src.append(pos)
+        stride.append(0)
+        pos += s + rng.randint(0, 5)
+    t = oracle_pins._T([1] * len(shapes), shapes, src, [rng.choice([1, 16, 256])
+                                                        for _ in shapes])
+    t.src_row_stride = np.array(stride, np.uint64)
+    return t
+
+
+@settings(max_examples=150, deadline=None)
+@given(st.data())
+def test_random_strided_tables(orc, data):
+    seed = data.draw(st.integers(0, 2 ** 32 - 1))
+    rng = random.Random(seed)
+    n = data.draw(st.integers(1, 6))
+    R = data.draw(st.integers(1, 12))
+    t = _column_blocks(rng, n, R, data.draw(st.integers(0, 50)), data.draw(st.integers(0, 40)),
+                       data.draw(st.integers(0, 4)))
+    order = list(range(t.n))
+    rng.shuffle(order)                        # table order need not be source order
+    perm = oracle_pins._T(t.dtype[order], [t.shapes[i] for i in order], t.src_offset[order],
+                          t.dst_align[order])
+    perm.src_row_stride = t.src_row_stride[order]
+    perm.chunk_bytes = 16 * data.draw(st.integers(1, 24))
+    _compare_rows(orc, perm)
+
+
+def test_row_errors(orc):
+    def tab(shapes, src, stride, align=None):
+        t = oracle_pins._T([1] * len(shapes), shapes, src, align or [1] * len(shapes))
+        t.src_row_stride = np.array(stride, np.uint64)
+        return t
+    assert _err(tab([(4, 8)], [0], [8]), 64) == "II_OK"
+    assert _err(tab([(4, 8)], [0], [7]), 64) == "II_EINVAL"          # rows closer than a row
+    assert _err(tab([(1, 8)], [0], [7]), 64) == "II_OK"              # one row: stride unused
+    assert _err(tab([()], [0], [8]), 64) == "II_EINVAL"              # strided scalar
+    assert _err(tab([(0, 8)], [0], [3]), 64) == "II_OK"              # empty: ignored
+    assert _err(tab([(4, 8), (4, 8)], [0, 8], [16, 16]), 64) == "II_OK"
+    assert _err(tab([(4, 8), (4, 8)], [0, 7], [16, 16]), 64) == "II_EOVERLAP"
+    assert _err(tab([(3, 8)], [0], [(1 << 63)]), 64) == "II_EOVERFLOW"
+    assert _err(tab([(2, 8)], [(1 << 64) - 40], [16]), 64) == "II_OK"        # last row ends at 2^64 - 16
+    assert _err(tab([(2, 8)], [(1 << 64) - 20], [16]), 64) == "II_EOVERFLOW"
+    # where the oracle defines the class, the two agree on random bad tables
+    rng = random.Random(9)
+    for _ in range(300):
+        t = _column_blocks(rng, rng.randint(1, 4), rng.randint(1, 5), rng.randint(0, 8),
+                           rng.randint(0, 9), rng.randint(0, 2))
+        st_ = t.src_row_stride.copy()
+        so = t.src_offset.copy()
+        i = rng.randrange(t.n)
+        kind = rng.randrange(3)
+        if kind == 0 and st_[i]:
+            st_[i] = np.uint64(rng.randint(1, 30))
+        elif kind == 1:
+            so[i] = np.uint64(int(so[i]) + rng.randint(-3, 3)) if int(so[i]) >= 3 else so[i]
+        else:
+            t.dst_align[i] = np.uint64(rng.choice([1, 3, 16]))
+        t.src_offset, t.src_row_stride = so, st_
+        nb = orc.nbytes(t)
+        rows = orc.rows(t, nb)
+        want = {0: "II_OK", 1: "II_EINVAL", 2: "II_EOVERFLOW", 3: "II_EOVERLAP"}[
+            orc.check_rows(nb, t.src_offset, rows, t.src_row_stride, t.dst_align)]
+        assert _err(t, 64) == want, (t.shapes, so, st_, t.dst_align)
