@@ -59,6 +59,16 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def table_bytes(plan) -> int:
+    """Bytes of plan tables one image launch reads: a 16-byte segment row per
+    segment and an 8-byte segment range per tile; for a table with gaps
+    between its segments also an 8-byte window and a 4-byte chunk index per
+    tile."""
+    _, clen, _ = plan.chunks()
+    gaps = not np.array_equal(plan.packing()["chunk_len"], clen)
+    return plan.num_segments * 16 + len(plan.tiles()["first"]) * (8 + (12 if gaps else 0))
+
+
 def h2d_peak(torch, dev, chunk_bytes: int) -> dict:
     """Pinned host -> device hipMemcpyAsync bandwidth: sizes {chunk, 1 GiB} x
     {1, 2} streams, 10 repetitions each; best median wins."""
@@ -399,6 +409,35 @@ def main() -> int:
     kernel_ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
     log(f"steps: {ms_step:.3f} ms/step wall, kernel {kernel_ms:.3f} ms")
 
+    # ---- tensor-parallel shard (rank 1 of 4) read out of the same unsharded image
+    tp = {"table": None}
+    tp_t = synth.llama8b_tp(1, 4)
+    assert tp_t.blob_bytes == table.blob_bytes and tp_t.seed == table.seed  # same file
+    tp_plan = ii.ii_plan(tp_t)
+    _, tp_off = tp_plan.tensors()
+    tp_arena = torch.empty(tp_plan.arena_bytes, dtype=torch.uint8, device=dev)
+    tp_dst = tp_arena.data_ptr() + tp_off
+    for _ in range(args.warmup):
+        ii.ii_load_device(tp_plan, image, tp_dst, stream)
+    tev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in tev:
+        a.record(stream)
+        ii.ii_load_device(tp_plan, image, tp_dst, stream)
+        b.record(stream)
+    torch.cuda.synchronize(dev)
+    tp_kms = statistics.mean(a.elapsed_time(b) for a, b in tev)
+    tp_alg = 2 * tp_plan.payload_bytes + table_bytes(tp_plan)
+    tp.update(table=tp_t.name, tensors=tp_t.n, payload_bytes=tp_plan.payload_bytes,
+              segments=tp_plan.num_segments, chunks=tp_plan.num_chunks,
+              span_bytes=tp_plan.span[1] - tp_plan.span[0],
+              pinned_copy_bytes=tp_plan.copy_bytes,
+              kernel={"ms": tp_kms, "GBps": tp_alg / (tp_kms * 1e-3) / 1e9,
+                      "frac_of_hbm_peak": tp_alg / (tp_kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                      "bytes_per_launch": tp_alg})
+    log(f"tp shard {tp_t.name}: kernel {tp_kms:.3f} ms, "
+        f"{tp['kernel']['GBps']:.0f} GB/s algorithmic, S={tp_plan.num_segments}")
+
     # spot check of the timed configuration against the blob (full parity is in the tests)
     rng = np.random.default_rng(0)
     for i in rng.choice(table.n, size=8, replace=False):
@@ -412,9 +451,7 @@ def main() -> int:
             return 1
 
     # ---- roofline of the scatter kernel
-    tb, tpc, _, _ = plan.tiles()
-    meta = plan.num_segments * 16 + plan.num_chunks * tpc * 8
-    alg_bytes = 2 * payload + meta
+    alg_bytes = 2 * payload + table_bytes(plan)
     achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
     traffic = None
     if os.path.exists(TRAFFIC_FILE):
@@ -445,14 +482,37 @@ def main() -> int:
         log(f"e2e {label}: {payload / t / 1e9:.2f} GB/s "
             f"({100 * payload / t / 1e9 / h2d['GBps']:.1f}% of H2D peak)")
 
+    def tp_load(src) -> float:
+        t1 = time.perf_counter()
+        ii.ii_load(tp_plan, src, tp_dst, stream)
+        torch.cuda.synchronize(dev)
+        return time.perf_counter() - t1
+
+    def tp_report(label, times, link_bytes):
+        t = statistics.median(times)
+        tp[label] = {"GBps": tp_plan.payload_bytes / t / 1e9, "link_bytes": link_bytes,
+                     "link_GBps": link_bytes / t / 1e9,
+                     "frac_of_h2d_peak": tp_plan.payload_bytes / t / 1e9 / h2d["GBps"],
+                     "median_s": t, "runs": len(times)}
+        log(f"tp shard {label}: {tp_plan.payload_bytes / t / 1e9:.2f} GB/s of shard bytes, "
+            f"link {link_bytes / t / 1e9:.2f} GB/s")
+
     # pageable blob: staged through the pinned ring by the host threads
     timed_load(blob)  # warm: ring allocation, tables
     report("pageable", [timed_load(blob) for _ in range(args.e2e_reps)])
+    # the shard: the host stage gathers only its bytes, so the link moves the payload
+    tp_load(blob)
+    tp_report("e2e_pageable_packed", [tp_load(blob) for _ in range(args.e2e_reps)],
+              tp_plan.payload_bytes)
     # pinned blob: DMA straight from it; its first load also maps its pages for the device
     pinned = ii.ii_host_alloc(blob.size)
     synth.fill(pinned.ptr, 0, blob.size, table.seed)
     report("pinned_first_load", [timed_load(pinned)])
     report("pinned", [timed_load(pinned) for _ in range(args.e2e_reps)])
+    # the shard from the pinned blob: each chunk's used range goes by DMA as is
+    tp_load(pinned)
+    tp_report("e2e_pinned_trimmed", [tp_load(pinned) for _ in range(args.e2e_reps)],
+              tp_plan.copy_bytes)
     e2e["ring"] = {"depth": 3, "copy_streams": 2, "chunk_bytes": plan.chunk_bytes}
     e2e["host_threads"] = int(os.environ.get("II_HOST_THREADS", min(8, os.cpu_count() or 1)))
     pinned.free()
@@ -518,6 +578,7 @@ def main() -> int:
                      "frac_of_d2d_ceiling": achieved / d2d["GBps"]},
         "cpu_baseline": cpu,
         "e2e": e2e,
+        "tp_shard": tp,
     }
     print(json.dumps(out), flush=True)
     return 0

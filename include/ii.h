@@ -289,11 +289,19 @@ size_t ii_plan_num_segments(const ii_plan_t* plan);
 uint64_t ii_plan_chunk_bytes(const ii_plan_t* plan);
 uint64_t ii_plan_payload_bytes(const ii_plan_t* plan); /* sum of nbytes */
 uint64_t ii_plan_arena_bytes(const ii_plan_t* plan);
-/* bytes one ii_load / ii_load_file moves from host to device: per chunk
+/* bytes one ii_load from a pinned blob moves from host to device: per chunk
  * that holds segments, its first segment's start to its last segment's end,
  * rounded out to 256-byte boundaries inside the chunk (hi - lo for a table
- * whose tensors tile their span) */
+ * whose tensors tile their span). Loads from a pageable blob or a file
+ * stage packed chunks and move payload_bytes. */
 uint64_t ii_plan_copy_bytes(const ii_plan_t* plan);
+/* Packed staging layout (loads from a pageable blob or a file gather only
+ * the segments' bytes of a chunk into its pinned slot, back to back in
+ * segment order): per segment its offset in the slot (num_segments), per
+ * chunk the bytes staged (num_chunks). For a table whose tensors tile their
+ * span this equals the chunk layout. NULL skips a field. Errors: II_EINVAL
+ * (NULL plan). */
+int ii_plan_packing(const ii_plan_t* plan, uint32_t* seg_off, uint64_t* chunk_len);
 /* span [lo, hi) of source bytes; both 0 when every tensor is empty */
 void ii_plan_span(const ii_plan_t* plan, uint64_t* lo, uint64_t* hi);
 /* per tensor (arrays of num_tensors; NULL skips a field) */
@@ -306,13 +314,16 @@ int ii_plan_chunks(const ii_plan_t* plan, uint64_t* src_begin, uint64_t* len,
  * num_segments) */
 int ii_plan_segments(const ii_plan_t* plan, uint32_t* chunk, uint32_t* chunk_off,
                      uint32_t* tensor, uint64_t* tensor_off, uint32_t* len);
-/* the kernel's work split: each chunk is cut into tiles_per_chunk windows of
- * tile_bytes; tile g = k * tiles_per_chunk + t of chunk k covers chunk bytes
- * [t * tile_bytes, min((t+1) * tile_bytes, len_k)) and meets exactly the
- * segments [first[g], last[g]). Arrays of num_chunks * tiles_per_chunk
- * entries; pass NULL arrays to read only the two sizes. */
-int ii_plan_tiles(const ii_plan_t* plan, uint32_t* tile_bytes, uint32_t* tiles_per_chunk,
-                  uint32_t* first, uint32_t* last);
+/* the kernel's work split, one workgroup per tile, tiles in chunk order:
+ * tile g takes tile_bytes of its chunk's segment bytes (counted in segment
+ * order, gaps between segments skipped; the chunk's last tile takes the
+ * rest) and meets exactly the segments [first[g], last[g]). In a packed
+ * staging slot those bytes are slot offsets [m * tile_bytes, ...), m = g's
+ * index within its chunk; in the chunk itself they are the chunk offsets
+ * [w0[g], w1[g]). A chunk without segments has no tiles. Arrays of
+ * *num_tiles entries; pass NULL arrays to read only the sizes. */
+int ii_plan_tiles(const ii_plan_t* plan, uint32_t* tile_bytes, uint64_t* num_tiles,
+                  uint32_t* chunk, uint32_t* first, uint32_t* last, uint32_t* w0, uint32_t* w1);
 /* name of row i as given to ii_plan ("" if none); valid while the plan lives */
 const char* ii_plan_tensor_name(const ii_plan_t* plan, size_t i);
 

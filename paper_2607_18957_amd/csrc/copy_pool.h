@@ -76,6 +76,61 @@ class CopyPool {
         return err.load();
     }
 
+    // A gather: run r copies len[r] bytes from source offset off[r] to dst
+    // + poff[r], where the runs tile [0, total) of dst in order (poff[0] = 0,
+    // poff[r+1] = poff[r] + len[r]). src holds source offset `skew` at
+    // src[0] (every off[r] >= skew). The threads split dst bytes evenly and
+    // each finds its first run by binary search, so many small runs (rows of
+    // a sharded tensor) spread like one large copy.
+    void gather(uint8_t* dst, const uint8_t* src, int64_t skew, const uint32_t* off,
+                const uint32_t* poff, const uint32_t* len, size_t nruns, uint64_t total) {
+        if (!nruns) return;
+        auto piece = [=](uint64_t b, uint64_t e) {
+            size_t r = (size_t)(std::upper_bound(poff, poff + nruns, (uint32_t)b) - poff) - 1;
+            for (; r < nruns && poff[r] < e; ++r) {
+                const uint64_t rb = std::max<uint64_t>(b, poff[r]);
+                const uint64_t re = std::min<uint64_t>(e, (uint64_t)poff[r] + len[r]);
+                const uint64_t at = (uint64_t)((int64_t)off[r] - skew) + (rb - poff[r]);
+                if (re > rb) memcpy(dst + rb, src + at, re - rb);
+            }
+        };
+        if (n_ <= 1 || total < (4u << 20)) piece(0, total);
+        else split(total, 64, piece);
+    }
+
+    // The same gather with the source in a file: run r reads file bytes
+    // [base + off[r], +len[r]) into dst + poff[r] (buffered reads). Returns
+    // 0 or the errno of the first failing read (EIO at end of file).
+    int read_gather(int fd, uint8_t* dst, uint64_t base, const uint32_t* off,
+                    const uint32_t* poff, const uint32_t* len, size_t nruns, uint64_t total) {
+        if (!nruns) return 0;
+        std::atomic<int> err{0};
+        auto piece = [&](uint64_t b, uint64_t e) {
+            size_t r = (size_t)(std::upper_bound(poff, poff + nruns, (uint32_t)b) - poff) - 1;
+            for (; r < nruns && poff[r] < e && !err.load(std::memory_order_relaxed); ++r) {
+                uint64_t rb = std::max<uint64_t>(b, poff[r]);
+                const uint64_t re = std::min<uint64_t>(e, (uint64_t)poff[r] + len[r]);
+                while (rb < re) {
+                    const ssize_t got = ::pread(fd, dst + rb, re - rb,
+                                                (off_t)(base + off[r] + (rb - poff[r])));
+                    if (got < 0) {
+                        if (errno == EINTR) continue;
+                        err.store(errno ? errno : EIO);
+                        return;
+                    }
+                    if (got == 0) {
+                        err.store(EIO);
+                        return;
+                    }
+                    rb += (uint64_t)got;
+                }
+            }
+        };
+        if (n_ <= 1 || total < (4u << 20)) piece(0, total);
+        else split(total, 64, piece);
+        return err.load();
+    }
+
    private:
     // Run fn over [0, len) cut into one piece per thread, pieces aligned to
     // `align`; the calling thread takes piece 0.

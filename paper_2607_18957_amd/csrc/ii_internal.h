@@ -22,13 +22,27 @@ struct SegDev {
 };
 static_assert(sizeof(SegDev) == 16, "SegDev must stay 16 bytes");
 
-// Work split of a chunk: a tile is a window of tile_bytes of the chunk; its
-// segments are [first, last) (every segment whose bytes meet the window).
+// Work split of a chunk: tile m of a chunk takes the chunk's segment bytes
+// [m * tile_bytes, (m+1) * tile_bytes) in segment order ("packed" offsets:
+// a segment's bytes counted from the chunk's first segment, gaps between
+// segments skipped). In a packed staging slot that is exactly the window
+// [m * tile_bytes, ...) of the slot; in the chunk itself (a resident image,
+// or a slot holding the chunk's bytes at their own offsets) the same bytes
+// form the window [w0, w1) of chunk offsets. Either way the tile meets the
+// segments [first, last). A chunk without segments has no tiles.
 struct TileDev {
     uint32_t first;
     uint32_t last;
 };
 static_assert(sizeof(TileDev) == 8, "TileDev must stay 8 bytes");
+// The tile's window [w0, w1) of chunk offsets, kept apart from TileDev so
+// that launches whose windows follow from the tile index read only 8 bytes
+// per tile.
+struct TileWin {
+    uint32_t w0;
+    uint32_t w1;
+};
+static_assert(sizeof(TileWin) == 8, "TileWin must stay 8 bytes");
 
 // Zero-fill range for the switch scrub: [begin, end) as device addresses.
 struct RangeDev {
@@ -71,10 +85,28 @@ struct ii_plan_s {
     // segments in chunk order, then by offset inside the chunk
     std::vector<uint32_t> seg_chunk, seg_off, seg_tensor, seg_len;
     std::vector<uint64_t> seg_toff;
-    // tiles
+    // Packed staging: when the host stage copies a chunk anyway (pageable
+    // blob, file), it gathers only the segments' bytes, back to back in
+    // segment order, so the link carries payload only. Segment s then sits
+    // at seg_poff[s] of its slot; chunk k's slot holds chunk_plen[k] bytes.
+    // A run is a maximal group of consecutive segments that are also
+    // adjacent in the chunk (one memcpy): chunk offset run_off, slot offset
+    // run_poff, run_len.
+    bool packed_distinct = false;  // false: packed layout == chunk layout for every chunk
+    std::vector<uint32_t> seg_poff;
+    std::vector<uint64_t> chunk_plen;
+    std::vector<uint64_t> chunk_run_begin;  // num_chunks + 1
+    std::vector<uint32_t> run_off, run_poff, run_len;
+    // tiles (see TileDev), chunk by chunk
     uint32_t tile_bytes = ii::kDefaultTile;
+    std::vector<ii::TileDev> tiles;
+    std::vector<ii::TileWin> tile_win;
+    std::vector<uint32_t> tile_chunk;        // chunk of each tile
+    std::vector<uint64_t> chunk_tile_begin;  // num_chunks + 1
+    // ceil(chunk_bytes / tile_bytes) when no chunk has a gap between its
+    // segments (every full chunk then has that many tiles and tile g is
+    // window g % it of chunk g / it), else 0
     uint32_t tiles_per_chunk = 0;
-    std::vector<ii::TileDev> tiles;  // num_chunks * tiles_per_chunk
     // runtime configuration
     uint32_t ring_depth = 3;
     uint32_t host_threads = 8;

@@ -276,29 +276,69 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
             p->copy_bytes += e - b;
         }
 
-        // 5. tiles: per chunk, windows of tile_bytes and the segments meeting them
+        // 5. packed staging layout and gather runs
+        p->seg_poff.resize(S);
+        p->chunk_plen.assign(p->num_chunks, 0);
+        p->chunk_run_begin.assign(p->num_chunks + 1, 0);
+        for (size_t k = 0; k < p->num_chunks; ++k) {
+            const uint64_t s0 = p->chunk_seg_begin[k], s1 = p->chunk_seg_begin[k + 1];
+            uint64_t pos = 0;
+            for (uint64_t x = s0; x < s1; ++x) {
+                p->seg_poff[x] = (uint32_t)pos;
+                if (p->seg_poff[x] != p->seg_off[x]) p->packed_distinct = true;
+                const bool joins = x > s0 && p->seg_off[x - 1] + p->seg_len[x - 1] == p->seg_off[x];
+                if (joins) {
+                    p->run_len.back() += p->seg_len[x];
+                } else {
+                    p->run_off.push_back(p->seg_off[x]);
+                    p->run_poff.push_back((uint32_t)pos);
+                    p->run_len.push_back(p->seg_len[x]);
+                }
+                pos += p->seg_len[x];
+            }
+            p->chunk_plen[k] = pos;
+            if (pos != p->chunk_len(k)) p->packed_distinct = true;
+            p->chunk_run_begin[k + 1] = p->run_len.size();
+        }
+
+        // 6. tiles: per chunk, tile_bytes of segment bytes each (packed
+        // offsets), and the same bytes as a window of chunk offsets
         uint32_t T = env_u32("II_TILE_BYTES", kDefaultTile, 1024, kMaxTile) & ~15u;
         p->tile_bytes = T;
-        p->tiles_per_chunk = (uint32_t)((C + T - 1) / T);
-        p->tiles.assign(p->num_chunks * p->tiles_per_chunk, TileDev{0, 0});
+        const std::vector<uint32_t>& po = p->seg_poff;
+        p->chunk_tile_begin.assign(p->num_chunks + 1, 0);
         for (size_t k = 0; k < p->num_chunks; ++k) {
-            uint64_t s0 = p->chunk_seg_begin[k], s1 = p->chunk_seg_begin[k + 1];
-            uint64_t len = p->chunk_len(k);
-            uint64_t first = s0, last = s0;
-            for (uint32_t t = 0; t < p->tiles_per_chunk; ++t) {
-                uint64_t w0 = (uint64_t)t * T, w1 = std::min(len, w0 + T);
-                TileDev& td = p->tiles[k * p->tiles_per_chunk + t];
-                if (w0 >= len) {
-                    td.first = td.last = (uint32_t)s1;
-                    continue;
+            const uint64_t s0 = p->chunk_seg_begin[k], s1 = p->chunk_seg_begin[k + 1];
+            const uint64_t plen = p->chunk_plen[k], M = (plen + T - 1) / T;
+            // chunk offset of packed offset P (P < plen), given the segment
+            // g that holds it
+            auto raw = [&](uint64_t g, uint64_t P) { return p->seg_off[g] + (P - po[g]); };
+            uint64_t f = s0, l = s0;
+            for (uint64_t m = 0; m < M; ++m) {
+                const uint64_t P0 = m * T, P1 = std::min(plen, P0 + T);
+                while (f < s1 && (uint64_t)po[f] + p->seg_len[f] <= P0) ++f;
+                if (l < f) l = f;
+                while (l < s1 && po[l] < P1) ++l;
+                TileWin tw;
+                tw.w0 = (uint32_t)raw(f, P0);
+                if (P1 == plen) {
+                    tw.w1 = p->seg_off[s1 - 1] + p->seg_len[s1 - 1];
+                } else {
+                    // the segment holding P1: l if it starts there, else l - 1
+                    const uint64_t g = (l < s1 && po[l] == P1) ? l : l - 1;
+                    tw.w1 = (uint32_t)raw(g, P1);
                 }
-                while (first < s1 && (uint64_t)p->seg_off[first] + p->seg_len[first] <= w0) ++first;
-                if (last < first) last = first;
-                while (last < s1 && p->seg_off[last] < w1) ++last;
-                td.first = (uint32_t)first;
-                td.last = (uint32_t)last;
+                p->tiles.push_back(TileDev{(uint32_t)f, (uint32_t)l});
+                p->tile_win.push_back(tw);
+                p->tile_chunk.push_back((uint32_t)k);
             }
+            p->chunk_tile_begin[k + 1] = p->tiles.size();
         }
+        if (p->tiles.size() > 0x7fffffffull)
+            return fail(II_EINVAL, "ii_plan: more than 2^31 tiles");
+        // no chunk has a gap: tile m of every chunk is the window [m*T,
+        // (m+1)*T) of it, and full chunks have ceil(C / T) tiles each
+        p->tiles_per_chunk = p->packed_distinct ? 0 : (uint32_t)((C + T - 1) / T);
     } catch (const std::bad_alloc&) {
         return fail(II_ENOMEM, "ii_plan: host allocation failed");
     }
@@ -367,15 +407,28 @@ extern "C" int ii_plan_segments(const ii_plan_t* p, uint32_t* chunk, uint32_t* c
     return II_OK;
 }
 
-extern "C" int ii_plan_tiles(const ii_plan_t* p, uint32_t* tile_bytes, uint32_t* tiles_per_chunk,
-                             uint32_t* first, uint32_t* last) {
+extern "C" int ii_plan_tiles(const ii_plan_t* p, uint32_t* tile_bytes, uint64_t* num_tiles,
+                             uint32_t* chunk, uint32_t* first, uint32_t* last, uint32_t* w0,
+                             uint32_t* w1) {
     if (!p) return fail(II_EINVAL, "ii_plan_tiles: plan is NULL");
     if (tile_bytes) *tile_bytes = p->tile_bytes;
-    if (tiles_per_chunk) *tiles_per_chunk = p->tiles_per_chunk;
+    if (num_tiles) *num_tiles = p->tiles.size();
     for (size_t g = 0; g < p->tiles.size(); ++g) {
+        if (chunk) chunk[g] = p->tile_chunk[g];
         if (first) first[g] = p->tiles[g].first;
         if (last) last[g] = p->tiles[g].last;
+        if (w0) w0[g] = p->tile_win[g].w0;
+        if (w1) w1[g] = p->tile_win[g].w1;
     }
+    return II_OK;
+}
+
+extern "C" int ii_plan_packing(const ii_plan_t* p, uint32_t* seg_off, uint64_t* chunk_len) {
+    if (!p) return fail(II_EINVAL, "ii_plan_packing: plan is NULL");
+    const size_t S = p->seg_len.size();
+    if (seg_off && S) memcpy(seg_off, p->seg_poff.data(), S * 4);
+    if (chunk_len)
+        for (size_t k = 0; k < p->num_chunks; ++k) chunk_len[k] = p->chunk_plen[k];
     return II_OK;
 }
 

@@ -37,13 +37,13 @@
 
 namespace ii {
 
-hipError_t launch_scatter_slot(const uint8_t* slot, uint32_t k, const SegDev* segs,
-                               const TileDev* tiles, uint64_t chunk_bytes, uint64_t last_len,
-                               uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes,
-                               hipStream_t stream);
-hipError_t launch_scatter_image(const uint8_t* span, const SegDev* segs, const TileDev* tiles,
-                                uint64_t chunk_bytes, uint64_t last_len, uint32_t num_chunks,
-                                uint32_t tpc, uint32_t tile_bytes, hipStream_t stream);
+hipError_t launch_scatter_slot(const uint8_t* slot, const TileDev* tiles, const TileWin* wins,
+                               uint32_t ntiles, const SegDev* segs, bool packed,
+                               uint32_t tile_bytes, uint64_t plen, hipStream_t stream);
+hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const TileWin* wins,
+                                const uint32_t* tile_chunk, uint64_t ntiles, uint32_t num_chunks,
+                                uint32_t per_chunk, const SegDev* segs, uint64_t chunk_bytes,
+                                uint64_t last_len, uint32_t tile_bytes, hipStream_t stream);
 hipError_t launch_zero(const RangeDev* ranges, uint32_t n, hipStream_t stream);
 
 #define II_HIP(call)                                                                   \
@@ -62,6 +62,11 @@ struct Runtime {
     SegDev* d_segs = nullptr;
     SegDev* h_segs = nullptr;  // pinned staging for d_segs uploads
     TileDev* d_tiles = nullptr;
+    TileWin* d_wins = nullptr;
+    uint32_t* d_tile_chunk = nullptr;
+    // segment rows with packed staging offsets (plans with packed_distinct)
+    SegDev* d_psegs = nullptr;
+    SegDev* h_psegs = nullptr;
     bool tiles_ready = false;
     hipEvent_t tables_idle = nullptr;   // after the last kernel that read d_segs
     hipEvent_t upload_done = nullptr;   // after the last read of h_segs
@@ -149,6 +154,10 @@ static void destroy(Runtime* r) {
     if (r->d_segs) (void)hipFree(r->d_segs);
     if (r->h_segs) (void)hipHostFree(r->h_segs);
     if (r->d_tiles) (void)hipFree(r->d_tiles);
+    if (r->d_wins) (void)hipFree(r->d_wins);
+    if (r->d_tile_chunk) (void)hipFree(r->d_tile_chunk);
+    if (r->d_psegs) (void)hipFree(r->d_psegs);
+    if (r->h_psegs) (void)hipHostFree(r->h_psegs);
     if (r->d_ranges) (void)hipFree(r->d_ranges);
     if (r->h_ranges) (void)hipHostFree(r->h_ranges);
     if (r->tables_idle) (void)hipEventDestroy(r->tables_idle);
@@ -191,6 +200,20 @@ static int ensure_tables(ii_plan_t* p) {
     if (S && !r->d_segs) {
         II_HIP(hipMalloc(&r->d_segs, S * sizeof(SegDev)));
         II_HIP(hipHostMalloc(&r->h_segs, S * sizeof(SegDev), 0));
+    }
+    if (S && p->packed_distinct && !r->d_psegs) {
+        II_HIP(hipMalloc(&r->d_psegs, S * sizeof(SegDev)));
+        II_HIP(hipHostMalloc(&r->h_psegs, S * sizeof(SegDev), 0));
+    }
+    if (!p->tiles.empty() && !r->d_wins) {
+        II_HIP(hipMalloc(&r->d_wins, p->tile_win.size() * sizeof(TileWin)));
+        II_HIP(hipMemcpy(r->d_wins, p->tile_win.data(), p->tile_win.size() * sizeof(TileWin),
+                         hipMemcpyHostToDevice));
+    }
+    if (!p->tiles.empty() && !r->d_tile_chunk) {
+        II_HIP(hipMalloc(&r->d_tile_chunk, p->tile_chunk.size() * sizeof(uint32_t)));
+        II_HIP(hipMemcpy(r->d_tile_chunk, p->tile_chunk.data(),
+                         p->tile_chunk.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
     }
     if (!p->tiles.empty() && !r->d_tiles) {
         II_HIP(hipMalloc(&r->d_tiles, p->tiles.size() * sizeof(TileDev)));
@@ -320,8 +343,14 @@ static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, ui
         for (size_t i = 0; i < S; ++i)
             r->h_segs[i] = SegDev{p->seg_off[i], p->seg_len[i],
                                   dst[p->seg_tensor[i]] + p->seg_toff[i]};
+        if (p->packed_distinct)
+            for (size_t i = 0; i < S; ++i)
+                r->h_psegs[i] = SegDev{p->seg_poff[i], p->seg_len[i], r->h_segs[i].dst};
         if (r->tables_used) II_HIP(hipStreamWaitEvent(s, r->tables_idle, 0));
         II_HIP(hipMemcpyAsync(r->d_segs, r->h_segs, S * sizeof(SegDev), hipMemcpyHostToDevice, s));
+        if (p->packed_distinct)
+            II_HIP(hipMemcpyAsync(r->d_psegs, r->h_psegs, S * sizeof(SegDev),
+                                  hipMemcpyHostToDevice, s));
         II_HIP(hipEventRecord(r->upload_done, s));
         r->uploaded = true;
     }
@@ -425,6 +454,9 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
     Runtime* r = p->rt;
     const uint8_t* blob = src.blob;
     const bool pinned = src.fd < 0 && is_pinned_host(blob);
+    // the host stage gathers packed chunks whenever it copies anyway
+    const bool packed = !pinned && p->packed_distinct;
+    const SegDev* segs = packed ? r->d_psegs : r->d_segs;
 
     const bool trace = p->trace;
     if (trace) {
@@ -443,11 +475,12 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         if (rc) return rc;
     }
 
-    const uint32_t D = r->depth, K = (uint32_t)p->num_chunks;
-    const uint64_t C = p->chunk_bytes, last_len = K ? p->chunk_len(K - 1) : 0;
-    // Chunk j of the ring is chunk live[j] of the plan; only the used range
-    // [u0, u1) of a chunk crosses the link, and it keeps its offsets in the
-    // slot, so the kernel reads the segments where the plan puts them.
+    const uint32_t D = r->depth;
+    const uint64_t C = p->chunk_bytes;
+    // Chunk j of the ring is chunk live[j] of the plan. Packed: the host
+    // stage gathers the chunk's segments back to back and only they cross
+    // the link. Otherwise (pinned blob) the used range [u0, u1) of the chunk
+    // crosses at its own offsets in the slot.
     const std::vector<uint32_t>& live = r->live;
     const uint32_t L = (uint32_t)live.size();
     std::unique_ptr<ReadAhead> ahead;
@@ -473,20 +506,29 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         const uint32_t k = live[j], slot = j % D;
         uint64_t u0, u1;
         p->chunk_used(k, &u0, &u1);
-        const uint64_t len = u1 - u0;
-        const uint64_t at = p->lo + (uint64_t)k * C + u0;  // blob / file offset of the bytes
+        const uint64_t cbeg = p->lo + (uint64_t)k * C;  // blob / file offset of the chunk
+        const uint64_t at = cbeg + u0;                   // ... and of its used range
+        // packed: the slot receives the chunk's runs back to back from offset
+        // 0; otherwise the used range keeps its chunk offsets
+        const uint64_t r0 = p->chunk_run_begin[k], nr = p->chunk_run_begin[k + 1] - r0;
+        const uint64_t len = packed ? p->chunk_plen[k] : u1 - u0;
+        const uint64_t doff = packed ? 0 : u0;
         const uint8_t* from = blob ? blob + at : nullptr;
         if (!pinned) {
             // InDisk -> InMem: the pinned slot is free once its last copy finished
             if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
-            uint8_t* stage = r->hslot[slot] + u0;
+            uint8_t* stage = r->hslot[slot] + doff;
+            const uint32_t *ro = p->run_off.data() + r0, *rp = p->run_poff.data() + r0,
+                           *rl = p->run_len.data() + r0;
             if (src.fd < 0) {
-                r->pool->copy(stage, from, len);
+                if (packed) r->pool->gather(stage, blob + cbeg, 0, ro, rp, rl, nr, len);
+                else r->pool->copy(stage, from, len);
             } else if (!src.direct) {
-                const int err = r->pool->read(src.fd, stage, at, len, 1, len);
+                const int err = packed ? r->pool->read_gather(src.fd, stage, cbeg, ro, rp, rl, nr, len)
+                                       : r->pool->read(src.fd, stage, at, len, 1, len);
                 if (err)
                     return fail(II_EIO, "reading chunk %u (file bytes %llu..%llu): %s", k,
-                                (unsigned long long)at, (unsigned long long)(at + len),
+                                (unsigned long long)at, (unsigned long long)(cbeg + u1),
                                 strerror(err));
             } else {
                 // direct I/O: whole blocks, read ahead into aligned buffers;
@@ -496,7 +538,11 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
                 if (!b)
                     return fail(II_EIO, "reading chunk %u (file bytes from %llu): %s", k,
                                 (unsigned long long)(at & ~(kIoAlign - 1)), strerror(err));
-                r->pool->copy(stage, b + (at & (kIoAlign - 1)), len);
+                const uint64_t a = at & ~(kIoAlign - 1);  // file offset of b[0]
+                if (packed)  // b[0] is chunk offset a - cbeg (may be negative)
+                    r->pool->gather(stage, b, (int64_t)(a - cbeg), ro, rp, rl, nr, len);
+                else
+                    r->pool->copy(stage, b + (at - a), len);
                 ahead->release(j);
             }
             from = stage;
@@ -505,15 +551,16 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         hipStream_t cs = r->copy_s[j % r->ncopy];
         if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(cs, r->scatter_done[slot], 0));
         if (trace) II_HIP(hipEventRecord(r->tr_cs[j], cs));
-        II_HIP(hipMemcpyAsync(r->dslot[slot] + u0, from, len, hipMemcpyHostToDevice, cs));
+        II_HIP(hipMemcpyAsync(r->dslot[slot] + doff, from, len, hipMemcpyHostToDevice, cs));
         II_HIP(hipEventRecord(r->copy_done[slot], cs));
         if (trace) II_HIP(hipEventRecord(r->tr_ce[j], cs));
         r->copy_rec[slot] = 1;
         // InGPU -> tensors Loaded, then the slot is released
         II_HIP(hipStreamWaitEvent(r->scatter_s, r->copy_done[slot], 0));
         if (trace) II_HIP(hipEventRecord(r->tr_ss[j], r->scatter_s));
-        II_HIP(launch_scatter_slot(r->dslot[slot], k, r->d_segs, r->d_tiles, C, last_len, K,
-                                   p->tiles_per_chunk, p->tile_bytes, r->scatter_s));
+        const uint64_t t0 = p->chunk_tile_begin[k], nt = p->chunk_tile_begin[k + 1] - t0;
+        II_HIP(launch_scatter_slot(r->dslot[slot], r->d_tiles + t0, r->d_wins + t0, (uint32_t)nt,
+                                   segs, packed, p->tile_bytes, p->chunk_plen[k], r->scatter_s));
         II_HIP(hipEventRecord(r->scatter_done[slot], r->scatter_s));
         if (trace) II_HIP(hipEventRecord(r->tr_se[j], r->scatter_s));
         r->scatter_rec[slot] = 1;
@@ -536,12 +583,10 @@ static int run_device(ii_plan_t* p, const uint8_t* image, const uint64_t* dst, h
     const uint64_t ib = reinterpret_cast<uint64_t>(image);
     rc = prepare_segments(p, dst, stream, ib + p->lo, ib + p->hi);
     if (rc) return rc;
-    const uint32_t K = (uint32_t)p->num_chunks;
-    if (K) {
-        II_HIP(launch_scatter_image(image + p->lo, r->d_segs, r->d_tiles, p->chunk_bytes,
-                                    p->chunk_len(K - 1), K, p->tiles_per_chunk, p->tile_bytes,
-                                    stream));
-    }
+    const uint64_t last_len = p->num_chunks ? p->chunk_len(p->num_chunks - 1) : 0;
+    II_HIP(launch_scatter_image(image + p->lo, r->d_tiles, r->d_wins, r->d_tile_chunk,
+                                p->tiles.size(), (uint32_t)p->num_chunks, p->tiles_per_chunk,
+                                r->d_segs, p->chunk_bytes, last_len, p->tile_bytes, stream));
     II_HIP(hipEventRecord(r->tables_idle, stream));
     r->tables_used = true;
     return II_OK;

@@ -8,9 +8,13 @@
 // movement, bound by HBM bandwidth: per payload byte one read of the chunk
 // and one write of the tensor.
 //
-// Work split. A chunk is cut into tiles of tile_bytes; one 256-thread
-// workgroup owns one tile. The planner stores, per tile, the window of
-// segment rows whose bytes meet it, so a workgroup reads only its own rows.
+// Work split. A chunk's segment bytes are cut into tiles of tile_bytes, in
+// segment order with gaps between segments skipped; one 256-thread
+// workgroup owns one tile. The planner stores, per tile, the segment rows
+// whose bytes meet it and the tile's window of chunk offsets, so a
+// workgroup reads only its own rows, and no workgroup is launched for bytes
+// no tensor needs (the gaps a sharded table leaves in the file). In a
+// packed staging slot the window is simply the tile's share of slot offsets.
 //
 // Units. Destination memory is written in 16-byte blocks aligned to 16
 // bytes, so every store of a block that a segment covers completely is one
@@ -89,28 +93,24 @@ __device__ __forceinline__ uint32_t wave_scan(uint32_t v) {
 
 }  // namespace
 
-// One workgroup's share of the scatter: tile t of chunk k, whose bytes start
-// at device address cbase.
-__device__ __forceinline__ void scatter_tile(uint64_t cbase, uint32_t k, uint32_t t,
-                                             const SegDev* __restrict__ segs,
-                                             const TileDev* __restrict__ tiles,
-                                             uint64_t chunk_bytes, uint64_t last_len,
-                                             uint32_t num_chunks, uint32_t tpc,
-                                             uint32_t tile_bytes) {
+// One workgroup's share of the scatter: the units anchored in the window
+// [w0, w1) of offsets from device address cbase, among segments [s_first,
+// s_last). Every tile holds segment bytes, so s_first < s_last (the planner
+// guarantees it); the batch loop runs at least once with no guard, which
+// lets the argument loads issue together with the tile's own.
+__device__ __forceinline__ void scatter_tile(uint64_t cbase, uint64_t w0, uint64_t w1,
+                                             uint32_t s_first, uint32_t s_last,
+                                             const SegDev* __restrict__ segs) {
     __shared__ SegRow rows[kMaxSegBatch];
     __shared__ uint32_t pre[kMaxSegBatch];
     __shared__ uint32_t wsum[kBlock / 64];
 
     const uint32_t tid = threadIdx.x;
-    const uint64_t clen = (k + 1 == num_chunks) ? last_len : chunk_bytes;
-    const uint64_t w0 = (uint64_t)t * tile_bytes;
-    if (k >= num_chunks || w0 >= clen) return;  // uniform across the workgroup
-    const uint64_t w1 = min(clen, w0 + tile_bytes);
-    const TileDev td = tiles[(uint64_t)k * tpc + t];
     DevMem mem;
 
-    for (uint32_t s0 = td.first; s0 < td.last; s0 += kMaxSegBatch) {
-        const uint32_t ns = min((uint32_t)kMaxSegBatch, td.last - s0);
+    uint32_t s0 = s_first;
+    do {
+        const uint32_t ns = min((uint32_t)kMaxSegBatch, s_last - s0);
         uint32_t cnt = 0;
         if (tid < ns) {
             const SegDev sd = segs[s0 + tid];
@@ -153,29 +153,63 @@ __device__ __forceinline__ void scatter_tile(uint64_t cbase, uint32_t k, uint32_
                 if (io[j].c1 > io[j].c0) store_unit(mem, io[j].d, v[j], io[j].c0, io[j].c1);
         }
         __syncthreads();  // rows/pre are rewritten by the next batch
-    }
+        s0 += kMaxSegBatch;
+    } while (s0 < s_last);
 }
 
-// Ring path: chunk k, staged in a device slot that starts at `slot`. One
-// workgroup per tile of the chunk.
+// Ring path: one chunk, staged in a device slot that starts at `slot`; one
+// workgroup per tile of the chunk (`tiles` and `wins` point at the chunk's
+// first). Packed slot: tile m takes slot offsets [m * tile_bytes, ...) up to
+// plen; otherwise the slot holds the chunk at its own offsets and the tile's
+// window of chunk offsets applies.
 __global__ __launch_bounds__(kBlock) void scatter_slot(
-    const uint8_t* __restrict__ slot, uint32_t k, const SegDev* __restrict__ segs,
-    const TileDev* __restrict__ tiles, uint64_t chunk_bytes, uint64_t last_len,
-    uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes) {
-    scatter_tile(reinterpret_cast<uint64_t>(slot), k, blockIdx.x, segs, tiles, chunk_bytes,
-                 last_len, num_chunks, tpc, tile_bytes);
+    const uint8_t* __restrict__ slot, const TileDev* __restrict__ tiles,
+    const TileWin* __restrict__ wins, const SegDev* __restrict__ segs, uint32_t packed,
+    uint32_t tile_bytes, uint64_t plen) {
+    const uint32_t g = blockIdx.x;
+    const TileDev td = tiles[g];
+    uint64_t w0, w1;
+    if (packed) {
+        w0 = (uint64_t)g * tile_bytes;
+        w1 = min(plen, w0 + tile_bytes);
+    } else {
+        const TileWin tw = wins[g];
+        w0 = tw.w0;
+        w1 = tw.w1;
+    }
+    scatter_tile(reinterpret_cast<uint64_t>(slot), w0, w1, td.first, td.last, segs);
 }
 
-// Resident-image path: every chunk in one launch; `span` is the device address
-// of the blob's span byte lo, so chunk k starts at span + k * chunk_bytes.
-// Workgroup g handles tile g % tpc of chunk g / tpc.
+// Resident-image path: every tile of every chunk in one launch; `span` is the
+// device address of the blob's span byte lo, so chunk k starts at span +
+// k * chunk_bytes. When the segments of every chunk fill it with no gap (a
+// table whose tensors tile their span), every chunk but the last has
+// per_chunk = ceil(chunk_bytes / tile_bytes) tiles, tile g is tile
+// g % per_chunk of chunk g / per_chunk, and its window is that share of the
+// chunk, so only the 8-byte segment range is read; otherwise (per_chunk = 0)
+// the chunk index and the window are read too.
 __global__ __launch_bounds__(kBlock) void scatter_image(
-    const uint8_t* __restrict__ span, const SegDev* __restrict__ segs,
-    const TileDev* __restrict__ tiles, uint64_t chunk_bytes, uint64_t last_len,
-    uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes) {
-    const uint32_t k = blockIdx.x / tpc, t = blockIdx.x % tpc;
-    scatter_tile(reinterpret_cast<uint64_t>(span) + (uint64_t)k * chunk_bytes, k, t, segs, tiles,
-                 chunk_bytes, last_len, num_chunks, tpc, tile_bytes);
+    const uint8_t* __restrict__ span, const TileDev* __restrict__ tiles,
+    const TileWin* __restrict__ wins, const uint32_t* __restrict__ tile_chunk,
+    const SegDev* __restrict__ segs, uint64_t chunk_bytes, uint64_t last_len,
+    uint32_t num_chunks, uint32_t per_chunk, uint32_t tile_bytes) {
+    const uint32_t g = blockIdx.x;
+    const TileDev td = tiles[g];
+    uint32_t k;
+    uint64_t w0, w1;
+    if (per_chunk) {
+        k = g / per_chunk;
+        const uint64_t clen = (k + 1 == num_chunks) ? last_len : chunk_bytes;
+        w0 = (uint64_t)(g - k * per_chunk) * tile_bytes;
+        w1 = min(clen, w0 + tile_bytes);
+    } else {
+        k = tile_chunk[g];
+        const TileWin tw = wins[g];
+        w0 = tw.w0;
+        w1 = tw.w1;
+    }
+    const uint64_t cbase = reinterpret_cast<uint64_t>(span) + (uint64_t)k * chunk_bytes;
+    scatter_tile(cbase, w0, w1, td.first, td.last, segs);
 }
 
 // Zero the byte ranges [r.begin, r.end) (device addresses). One workgroup per
@@ -197,24 +231,24 @@ __global__ __launch_bounds__(kBlock) void zero_ranges(const RangeDev* __restrict
     }
 }
 
-hipError_t launch_scatter_slot(const uint8_t* slot, uint32_t k, const SegDev* segs,
-                               const TileDev* tiles, uint64_t chunk_bytes, uint64_t last_len,
-                               uint32_t num_chunks, uint32_t tpc, uint32_t tile_bytes,
-                               hipStream_t stream) {
-    if (tpc == 0) return hipSuccess;
-    hipLaunchKernelGGL(scatter_slot, dim3(tpc), dim3(kBlock), 0, stream, slot, k, segs, tiles,
-                       chunk_bytes, last_len, num_chunks, tpc, tile_bytes);
+hipError_t launch_scatter_slot(const uint8_t* slot, const TileDev* tiles, const TileWin* wins,
+                               uint32_t ntiles, const SegDev* segs, bool packed,
+                               uint32_t tile_bytes, uint64_t plen, hipStream_t stream) {
+    if (ntiles == 0) return hipSuccess;
+    hipLaunchKernelGGL(scatter_slot, dim3(ntiles), dim3(kBlock), 0, stream, slot, tiles, wins,
+                       segs, packed ? 1u : 0u, tile_bytes, plen);
     return hipGetLastError();
 }
 
-hipError_t launch_scatter_image(const uint8_t* span, const SegDev* segs, const TileDev* tiles,
-                                uint64_t chunk_bytes, uint64_t last_len, uint32_t num_chunks,
-                                uint32_t tpc, uint32_t tile_bytes, hipStream_t stream) {
-    const uint64_t blocks = (uint64_t)num_chunks * tpc;
-    if (blocks == 0) return hipSuccess;
-    if (blocks > 0x7fffffffull) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(scatter_image, dim3((uint32_t)blocks), dim3(kBlock), 0, stream, span, segs,
-                       tiles, chunk_bytes, last_len, num_chunks, tpc, tile_bytes);
+hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const TileWin* wins,
+                                const uint32_t* tile_chunk, uint64_t ntiles, uint32_t num_chunks,
+                                uint32_t per_chunk, const SegDev* segs, uint64_t chunk_bytes,
+                                uint64_t last_len, uint32_t tile_bytes, hipStream_t stream) {
+    if (ntiles == 0) return hipSuccess;
+    if (ntiles > 0x7fffffffull) return hipErrorInvalidConfiguration;
+    hipLaunchKernelGGL(scatter_image, dim3((uint32_t)ntiles), dim3(kBlock), 0, stream, span, tiles,
+                       wins, tile_chunk, segs, chunk_bytes, last_len, num_chunks, per_chunk,
+                       tile_bytes);
     return hipGetLastError();
 }
 

@@ -77,9 +77,10 @@ for _n in ("ii_plan_chunk_bytes", "ii_plan_payload_bytes", "ii_plan_arena_bytes"
     _sig(_n, _u64, _vp)
 _sig("ii_plan_span", None, _vp, _P(_u64), _P(_u64))
 _sig("ii_plan_tensors", _c.c_int, _vp, _vp, _vp)
+_sig("ii_plan_packing", _c.c_int, _vp, _vp, _vp)
 _sig("ii_plan_chunks", _c.c_int, _vp, _vp, _vp, _vp)
 _sig("ii_plan_segments", _c.c_int, _vp, _vp, _vp, _vp, _vp, _vp)
-_sig("ii_plan_tiles", _c.c_int, _vp, _P(_u32), _P(_u32), _vp, _vp)
+_sig("ii_plan_tiles", _c.c_int, _vp, _P(_u32), _P(_u64), _vp, _vp, _vp, _vp, _vp)
 _sig("ii_plan_tensor_name", _c.c_char_p, _vp, _sz)
 _sig("ii_host_alloc", _c.c_int, _u64, _P(_vp))
 _sig("ii_host_free", _c.c_int, _vp)
@@ -254,15 +255,29 @@ class Plan:
                                                       "tensor_off", "len"))), "ii_plan_segments")
         return out
 
-    def tiles(self) -> tuple[int, int, np.ndarray, np.ndarray]:
-        tb, tpc = _u32(), _u32()
-        _check(_lib.ii_plan_tiles(self.handle, _c.byref(tb), _c.byref(tpc), None, None),
+    def tiles(self) -> dict:
+        """The kernel's tiles: tile_bytes and, per tile, chunk, first, last,
+        w0, w1 (see ii_plan_tiles)."""
+        tb, nt = _u32(), _u64()
+        _check(_lib.ii_plan_tiles(self.handle, _c.byref(tb), _c.byref(nt), None, None, None,
+                                  None, None), "ii_plan_tiles")
+        g = nt.value
+        out = {f: np.zeros(g, np.uint32) for f in ("chunk", "first", "last", "w0", "w1")}
+        p = lambda a: a.ctypes.data if a.size else None  # noqa: E731
+        _check(_lib.ii_plan_tiles(self.handle, _c.byref(tb), _c.byref(nt), p(out["chunk"]),
+                                  p(out["first"]), p(out["last"]), p(out["w0"]), p(out["w1"])),
                "ii_plan_tiles")
-        g = self.num_chunks * tpc.value
-        first, last = np.zeros(g, np.uint32), np.zeros(g, np.uint32)
-        _check(_lib.ii_plan_tiles(self.handle, _c.byref(tb), _c.byref(tpc), first.ctypes.data,
-                                  last.ctypes.data), "ii_plan_tiles")
-        return tb.value, tpc.value, first, last
+        out["tile_bytes"] = tb.value
+        return out
+
+    def packing(self) -> dict:
+        """Packed staging layout: seg_off (per segment), chunk_len (per chunk)."""
+        out = dict(seg_off=np.zeros(self.num_segments, np.uint32),
+                   chunk_len=np.zeros(self.num_chunks, np.uint64))
+        p = lambda a: a.ctypes.data if a.size else None  # noqa: E731
+        _check(_lib.ii_plan_packing(self.handle, p(out["seg_off"]), p(out["chunk_len"])),
+               "ii_plan_packing")
+        return out
 
     def name(self, i: int) -> str:
         return _lib.ii_plan_tensor_name(self.handle, i).decode()

@@ -97,18 +97,27 @@ struct EmuMem {
 
 extern "C" {
 
-// Emulate every tile of every chunk. Segment rows and tile windows are the
-// plan's (as exported by the C-ABI); dst_addr are emulated destination
+// Emulate every tile, in the plan's tile order. Segment rows and tiles are
+// the plan's (as exported by the C-ABI); dst_addr are emulated destination
 // addresses inside [arena_base, arena_base + arena_len); src_base is the
 // emulated address of span byte lo (chunk k starts at src_base + k*C).
-// Returns 0 if every check held, else 1 with a message in err.
+// packed = 0: each tile's window [w0, w1) of chunk offsets applies, as in a
+// resident image; packed = 1: seg_off are packed slot offsets and tile m of
+// chunk k takes [m * tile_bytes, ...) up to chunk_plen[k], as in a packed
+// staging slot; per_chunk != 0 (resident image of a gap-free table): as the
+// kernel does, tile g is window g % per_chunk of chunk g / per_chunk and
+// tile_chunk / w0 / w1 are not read. Returns 0 if every check held, else 1
+// with a message in err.
 int emu_scatter(uint64_t num_chunks, uint64_t chunk_bytes, uint64_t lo, uint64_t hi,
                 const uint8_t* blob, const uint32_t* seg_off, const uint32_t* seg_len,
-                const uint32_t* seg_tensor, const uint64_t* seg_toff, uint32_t tile_bytes,
-                uint32_t tpc, const uint32_t* tile_first, const uint32_t* tile_last,
-                const uint64_t* tensor_dst, const uint64_t* tensor_nbytes, uint64_t ntensors,
-                uint64_t src_base, uint64_t arena_base, uint64_t arena_len, uint8_t* arena,
-                uint32_t batch, char* err, int errlen, uint64_t* stats) {
+                const uint32_t* seg_tensor, const uint64_t* seg_toff, uint64_t ntiles,
+                const uint32_t* tile_chunk, const uint32_t* tile_first, const uint32_t* tile_last,
+                const uint32_t* tile_w0, const uint32_t* tile_w1, int packed, uint32_t per_chunk,
+                uint32_t tile_bytes,
+                const uint64_t* chunk_plen, const uint64_t* tensor_dst,
+                const uint64_t* tensor_nbytes, uint64_t ntensors, uint64_t src_base,
+                uint64_t arena_base, uint64_t arena_len, uint8_t* arena, uint32_t batch, char* err,
+                int errlen, uint64_t* stats) {
     EmuMem m;
     m.blob = blob;
     m.lo = lo;
@@ -124,14 +133,31 @@ int emu_scatter(uint64_t num_chunks, uint64_t chunk_bytes, uint64_t lo, uint64_t
     if (batch > kMaxSegBatch) batch = kMaxSegBatch;
     std::vector<uint32_t> pre(batch), cnt(batch), srow(batch);
 
-    for (uint64_t k = 0; k < num_chunks && m.err.empty(); ++k) {
-        const uint64_t clen = (k + 1 == num_chunks) ? (hi - lo) - chunk_bytes * k : chunk_bytes;
+    uint64_t tile_in_chunk = 0;
+    for (uint64_t g = 0; g < ntiles && m.err.empty(); ++g) {
+        uint64_t k, w0, w1;
+        if (per_chunk) {
+            k = g / per_chunk;
+            const uint64_t clen =
+                (k + 1 == num_chunks) ? (hi - lo) - chunk_bytes * k : chunk_bytes;
+            w0 = (g - k * per_chunk) * (uint64_t)tile_bytes;
+            w1 = std::min<uint64_t>(clen, w0 + tile_bytes);
+        } else {
+            k = tile_chunk[g];
+            w0 = tile_w0[g];
+            w1 = tile_w1[g];
+        }
+        if (k >= num_chunks) {
+            m.bad("tile of a chunk out of range", k);
+            break;
+        }
+        tile_in_chunk = (g && tile_chunk[g - 1] == k) ? tile_in_chunk + 1 : 0;
         const uint64_t cbase = src_base + k * chunk_bytes;
-        for (uint32_t t = 0; t < tpc && m.err.empty(); ++t) {
-            const uint64_t w0 = (uint64_t)t * tile_bytes;
-            if (w0 >= clen) continue;
-            const uint64_t w1 = std::min<uint64_t>(clen, w0 + tile_bytes);
-            const uint64_t g = k * tpc + t;
+        if (packed) {
+            w0 = tile_in_chunk * tile_bytes;
+            w1 = std::min<uint64_t>(chunk_plen[k], w0 + tile_bytes);
+        }
+        {
             const uint32_t first = tile_first[g], last = tile_last[g];
             max_rows = std::max<uint64_t>(max_rows, last - first);
             for (uint32_t s0 = first; s0 < last && m.err.empty(); s0 += batch) {

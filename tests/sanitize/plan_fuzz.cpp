@@ -6,8 +6,8 @@
 // interleave -- plans them with several chunk sizes, reads every getter and
 // checks the structural invariants that need no oracle: segments tile each
 // tensor exactly, lie inside their chunk and inside one row, and are
-// ordered; tile windows are consistent; the copied bytes lie between the
-// payload and the span. Any sanitizer report or failed check exits non-zero.
+// ordered; tiles take tile_bytes of segment bytes each with contiguous
+// windows; the copied bytes lie between the payload and the span. Any sanitizer report or failed check exits non-zero.
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -131,10 +131,15 @@ int main(int argc, char** argv) {
             CHECK(ii_plan_tensors(p, nb.data(), off.data()) == 0);
             CHECK(ii_plan_chunks(p, cb.data(), cl.data(), sb.data()) == 0);
             CHECK(ii_plan_segments(p, sc.data(), so.data(), st.data(), sto.data(), sl.data()) == 0);
-            uint32_t tb = 0, tpc = 0;
-            CHECK(ii_plan_tiles(p, &tb, &tpc, nullptr, nullptr) == 0);
-            std::vector<uint32_t> tf((size_t)K * tpc), tl((size_t)K * tpc);
-            CHECK(ii_plan_tiles(p, &tb, &tpc, tf.data(), tl.data()) == 0);
+            uint32_t tb = 0;
+            uint64_t G = 0;
+            CHECK(ii_plan_tiles(p, &tb, &G, nullptr, nullptr, nullptr, nullptr, nullptr) == 0);
+            std::vector<uint32_t> tk(G), tf(G), tl(G), tw0(G), tw1(G);
+            CHECK(ii_plan_tiles(p, &tb, &G, tk.data(), tf.data(), tl.data(), tw0.data(),
+                                tw1.data()) == 0);
+            std::vector<uint32_t> spo(S);
+            std::vector<uint64_t> plen(K);
+            CHECK(ii_plan_packing(p, spo.data(), plen.data()) == 0);
             for (size_t i = 0; i < N; ++i) (void)ii_plan_tensor_name(p, i);
             uint64_t lo, hi;
             ii_plan_span(p, &lo, &hi);
@@ -163,13 +168,29 @@ int main(int argc, char** argv) {
             for (size_t i = 0; i < N; ++i) CHECK(covered[i] == nb[i]);
             CHECK(total == ii_plan_payload_bytes(p));
             CHECK(ii_plan_copy_bytes(p) >= total && ii_plan_copy_bytes(p) <= hi - lo);
+            for (size_t k = 0; k < K; ++k) CHECK(sb[k] <= sb[k + 1]);
+            // tiles: in chunk order; per chunk ceil(plen / tb) of them; windows
+            // contiguous from the first segment to the last segment's end;
+            // segment windows inside the chunk's segments and advancing
+            size_t g = 0;
             for (size_t k = 0; k < K; ++k) {
-                CHECK(sb[k] <= sb[k + 1]);
-                for (uint32_t x = 0; x < tpc; ++x) {
-                    const size_t g = k * tpc + x;
-                    CHECK(tf[g] <= tl[g] && tl[g] <= S);
+                uint64_t plen_k = 0;
+                for (uint64_t s = sb[k]; s < sb[k + 1]; ++s) {
+                    CHECK(spo[s] == plen_k);
+                    plen_k += sl[s];
+                }
+                CHECK(plen[k] == plen_k);
+                const uint64_t M = (plen_k + tb - 1) / tb;
+                for (uint64_t m = 0; m < M; ++m, ++g) {
+                    CHECK(g < G && tk[g] == k);
+                    CHECK(sb[k] <= tf[g] && tf[g] < tl[g] && tl[g] <= sb[k + 1]);
+                    CHECK(tw0[g] < tw1[g] && tw1[g] <= cl[k]);
+                    if (m == 0) CHECK(tw0[g] == so[sb[k]]);
+                    else CHECK(tw0[g] == tw1[g - 1] && tf[g] >= tf[g - 1]);
+                    if (m + 1 == M) CHECK(tw1[g] == so[sb[k + 1] - 1] + sl[sb[k + 1] - 1]);
                 }
             }
+            CHECK(g == G);
             ii_plan_free(p);
         }
     }

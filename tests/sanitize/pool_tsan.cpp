@@ -1,6 +1,7 @@
 // The host copy pool under ThreadSanitizer: many copies of varied sizes
 // (below and above the split threshold), several pool sizes, every byte
-// checked, and pools created and destroyed repeatedly.
+// checked, and pools created and destroyed repeatedly; file reads,
+// read-ahead, and gathers of many runs from memory and from a file.
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -100,6 +101,57 @@ int main() {
         if (err != EIO) {
             fprintf(stderr, "read-ahead past the end: err %d, want EIO\n", err);
             return 2;
+        }
+    }
+    // gathers: many runs (rows of a sharded tensor) from memory and from the
+    // file, split across threads by destination bytes; every byte checked
+    // against a one-run-at-a-time copy, nothing written past the end
+    {
+        std::vector<uint32_t> off, poff, len;
+        uint64_t s = 0, total = 0;
+        uint32_t x = 12345;
+        while (s < (8u << 20)) {
+            x = x * 1103515245u + 12345u;
+            const uint32_t gap = (x >> 8) % 700, run = 1 + (x >> 16) % 9000;
+            s += gap;
+            off.push_back((uint32_t)s);
+            poff.push_back((uint32_t)total);
+            len.push_back(run);
+            s += run;
+            total += run;
+        }
+        const int64_t skews[] = {0, (int64_t)off[0], -64};  // b0[0] at, past, before offset 0
+        for (uint32_t threads : {1u, 3u, 8u}) {
+            ii::CopyPool pool(threads);
+            for (int64_t skew : skews) {
+                std::vector<uint8_t> want(total);
+                // b0[0] holds source offset `skew`: source offset o is b0[o - skew]
+                const uint8_t* b0 = src.data() + 4096;
+                for (size_t r = 0; r < off.size(); ++r)
+                    memcpy(want.data() + poff[r], b0 + ((int64_t)off[r] - skew), len[r]);
+                std::fill(dst.begin(), dst.end(), 0xEE);
+                pool.gather(dst.data(), b0, skew, off.data(), poff.data(), len.data(), off.size(),
+                            total);
+                if (memcmp(dst.data(), want.data(), total) != 0 || dst[total] != 0xEE) {
+                    fprintf(stderr, "gather mismatch (threads %u skew %lld)\n", threads,
+                            (long long)skew);
+                    return 2;
+                }
+                if (skew) continue;
+                std::fill(dst.begin(), dst.end(), 0xEE);
+                const int err = pool.read_gather(fd, dst.data(), 4096, off.data(), poff.data(),
+                                                 len.data(), off.size(), total);
+                if (err || memcmp(dst.data(), want.data(), total) != 0 || dst[total] != 0xEE) {
+                    fprintf(stderr, "read_gather mismatch (threads %u err %d)\n", threads, err);
+                    return 2;
+                }
+                // a base past the end of the file: EIO
+                if (pool.read_gather(fd, dst.data(), fsz, off.data(), poff.data(), len.data(),
+                                     off.size(), total) != EIO) {
+                    fprintf(stderr, "read_gather past the end did not fail\n");
+                    return 2;
+                }
+            }
         }
     }
     close(fd);

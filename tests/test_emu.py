@@ -19,7 +19,7 @@ from paper_2607_18957_amd import ii, synth
 
 
 def _run(orc, table, *, chunk=None, arena_phase=0, src_phase=0, batch=256, dst_of=None,
-         tile=None, monkeypatch=None):
+         tile=None, monkeypatch=None, packed=False):
     if tile:
         monkeypatch.setenv("II_TILE_BYTES", str(tile))
     plan = ii.ii_plan(table, chunk or table.chunk_bytes)
@@ -31,7 +31,8 @@ def _run(orc, table, *, chunk=None, arena_phase=0, src_phase=0, batch=256, dst_o
     dst = base + rel
     can = synth.canary(arena_len)
     got = can.copy()
-    ok, msg, stats = emu.scatter(plan, blob, dst, base, got, (1 << 40) + src_phase, batch)
+    run = emu.scatter_packed if packed else emu.scatter
+    ok, msg, stats = run(plan, blob, dst, base, got, (1 << 40) + src_phase, batch)
     assert ok, msg
     want = can.copy()
     # the oracle arena, at the same (possibly shifted) offsets
@@ -147,6 +148,7 @@ def test_tp_shards(orc, size):
         t = synth.tiny_tp(rank, size)
         _run(orc, t)
         _run(orc, t, chunk=64 << 10, arena_phase=5, src_phase=3)
+        _run(orc, t, chunk=64 << 10, arena_phase=5, src_phase=3, packed=True)
 
 
 def test_interleaved_column_blocks_misaligned(orc):
@@ -159,4 +161,21 @@ def test_interleaved_column_blocks_misaligned(orc):
         nb = orc.nbytes(t)
         _, hi = orc.span_rows(nb, t.src_offset, orc.rows(t, nb), t.src_row_stride)
         t.blob = np.frombuffer(rng.randbytes(hi + 64), dtype=np.uint8).copy()
-        _run(orc, t, arena_phase=rng.randint(0, 15), src_phase=rng.randint(0, 15))
+        _run(orc, t, arena_phase=rng.randint(0, 15), src_phase=rng.randint(0, 15),
+             packed=bool(rng.randint(0, 1)))
+
+
+def test_packed_stress_with_gaps(orc):
+    """Every other tensor of the stress set: the gaps make the packed layout
+    differ from the chunk layout for contiguous tensors too."""
+    full = synth.stress(n=6000, chunk=1 << 18)
+    keep = list(range(0, full.n, 2))
+    t = oracle_pins._T(full.dtype[keep], [full.shapes[i] for i in keep], full.src_offset[keep],
+                       full.dst_align[keep])
+    t.chunk_bytes = full.chunk_bytes
+    t.blob = synth.blob(full)
+    plan = ii.ii_plan(t)
+    pk = plan.packing()
+    _, l, _ = plan.chunks()
+    assert (pk["chunk_len"] < l).any()
+    _run(orc, t, packed=True, arena_phase=7, src_phase=9)

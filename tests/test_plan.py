@@ -45,35 +45,67 @@ def _compare(orc, table, chunk=None):
     assert np.array_equal(np.diff(sb.astype(np.int64)),
                           np.bincount(op["seg_chunk"], minlength=plan.num_chunks))
     _check_tiles(plan, s, l)
+    pk = _check_packing(plan, s)
+    if np.array_equal(pk["chunk_len"], l):   # dense chunks: packing changes nothing
+        assert np.array_equal(pk["seg_off"], s["chunk_off"])
+        # and tile m of chunk k is the window [m*T, (m+1)*T) of the chunk
+        t = plan.tiles()
+        ch = t["chunk"].astype(np.int64)
+        first_of = np.searchsorted(ch, ch, side="left")
+        m = np.arange(ch.size) - first_of
+        assert np.array_equal(t["w0"].astype(np.int64), m * t["tile_bytes"])
+        # and the kernel may find chunk and window from the tile index alone
+        M = -(-plan.chunk_bytes // t["tile_bytes"])
+        assert np.array_equal(ch, np.arange(ch.size) // M)
+        assert np.array_equal(m, np.arange(ch.size) % M)
     return plan
 
 
 def _check_tiles(plan, s, chunk_len):
-    tb, tpc, first, last = plan.tiles()
-    assert tb % 16 == 0 and tpc == -(-plan.chunk_bytes // tb)
+    """Tiles, chunk by chunk: tile m of a chunk takes segment bytes [m*T,
+    (m+1)*T) in packed order (slot offsets) and meets exactly the segments
+    whose packed bytes meet that range; its window [w0, w1) of chunk offsets
+    holds exactly those bytes: windows are contiguous, start at the chunk's
+    first segment and end at its last segment's end."""
+    t = plan.tiles()
+    T = t["tile_bytes"]
+    assert T % 16 == 0
+    pk = plan.packing()
     _, _, sb = plan.chunks()
+    K = plan.num_chunks
+    ch = t["chunk"].astype(np.int64)
+    assert (np.diff(ch) >= 0).all()
+    counts = np.bincount(ch, minlength=K) if ch.size else np.zeros(K, np.int64)
+    starts = np.concatenate([[0], np.cumsum(counts)])
     off = s["chunk_off"].astype(np.int64)
-    end = off + s["len"].astype(np.int64)
-    for k in range(plan.num_chunks):
+    ln = s["len"].astype(np.int64)
+    poff = pk["seg_off"].astype(np.int64)
+    for k in range(K):
         a, b = int(sb[k]), int(sb[k + 1])
-        t = np.arange(tpc, dtype=np.int64)
-        w0 = t * tb
-        w1 = np.minimum(int(chunk_len[k]), w0 + tb)
-        live = w0 < int(chunk_len[k])
-        # segments meeting [w0, w1): end > w0 and off < w1 (rows are sorted and disjoint)
-        f = a + np.searchsorted(end[a:b], w0, side="right")
-        l = a + np.searchsorted(off[a:b], w1, side="left")
-        g = k * tpc + t
-        nonempty = live & (f < l)
-        assert np.array_equal(first[g[nonempty]], f[nonempty]), k
-        assert np.array_equal(last[g[nonempty]], l[nonempty]), k
-        empty = live & ~(f < l)
-        assert np.array_equal(first[g[empty]], last[g[empty]]), k
-        # brute force on a few windows
-        for tt in list(np.flatnonzero(live)[:3]) + list(np.flatnonzero(live)[-2:]):
-            meet = np.flatnonzero((off[a:b] < w1[tt]) & (end[a:b] > w0[tt])) + a
-            if meet.size:
-                assert (first[k * tpc + tt], last[k * tpc + tt]) == (meet[0], meet[-1] + 1)
+        plen = int(ln[a:b].sum())
+        assert int(pk["chunk_len"][k]) == plen
+        assert plen <= int(chunk_len[k])
+        M = -(-plen // T)
+        assert counts[k] == M, k
+        if not M:
+            continue
+        g = np.arange(starts[k], starts[k + 1])
+        P0 = np.arange(M, dtype=np.int64) * T
+        P1 = np.minimum(plen, P0 + T)
+        f = a + np.searchsorted(poff[a:b] + ln[a:b], P0, side="right")
+        l = a + np.searchsorted(poff[a:b], P1, side="left")
+        assert np.array_equal(t["first"][g], f), k
+        assert np.array_equal(t["last"][g], l), k
+        w0, w1 = t["w0"][g].astype(np.int64), t["w1"][g].astype(np.int64)
+        assert w0[0] == off[a] and w1[-1] == off[b - 1] + ln[b - 1]
+        assert np.array_equal(w0[1:], w1[:-1]) and (w1 > w0).all()
+        # segment bytes below chunk offset x, for every window edge
+        cum = np.concatenate([[0], np.cumsum(ln[a:b])])
+        def below(x):
+            j = np.searchsorted(off[a:b], x, side="right") - 1
+            jj = np.maximum(j, 0)
+            return np.where(j < 0, 0, cum[jj] + np.clip(x - off[a:b][jj], 0, ln[a:b][jj]))
+        assert np.array_equal(below(w1) - below(w0), P1 - P0), k
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama8b", "mistral7b", "llama70b"])
@@ -102,7 +134,7 @@ def test_small_tiles(orc, monkeypatch):
     monkeypatch.setenv("II_TILE_BYTES", "1024")
     t = synth.stress(n=3000, chunk=1 << 16)
     plan = _compare(orc, t)
-    assert plan.tiles()[0] == 1024
+    assert plan.tiles()["tile_bytes"] == 1024
 
 
 def test_exhaustive_tiny_tables(orc):
@@ -236,7 +268,23 @@ def _compare_rows(orc, table, chunk=None):
     assert sb[0] == 0 and sb[-1] == plan.num_segments
     assert plan.copy_bytes == _expected_copy_bytes(op)
     _check_tiles(plan, s, l)
+    _check_packing(plan, s)
     return plan
+
+
+def _check_packing(plan, s):
+    """Packed staging: within each chunk the segments sit back to back in
+    segment order from offset 0; a chunk stages the sum of its segment
+    lengths."""
+    pk = plan.packing()
+    _, _, sb = plan.chunks()
+    ln = s["len"].astype(np.int64)
+    for k in range(plan.num_chunks):
+        a, b = int(sb[k]), int(sb[k + 1])
+        want = np.concatenate([[0], np.cumsum(ln[a:b])])
+        assert np.array_equal(pk["seg_off"][a:b].astype(np.int64), want[:-1]), k
+        assert int(pk["chunk_len"][k]) == int(want[-1]), k
+    return pk
 
 
 @pytest.mark.parametrize("size", [1, 2, 4, 8])
