@@ -298,12 +298,23 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -
         lines.append(f"{name:<34}{r['Calls']:>7}{float(r['AverageNs']):>14.1f}"
                      f"{float(r['MinNs']):>12.0f}{float(r['MaxNs']):>12.0f}"
                      f"{float(r['Percentage']):>8.2f}")
-    img = [r for r in rows if r["Name"].startswith("ii::scatter_image")][0]
+    def named(n):
+        return [r for r in rows if r["Name"].split("(")[0] == n]
+    img = named("ii::scatter_image")[0]
     avg_ms = float(img["AverageNs"]) / 1e6
     lines += ["", f"scatter_image average per launch: {avg_ms:.4f} ms (rocprofv3)",
               f"bench.py HIP-event mean in the same run: {run['roofline']['kernel_ms']:.4f} ms",
               f"bench.py value in the same run: {run['value']:.1f} GB/s, "
               f"roofline frac {run['roofline']['frac']:.4f}"]
+    gaps = named("ii::scatter_image_gaps")
+    if gaps and "tp_shard" in run:
+        tp = run["tp_shard"]
+        lines += ["", f"scatter_image_gaps ({tp['table']}: rank 1 of 4 read out of the unsharded "
+                      f"file, {tp['payload_bytes']} B, {tp['segments']} segments) average per "
+                      f"launch: {float(gaps[0]['AverageNs']) / 1e6:.4f} ms (rocprofv3)",
+                  f"bench.py HIP-event mean in the same run: {tp['kernel']['ms']:.4f} ms, "
+                  f"{tp['kernel']['GBps']:.1f} GB/s algorithmic, frac "
+                  f"{tp['kernel']['frac_of_hbm_peak']:.4f}"]
     open(os.path.join(ROOT, "profiles", "scatter_image_llama8b_kernel_stats.txt"), "w").write(
         "\n".join(lines) + "\n")
 
@@ -315,7 +326,7 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -
     cal_kib = (4 << 30) / 1024
     f_scale = cal_kib / fetch[cal][0]
     w_scale = cal_kib / write[cal][0]
-    key = [k for k in fetch if k[0].startswith("ii::scatter_image")][0]
+    key = [k for k in fetch if k[0].split("(")[0] == "ii::scatter_image"][0]
     fetch_b = fetch[key][0] * 1024 * f_scale
     write_b = write[key][0] * 1024 * w_scale
     payload = run["config"]["payload_bytes"]
@@ -344,7 +355,21 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -
          f"(2 x payload {payload} + segment and tile tables)",
          f"  measured / algorithmic         {(fetch_b + write_b) / run['roofline']['bytes_per_launch']:.4f}",
          f"kernel source hash        {kernel_source_hash()}"]
-    slot = [k for k in fetch if k[0].startswith("ii::scatter_slot")]
+    gk = [k for k in fetch if k[0].split("(")[0] == "ii::scatter_image_gaps"]
+    if gk and "tp_shard" in run:
+        k = gk[0]
+        tp = run["tp_shard"]
+        gf, gw = fetch[k][0] * 1024 * f_scale, write[k][0] * 1024 * w_scale
+        alg = tp["kernel"]["bytes_per_launch"]
+        out["tp_shard"] = {"kernel": "scatter_image_gaps", "workload": tp["table"],
+                           "fetch_bytes": gf, "write_bytes": gw, "bytes_per_launch": gf + gw,
+                           "algorithmic_bytes": alg, "dispatches": fetch[k][1]}
+        json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
+        t += [f"scatter_image_gaps        {fetch[k][1]} dispatches (grid {k[1]}), {tp['table']}",
+              f"  FETCH_SIZE per dispatch {fetch[k][0]:.1f} KiB  -> {gf:.0f} B",
+              f"  WRITE_SIZE per dispatch {write[k][0]:.1f} KiB  -> {gw:.0f} B",
+              f"  measured / algorithmic         {(gf + gw) / alg:.4f} (algorithmic {alg} B)"]
+    slot = [k for k in fetch if k[0].split("(")[0] == "ii::scatter_slot"]
     if slot:
         k = slot[0]
         t += [f"scatter_slot (ring path)  {fetch[k][1]} dispatches, per 64 MiB chunk: "
@@ -428,11 +453,17 @@ def main() -> int:
     torch.cuda.synchronize(dev)
     tp_kms = statistics.mean(a.elapsed_time(b) for a, b in tev)
     tp_alg = 2 * tp_plan.payload_bytes + table_bytes(tp_plan)
+    tp_traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        rec = json.load(open(TRAFFIC_FILE))
+        if rec.get("kernel_source_hash") == kernel_source_hash() and "tp_shard" in rec:
+            tp_traffic = rec["tp_shard"]["bytes_per_launch"]
     tp.update(table=tp_t.name, tensors=tp_t.n, payload_bytes=tp_plan.payload_bytes,
               segments=tp_plan.num_segments, chunks=tp_plan.num_chunks,
               span_bytes=tp_plan.span[1] - tp_plan.span[0],
               pinned_copy_bytes=tp_plan.copy_bytes,
-              kernel={"ms": tp_kms, "GBps": tp_alg / (tp_kms * 1e-3) / 1e9,
+              kernel={"name": "scatter_image_gaps", "ms": tp_kms,
+                      "GBps": tp_alg / (tp_kms * 1e-3) / 1e9, "traffic": tp_traffic,
                       "frac_of_hbm_peak": tp_alg / (tp_kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
                       "bytes_per_launch": tp_alg})
     log(f"tp shard {tp_t.name}: kernel {tp_kms:.3f} ms, "

@@ -182,34 +182,37 @@ __global__ __launch_bounds__(kBlock) void scatter_slot(
 
 // Resident-image path: every tile of every chunk in one launch; `span` is the
 // device address of the blob's span byte lo, so chunk k starts at span +
-// k * chunk_bytes. When the segments of every chunk fill it with no gap (a
-// table whose tensors tile their span), every chunk but the last has
-// per_chunk = ceil(chunk_bytes / tile_bytes) tiles, tile g is tile
-// g % per_chunk of chunk g / per_chunk, and its window is that share of the
-// chunk, so only the 8-byte segment range is read; otherwise (per_chunk = 0)
-// the chunk index and the window are read too.
+// k * chunk_bytes. This kernel serves tables whose segments fill every chunk
+// with no gap: every chunk but the last has per_chunk = ceil(chunk_bytes /
+// tile_bytes) tiles, tile g is tile g % per_chunk of chunk g / per_chunk,
+// and its window is that share of the chunk, so a workgroup reads only its
+// 8-byte segment range.
 __global__ __launch_bounds__(kBlock) void scatter_image(
     const uint8_t* __restrict__ span, const TileDev* __restrict__ tiles,
-    const TileWin* __restrict__ wins, const uint32_t* __restrict__ tile_chunk,
     const SegDev* __restrict__ segs, uint64_t chunk_bytes, uint64_t last_len,
     uint32_t num_chunks, uint32_t per_chunk, uint32_t tile_bytes) {
     const uint32_t g = blockIdx.x;
     const TileDev td = tiles[g];
-    uint32_t k;
-    uint64_t w0, w1;
-    if (per_chunk) {
-        k = g / per_chunk;
-        const uint64_t clen = (k + 1 == num_chunks) ? last_len : chunk_bytes;
-        w0 = (uint64_t)(g - k * per_chunk) * tile_bytes;
-        w1 = min(clen, w0 + tile_bytes);
-    } else {
-        k = tile_chunk[g];
-        const TileWin tw = wins[g];
-        w0 = tw.w0;
-        w1 = tw.w1;
-    }
-    const uint64_t cbase = reinterpret_cast<uint64_t>(span) + (uint64_t)k * chunk_bytes;
-    scatter_tile(cbase, w0, w1, td.first, td.last, segs);
+    const uint32_t k = g / per_chunk;
+    const uint64_t clen = (k + 1 == num_chunks) ? last_len : chunk_bytes;
+    const uint64_t w0 = (uint64_t)(g - k * per_chunk) * tile_bytes;
+    const uint64_t w1 = min(clen, w0 + tile_bytes);
+    scatter_tile(reinterpret_cast<uint64_t>(span) + (uint64_t)k * chunk_bytes, w0, w1, td.first,
+                 td.last, segs);
+}
+
+// The resident-image path for tables with gaps between segments (tensor-
+// parallel shards read out of an unsharded file): tiles cover only segment
+// bytes, so each workgroup also reads its chunk index and its window.
+__global__ __launch_bounds__(kBlock) void scatter_image_gaps(
+    const uint8_t* __restrict__ span, const TileDev* __restrict__ tiles,
+    const TileWin* __restrict__ wins, const uint32_t* __restrict__ tile_chunk,
+    const SegDev* __restrict__ segs, uint64_t chunk_bytes) {
+    const uint32_t g = blockIdx.x;
+    const TileDev td = tiles[g];
+    const TileWin tw = wins[g];
+    const uint64_t cbase = reinterpret_cast<uint64_t>(span) + (uint64_t)tile_chunk[g] * chunk_bytes;
+    scatter_tile(cbase, tw.w0, tw.w1, td.first, td.last, segs);
 }
 
 // Zero the byte ranges [r.begin, r.end) (device addresses). One workgroup per
@@ -246,9 +249,12 @@ hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const
                                 uint64_t last_len, uint32_t tile_bytes, hipStream_t stream) {
     if (ntiles == 0) return hipSuccess;
     if (ntiles > 0x7fffffffull) return hipErrorInvalidConfiguration;
-    hipLaunchKernelGGL(scatter_image, dim3((uint32_t)ntiles), dim3(kBlock), 0, stream, span, tiles,
-                       wins, tile_chunk, segs, chunk_bytes, last_len, num_chunks, per_chunk,
-                       tile_bytes);
+    if (per_chunk)
+        hipLaunchKernelGGL(scatter_image, dim3((uint32_t)ntiles), dim3(kBlock), 0, stream, span,
+                           tiles, segs, chunk_bytes, last_len, num_chunks, per_chunk, tile_bytes);
+    else
+        hipLaunchKernelGGL(scatter_image_gaps, dim3((uint32_t)ntiles), dim3(kBlock), 0, stream,
+                           span, tiles, wins, tile_chunk, segs, chunk_bytes);
     return hipGetLastError();
 }
 
