@@ -110,9 +110,9 @@ typedef struct ii_plan_s ii_plan_t; /* opaque */
  * stride); chunk k covers [lo + k*chunk_bytes, min(lo + (k+1)*chunk_bytes,
  * hi)). A segment is one tensor's piece of one chunk (for a tensor given as
  * rows, one row's piece of one chunk), ordered by offset in the chunk.
- * The ring loads move, per chunk, only the bytes from its first segment's
- * start to its last segment's end (rounded out to 256 bytes), and skip chunks
- * that hold no segment; the total is ii_plan_copy_bytes.
+ * The ring loads skip chunks that hold no segment, and move of each other
+ * chunk only its segment bytes (gathered on the host) or the range from its
+ * first segment's start to its last segment's end (see ii_plan_copy_bytes).
  * Destination layout (used by ii_switch and by callers carving an arena): in
  * table order, tensor i starts at the smallest multiple of dst_align[i] at or
  * after the end of tensor i-1; arena_bytes is the end rounded up to the
@@ -289,11 +289,14 @@ size_t ii_plan_num_segments(const ii_plan_t* plan);
 uint64_t ii_plan_chunk_bytes(const ii_plan_t* plan);
 uint64_t ii_plan_payload_bytes(const ii_plan_t* plan); /* sum of nbytes */
 uint64_t ii_plan_arena_bytes(const ii_plan_t* plan);
-/* bytes one ii_load from a pinned blob moves from host to device: per chunk
- * that holds segments, its first segment's start to its last segment's end,
- * rounded out to 256-byte boundaries inside the chunk (hi - lo for a table
- * whose tensors tile their span). Loads from a pageable blob or a file
- * stage packed chunks and move payload_bytes. */
+/* bytes one ii_load from a pinned blob moves from host to device. Per chunk
+ * that holds segments: its used range -- first segment's start to last
+ * segment's end, rounded out to 256-byte boundaries inside the chunk --
+ * which is copied in place, unless more than a quarter of that range is
+ * gaps between segments; such a chunk is gathered through the staging slot
+ * and moves only its segment bytes. hi - lo for a table whose tensors tile
+ * their span. Loads from a pageable blob or a file gather every chunk with
+ * gaps and move payload_bytes. */
 uint64_t ii_plan_copy_bytes(const ii_plan_t* plan);
 /* Packed staging layout (loads from a pageable blob or a file gather only
  * the segments' bytes of a chunk into its pinned slot, back to back in

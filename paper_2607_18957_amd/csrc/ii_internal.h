@@ -1,4 +1,4 @@
-// Internal declarations shared by the planner, the runtime and the kernels.
+// Internal declarations shared by the planner and the runtime.
 #pragma once
 
 #include <algorithm>
@@ -10,47 +10,11 @@
 
 #include "ii.h"
 #include "scatter_math.h"
+#include "scatter_types.h"
 
 namespace ii {
 
-// One segment as the scatter kernel reads it: a piece of one tensor inside
-// one chunk. 16 bytes so a wave loads its rows with dwordx4 loads.
-struct SegDev {
-    uint32_t off;  // offset of the piece inside its chunk
-    uint32_t len;  // bytes
-    uint64_t dst;  // device address the piece's first byte goes to
-};
-static_assert(sizeof(SegDev) == 16, "SegDev must stay 16 bytes");
-
-// Work split of a chunk: tile m of a chunk takes the chunk's segment bytes
-// [m * tile_bytes, (m+1) * tile_bytes) in segment order ("packed" offsets:
-// a segment's bytes counted from the chunk's first segment, gaps between
-// segments skipped). In a packed staging slot that is exactly the window
-// [m * tile_bytes, ...) of the slot; in the chunk itself (a resident image,
-// or a slot holding the chunk's bytes at their own offsets) the same bytes
-// form the window [w0, w1) of chunk offsets. Either way the tile meets the
-// segments [first, last). A chunk without segments has no tiles.
-struct TileDev {
-    uint32_t first;
-    uint32_t last;
-};
-static_assert(sizeof(TileDev) == 8, "TileDev must stay 8 bytes");
-// The tile's window [w0, w1) of chunk offsets, kept apart from TileDev so
-// that launches whose windows follow from the tile index read only 8 bytes
-// per tile.
-struct TileWin {
-    uint32_t w0;
-    uint32_t w1;
-};
-static_assert(sizeof(TileWin) == 8, "TileWin must stay 8 bytes");
-
-// Zero-fill range for the switch scrub: [begin, end) as device addresses.
-struct RangeDev {
-    uint64_t begin;
-    uint64_t end;
-};
-
-constexpr uint32_t kDefaultTile = 8u << 10;  // bytes of chunk per workgroup (<= kMaxTile)
+constexpr uint32_t kDefaultTile = 8u << 10;  // segment bytes per workgroup (<= kMaxTile)
 constexpr uint32_t kMaxCopyStreams = 2;       // host-to-device copy streams of a ring
 constexpr uint64_t kIoAlign = 4096;           // block alignment of direct-I/O file reads
 constexpr uint64_t kCopyAlign = 256;          // host-to-device copies start and end on these
@@ -78,7 +42,7 @@ struct ii_plan_s {
     std::vector<uint64_t> dst_offset;
     uint64_t payload = 0, arena_bytes = 0, max_align = 1;
     uint64_t lo = 0, hi = 0;
-    uint64_t copy_bytes = 0;  // host-to-device bytes per load (used range of each chunk)
+    uint64_t copy_bytes = 0;  // host-to-device bytes of a load from a pinned blob
     uint64_t chunk_bytes = 0;
     size_t num_chunks = 0;
     std::vector<uint64_t> chunk_seg_begin;  // num_chunks + 1
@@ -93,6 +57,10 @@ struct ii_plan_s {
     // adjacent in the chunk (one memcpy): chunk offset run_off, slot offset
     // run_poff, run_len.
     bool packed_distinct = false;  // false: packed layout == chunk layout for every chunk
+    // per chunk: a load from a pinned blob gathers this chunk through the
+    // staging slot too (its used range is more than a quarter gaps), instead
+    // of copying the used range in place
+    std::vector<uint8_t> chunk_gather_pinned;
     std::vector<uint32_t> seg_poff;
     std::vector<uint64_t> chunk_plen;
     std::vector<uint64_t> chunk_run_begin;  // num_chunks + 1

@@ -270,11 +270,6 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         std::vector<Piece>().swap(pieces);
         for (size_t k = 0; k < p->num_chunks; ++k)
             p->chunk_seg_begin[k + 1] += p->chunk_seg_begin[k];
-        for (size_t k = 0; k < p->num_chunks; ++k) {
-            uint64_t b, e;
-            p->chunk_used(k, &b, &e);
-            p->copy_bytes += e - b;
-        }
 
         // 5. packed staging layout and gather runs
         p->seg_poff.resize(S);
@@ -299,6 +294,16 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
             p->chunk_plen[k] = pos;
             if (pos != p->chunk_len(k)) p->packed_distinct = true;
             p->chunk_run_begin[k + 1] = p->run_len.size();
+        }
+        // pinned blobs: copy a chunk's used range in place unless more than a
+        // quarter of it is gaps, then gather it like a pageable chunk
+        p->chunk_gather_pinned.assign(p->num_chunks, 0);
+        for (size_t k = 0; k < p->num_chunks; ++k) {
+            uint64_t b, e;
+            p->chunk_used(k, &b, &e);
+            const bool gather = p->packed_distinct && 4 * (e - b - p->chunk_plen[k]) > (e - b);
+            p->chunk_gather_pinned[k] = gather;
+            p->copy_bytes += gather ? p->chunk_plen[k] : e - b;
         }
 
         // 6. tiles: per chunk, tile_bytes of segment bytes each (packed

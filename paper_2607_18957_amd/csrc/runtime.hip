@@ -454,9 +454,8 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
     Runtime* r = p->rt;
     const uint8_t* blob = src.blob;
     const bool pinned = src.fd < 0 && is_pinned_host(blob);
-    // the host stage gathers packed chunks whenever it copies anyway
-    const bool packed = !pinned && p->packed_distinct;
-    const SegDev* segs = packed ? r->d_psegs : r->d_segs;
+    // The host stage gathers packed chunks whenever it copies anyway, and
+    // for a pinned blob also where most of a chunk's used range is gaps.
 
     const bool trace = p->trace;
     if (trace) {
@@ -508,13 +507,15 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         p->chunk_used(k, &u0, &u1);
         const uint64_t cbeg = p->lo + (uint64_t)k * C;  // blob / file offset of the chunk
         const uint64_t at = cbeg + u0;                   // ... and of its used range
+        const bool packed = p->packed_distinct && (!pinned || p->chunk_gather_pinned[k]);
+        const bool staged = !pinned || packed;           // through the pinned slot
         // packed: the slot receives the chunk's runs back to back from offset
         // 0; otherwise the used range keeps its chunk offsets
         const uint64_t r0 = p->chunk_run_begin[k], nr = p->chunk_run_begin[k + 1] - r0;
         const uint64_t len = packed ? p->chunk_plen[k] : u1 - u0;
         const uint64_t doff = packed ? 0 : u0;
         const uint8_t* from = blob ? blob + at : nullptr;
-        if (!pinned) {
+        if (staged) {
             // InDisk -> InMem: the pinned slot is free once its last copy finished
             if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
             uint8_t* stage = r->hslot[slot] + doff;
@@ -560,7 +561,8 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         if (trace) II_HIP(hipEventRecord(r->tr_ss[j], r->scatter_s));
         const uint64_t t0 = p->chunk_tile_begin[k], nt = p->chunk_tile_begin[k + 1] - t0;
         II_HIP(launch_scatter_slot(r->dslot[slot], r->d_tiles + t0, r->d_wins + t0, (uint32_t)nt,
-                                   segs, packed, p->tile_bytes, p->chunk_plen[k], r->scatter_s));
+                                   packed ? r->d_psegs : r->d_segs, packed, p->tile_bytes,
+                                   p->chunk_plen[k], r->scatter_s));
         II_HIP(hipEventRecord(r->scatter_done[slot], r->scatter_s));
         if (trace) II_HIP(hipEventRecord(r->tr_se[j], r->scatter_s));
         r->scatter_rec[slot] = 1;

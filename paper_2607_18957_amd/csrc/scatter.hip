@@ -42,8 +42,8 @@
 // never read-modify-written.
 #include <hip/hip_runtime.h>
 
-#include "ii_internal.h"
 #include "scatter_math.h"
+#include "scatter_types.h"
 
 namespace ii {
 

@@ -231,15 +231,21 @@ def test_empty_plan():
 # -- tables given as rows (tensor-parallel shards) ----------------------------
 
 def _expected_copy_bytes(op, align=256):
-    """Per chunk that holds segments: first segment start to last segment
-    end, rounded out to `align` inside the chunk."""
+    """Bytes a load from a pinned blob moves: per chunk that holds segments,
+    the used range (first segment start to last segment end, rounded out to
+    `align` inside the chunk), or only the segment bytes where more than a
+    quarter of the used range is gaps (when any chunk of the table has
+    gaps)."""
     total = 0
     ch, off, ln = op["seg_chunk"], op["seg_chunk_off"].astype(np.int64), op["seg_len"].astype(np.int64)
+    dense = all(int(ln[ch == k].sum()) == int(op["chunk_len"][k])
+                for k in range(len(op["chunk_len"])))
     for k in np.unique(ch):
         m = ch == k
         b = int(off[m].min()) // align * align
         e = min(int(op["chunk_len"][k]), -(-int((off[m] + ln[m]).max()) // align) * align)
-        total += e - b
+        payload = int(ln[m].sum())
+        total += payload if (not dense and 4 * (e - b - payload) > e - b) else e - b
     return total
 
 
