@@ -255,6 +255,140 @@ def cpu_baseline(table, blob, budget_s: float = 12.0, max_passes: int = 4) -> di
                       f"{len(cores)} host cores"}
 
 
+def oracle_sample(table, blob, max_bytes: int, budget_s: float = 8.0) -> dict:
+    """The CPU oracle on one core over the table's first tensors up to
+    max_bytes (the whole table if it is smaller), passes until the budget is
+    used."""
+    import oracle
+    orc = oracle.default()
+    nb = orc.nbytes(table)
+    k = int(np.searchsorted(np.cumsum(nb.astype(np.int64)), max_bytes, side="right"))
+    k = max(1, min(table.n, k))
+    sub_nb, sub_src, sub_al = nb[:k], table.src_offset[:k], table.dst_align[:k]
+    payload = int(sub_nb.sum())
+    cores = os.sched_getaffinity(0)
+    os.sched_setaffinity(0, {min(cores)})
+    try:
+        passes, t0 = 0, time.perf_counter()
+        while passes == 0 or (time.perf_counter() - t0 < budget_s and passes < 1000):
+            orc.load_alloc_timed(sub_nb, sub_src, sub_al, blob)
+            passes += 1
+        dt = time.perf_counter() - t0
+    finally:
+        os.sched_setaffinity(0, cores)
+    return {"GBps": payload * passes / dt / 1e9, "tensors_per_s": k * passes / dt, "cores": 1,
+            "sample": f"first {k} of {table.n} tensors ({payload} B) x {passes} passes, "
+                      f"{dt:.1f} s on 1 of {len(cores)} host cores"}
+
+
+def all_configs(torch, dev, ii, synth) -> dict:
+    """Every workload of the build, one after another in one process: the
+    scatter kernel from a resident image (HIP events), end to end from a
+    pageable and a pinned blob, and the CPU oracle on one core beside them."""
+    stream = torch.cuda.current_stream(dev)
+    h2d = h2d_peak(torch, dev, 64 << 20)
+    out = {"h2d_peak_GBps": h2d["GBps"], "hbm_peak_GBps": HBM_PEAK_GBPS, "configs": {}}
+
+    def kernel_ms(plan, image, dst, reps):
+        for _ in range(3):
+            ii.ii_load_device(plan, image, dst, stream)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for a, b in ev:
+            a.record(stream)
+            ii.ii_load_device(plan, image, dst, stream)
+            b.record(stream)
+        torch.cuda.synchronize(dev)
+        return statistics.mean(a.elapsed_time(b) for a, b in ev)
+
+    def e2e(plan, src, dst, reps, fn=None):
+        fn = fn or ii.ii_load
+        times = []
+        for _ in range(reps):
+            t1 = time.perf_counter()
+            fn(plan, src, dst, stream)
+            torch.cuda.synchronize(dev)
+            times.append(time.perf_counter() - t1)
+        return times
+
+    def rate(plan, t):
+        return {"GBps": plan.payload_bytes / t / 1e9, "tensors_per_s": plan.num_tensors / t,
+                "frac_of_h2d_peak": plan.payload_bytes / t / 1e9 / h2d["GBps"], "s": t}
+
+    for cid, make, reps, osample in (("C0", synth.tiny, 20, 1 << 40),
+                                     ("C2", synth.stress, 5, 1 << 40),
+                                     ("C1", synth.llama8b, 5, 4 << 30),
+                                     ("C3", synth.llama70b, 1, 4 << 30)):
+        t = make()
+        plan = ii.ii_plan(t)
+        _, off = plan.tensors()
+        log(f"{cid} {t.name}: blob")
+        blob = synth.blob(t)
+        row = {"set": t.name, "tensors": t.n, "payload_bytes": plan.payload_bytes,
+               "chunk_bytes": plan.chunk_bytes, "chunks": plan.num_chunks,
+               "segments": plan.num_segments}
+        arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=dev)
+        dst = arena.data_ptr() + off
+        free, _ = torch.cuda.mem_get_info(dev)
+        if free > blob.size + (4 << 30):
+            image = torch.from_numpy(blob).to(dev)
+            ms = kernel_ms(plan, image, dst, 100 if cid == "C0" else 20)
+            alg = 2 * plan.payload_bytes + table_bytes(plan)
+            row["kernel"] = {"ms": ms, "GBps": alg / (ms * 1e-3) / 1e9,
+                             "frac_of_hbm_peak": alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                             "cache_resident": plan.payload_bytes < (256 << 20)}
+            del image
+            torch.cuda.empty_cache()
+        else:
+            row["kernel"] = {"skipped": "image and arena do not both fit in HBM"}
+        log(f"{cid}: end to end")
+        first = e2e(plan, blob, dst, 1)
+        row["pageable_first"] = rate(plan, first[0])
+        if reps > 1:
+            row["pageable"] = rate(plan, statistics.median(e2e(plan, blob, dst, reps)))
+        if cid != "C3":  # the host will not pin one 141 GB buffer
+            pinned = ii.ii_host_alloc(blob.size)
+            synth.fill(pinned.ptr, 0, blob.size, t.seed)
+            row["pinned_first"] = rate(plan, e2e(plan, pinned, dst, 1)[0])
+            row["pinned"] = rate(plan, statistics.median(e2e(plan, pinned, dst, reps)))
+            pinned.free()
+        if cid == "C2":
+            # the naive per-tensor pipeline on the same table: what merging saves
+            e2e(plan, blob, dst, 1, ii.ii_load_pertensor)
+            row["per_tensor_pageable"] = rate(
+                plan, statistics.median(e2e(plan, blob, dst, 3, ii.ii_load_pertensor)))
+        row["oracle"] = oracle_sample(t, blob, osample)
+        out["configs"][cid] = row
+        log(f"{cid}: " + ", ".join(f"{k} {v['GBps']:.1f} GB/s" for k, v in row.items()
+                                   if isinstance(v, dict) and "GBps" in v))
+        del arena, blob
+        torch.cuda.empty_cache()
+        plan.free()
+
+    # C4: the C1 arena reused for the Mistral-7B-shaped set
+    old_t, new_t = synth.llama8b(), synth.mistral7b()
+    po, pn = ii.ii_plan(old_t), ii.ii_plan(new_t)
+    ob, nbl = synth.blob(old_t), synth.blob(new_t)
+    arena = torch.empty(po.arena_bytes, dtype=torch.uint8, device=dev)
+    _, ooff = po.tensors()
+    times = []
+    for rep in range(4):
+        ii.ii_load(po, ob, arena.data_ptr() + ooff, stream)
+        torch.cuda.synchronize(dev)
+        t1 = time.perf_counter()
+        ii.ii_switch(po, pn, arena, po.arena_bytes, nbl, stream)
+        torch.cuda.synchronize(dev)
+        if rep:
+            times.append(time.perf_counter() - t1)
+    row = {"set": f"{old_t.name} arena -> {new_t.name}", "tensors": new_t.n,
+           "payload_bytes": pn.payload_bytes, "scrubbed_bytes": po.arena_bytes - pn.arena_bytes,
+           "switch_pageable": rate(pn, statistics.median(times)),
+           "oracle": oracle_sample(new_t, nbl, 4 << 30)}
+    out["configs"]["C4"] = row
+    log(f"C4: switch {row['switch_pageable']['GBps']:.1f} GB/s")
+    return out
+
+
 # ---------------------------------------------------------------------------
 # profile summaries (rocprofv3 CSV output -> profiles/*.txt, *.json)
 
@@ -391,6 +525,9 @@ def main() -> int:
     ap.add_argument("--e2e-reps", type=int, default=5)
     ap.add_argument("--compare-per-tensor", action="store_true",
                     help="also time the naive per-tensor pipeline on the 8B and stress sets")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the benchmark line, measure every workload (tiny, stress, "
+                         "8B, 70B, switch) and print one JSON line of results")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -402,6 +539,9 @@ def main() -> int:
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.configs:
+        print(json.dumps(all_configs(torch, dev, ii, synth)), flush=True)
+        return 0
     table = synth.llama8b()
     plan = ii.ii_plan(table)
     nb, off = plan.tensors()

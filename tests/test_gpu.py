@@ -108,7 +108,8 @@ def test_llama70b_full_sampled(orc):
     the host lets one process pin). The oracle cannot hold a second copy, so
     it runs on a sub-table (24 whole tensors, every kind and both ends of the
     file) and every other tensor is checked in random 4 KiB windows plus its
-    first and last bytes."""
+    first and last bytes. Both the ring path from the pageable blob and the
+    resident-image path (141 GB image and 141 GB arena in HBM at once)."""
     import time
     t = synth.llama70b()
     plan = ii.ii_plan(t)
@@ -129,16 +130,35 @@ def test_llama70b_full_sampled(orc):
     whole = sorted(set([0, 1, 2, 3, 4, 5, 6, 7, 8, 9, t.n - 3, t.n - 2, t.n - 1] +
                        list(rng.choice(t.n, size=11, replace=False))))
     outs = orc.load(orc.nbytes(t)[whole], t.src_offset[whole], blob)
-    for i, o in zip(whole, outs):
-        got = arena[int(off[i]):int(off[i]) + o.size].cpu().numpy()
-        assert np.array_equal(got, o), f"tensor {i} ({t.names[i]})"
-    for i in range(t.n):
-        n, s, d = int(nb[i]), int(t.src_offset[i]), int(off[i])
-        for j in [0, max(0, n - 4096)] + [int(x) for x in rng.integers(0, max(1, n - 4096), 2)]:
-            m = min(4096, n - j)
-            got = arena[d + j:d + j + m].cpu().numpy()
-            assert np.array_equal(got, blob[s + j:s + j + m]), (i, j)
-    _say(f"llama70b: {len(whole)} whole tensors and {t.n} sampled tensors bit-exact")
+
+    def check(label):
+        for i, o in zip(whole, outs):
+            got = arena[int(off[i]):int(off[i]) + o.size].cpu().numpy()
+            assert np.array_equal(got, o), f"{label}: tensor {i} ({t.names[i]})"
+        for i in range(t.n):
+            n, s, d = int(nb[i]), int(t.src_offset[i]), int(off[i])
+            for j in [0, max(0, n - 4096)] + [int(x) for x in rng.integers(0, max(1, n - 4096), 2)]:
+                m = min(4096, n - j)
+                got = arena[d + j:d + j + m].cpu().numpy()
+                assert np.array_equal(got, blob[s + j:s + j + m]), (label, i, j)
+    check("pageable")
+    _say(f"llama70b: {len(whole)} whole tensors and {t.n} sampled tensors bit-exact (pageable)")
+    # the resident-image path: 17.2M tiles, more workgroups than one dispatch
+    # can count (2^32 work-items), so the kernel goes in several launches
+    tb = plan.tiles()
+    assert len(tb["first"]) * 256 > 0xffffffff
+    arena.fill_(0x5A)
+    _say("llama70b: image")
+    image = torch.from_numpy(blob).to(DEV)
+    ii.ii_load_device(plan, image, arena.data_ptr() + off)
+    torch.cuda.synchronize()
+    del image
+    check("image")
+    # the last tensor's last bytes are written by the last launch
+    i = t.n - 1
+    n, s, d = int(nb[i]), int(t.src_offset[i]), int(off[i])
+    assert np.array_equal(arena[d + n - 65536:d + n].cpu().numpy(), blob[s + n - 65536:s + n])
+    _say(f"llama70b: {len(whole)} whole tensors and {t.n} sampled tensors bit-exact (image)")
     del arena
 
 
@@ -579,3 +599,35 @@ def test_tp_shard_llama8b_full(orc):
         assert np.array_equal(got[GUARD:GUARD + plan.arena_bytes], want), mode
         del got
     _say("llama8b tp1/4: bit-exact")
+
+
+@pytest.mark.slow
+def test_image_more_tiles_than_one_dispatch(orc, monkeypatch):
+    """1 KiB tiles over 18 GiB: 18.9M workgroups, more than one dispatch of
+    256-thread workgroups can count (2^32 work-items); the image kernel goes
+    in batches and the whole arena must equal the oracle's."""
+    monkeypatch.setenv("II_TILE_BYTES", "1024")
+    n, size = 9, 2 << 30
+    t = oracle_pins._T([1] * n, [(size,)] * n, [i * size + 512 * i for i in range(n)], [256] * n)
+    t.chunk_bytes = 64 << 20
+    plan = ii.ii_plan(t)
+    tiles = plan.tiles()
+    assert tiles["tile_bytes"] == 1024 and len(tiles["first"]) * 256 > 0xffffffff
+    _, off = plan.tensors()
+    total = int(t.src_offset[-1]) + size
+    blob = np.empty(total, np.uint8)
+    synth.fill(blob.ctypes.data, 0, total, 11, threads=16)
+    _say(f"many tiles: {len(tiles['first'])} tiles, oracle arena")
+    want = np.empty(plan.arena_bytes, np.uint8)
+    orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob, want)
+    buf = torch.empty(plan.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
+    buf.fill_(0xA5)
+    image = torch.from_numpy(blob).to(DEV)
+    _say("many tiles: image load")
+    ii.ii_load_device(plan, image, buf.data_ptr() + GUARD + off)
+    torch.cuda.synchronize()
+    del image
+    got = buf.cpu().numpy()
+    assert (got[:GUARD] == 0xA5).all() and (got[GUARD + plan.arena_bytes:] == 0xA5).all()
+    assert np.array_equal(got[GUARD:GUARD + plan.arena_bytes], want)
+    _say("many tiles: bit-exact")
