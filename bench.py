@@ -315,10 +315,44 @@ def all_configs(torch, dev, ii, synth) -> dict:
         return {"GBps": plan.payload_bytes / t / 1e9, "tensors_per_s": plan.num_tensors / t,
                 "frac_of_h2d_peak": plan.payload_bytes / t / 1e9 / h2d["GBps"], "s": t}
 
+    def switch_c4():
+        # C4: the C1 arena reused for the Mistral-7B-shaped set
+        old_t, new_t = synth.llama8b(), synth.mistral7b()
+        po, pn = ii.ii_plan(old_t), ii.ii_plan(new_t)
+        ob, nbl = synth.blob(old_t), synth.blob(new_t)
+        arena = torch.empty(po.arena_bytes, dtype=torch.uint8, device=dev)
+        _, ooff = po.tensors()
+        times = []
+        for rep in range(4):
+            ii.ii_load(po, ob, arena.data_ptr() + ooff, stream)
+            torch.cuda.synchronize(dev)
+            t1 = time.perf_counter()
+            ii.ii_switch(po, pn, arena, po.arena_bytes, nbl, stream)
+            torch.cuda.synchronize(dev)
+            if rep:
+                times.append(time.perf_counter() - t1)
+        row = {"set": f"{old_t.name} arena -> {new_t.name}", "tensors": new_t.n,
+               "payload_bytes": pn.payload_bytes,
+               "scrubbed_bytes": po.arena_bytes - pn.arena_bytes,
+               "switch_pageable": rate(pn, statistics.median(times)),
+               "oracle": oracle_sample(new_t, nbl, 4 << 30)}
+        out["configs"]["C4"] = row
+        log(f"C4: switch {row['switch_pageable']['GBps']:.1f} GB/s")
+        del arena
+        torch.cuda.empty_cache()
+        po.free()
+        pn.free()
+
+    # C4 runs before C3: freeing C3's 141 GB blob leaves the host slower for
+    # the next large pageable blobs of the same process
     for cid, make, reps, osample in (("C0", synth.tiny, 20, 1 << 40),
                                      ("C2", synth.stress, 5, 1 << 40),
                                      ("C1", synth.llama8b, 5, 4 << 30),
-                                     ("C3", synth.llama70b, 1, 4 << 30)):
+                                     ("C4", None, 0, 0),
+                                     ("C3", synth.llama70b, 2, 4 << 30)):
+        if cid == "C4":
+            switch_c4()
+            continue
         t = make()
         plan = ii.ii_plan(t)
         _, off = plan.tensors()
@@ -365,27 +399,6 @@ def all_configs(torch, dev, ii, synth) -> dict:
         torch.cuda.empty_cache()
         plan.free()
 
-    # C4: the C1 arena reused for the Mistral-7B-shaped set
-    old_t, new_t = synth.llama8b(), synth.mistral7b()
-    po, pn = ii.ii_plan(old_t), ii.ii_plan(new_t)
-    ob, nbl = synth.blob(old_t), synth.blob(new_t)
-    arena = torch.empty(po.arena_bytes, dtype=torch.uint8, device=dev)
-    _, ooff = po.tensors()
-    times = []
-    for rep in range(4):
-        ii.ii_load(po, ob, arena.data_ptr() + ooff, stream)
-        torch.cuda.synchronize(dev)
-        t1 = time.perf_counter()
-        ii.ii_switch(po, pn, arena, po.arena_bytes, nbl, stream)
-        torch.cuda.synchronize(dev)
-        if rep:
-            times.append(time.perf_counter() - t1)
-    row = {"set": f"{old_t.name} arena -> {new_t.name}", "tensors": new_t.n,
-           "payload_bytes": pn.payload_bytes, "scrubbed_bytes": po.arena_bytes - pn.arena_bytes,
-           "switch_pageable": rate(pn, statistics.median(times)),
-           "oracle": oracle_sample(new_t, nbl, 4 << 30)}
-    out["configs"]["C4"] = row
-    log(f"C4: switch {row['switch_pageable']['GBps']:.1f} GB/s")
     return out
 
 
