@@ -14,7 +14,7 @@
 
 namespace ii {
 
-constexpr uint32_t kDefaultTile = 8u << 10;  // segment bytes per workgroup (<= kMaxTile)
+constexpr uint32_t kDefaultTile = 4u << 10;  // segment bytes per workgroup (<= kMaxTile)
 constexpr uint32_t kMaxCopyStreams = 2;       // host-to-device copy streams of a ring
 constexpr uint64_t kIoAlign = 4096;           // block alignment of direct-I/O file reads
 constexpr uint64_t kCopyAlign = 256;          // host-to-device copies start and end on these

@@ -19,10 +19,13 @@
 
 namespace ii {
 
-constexpr uint32_t kBlock = 256;           // threads per scatter workgroup
-constexpr int kUnroll = 4;                 // units in flight per lane
+constexpr uint32_t kBlock = 128;           // threads per scatter workgroup
+constexpr int kUnroll = 2;                 // units in flight per lane
 constexpr uint32_t kMaxSegBatch = kBlock;  // segment rows staged in LDS at once
 constexpr uint32_t kMaxTile = 64u << 10;   // largest tile a workgroup takes
+// Largest workgroup count of one launch: a dispatch counts its grid in
+// work-items, in 32 bits.
+constexpr uint32_t kMaxGridBlocks = 0xffffffffu / kBlock;
 
 struct SegRow {
     uint64_t delta;  // source address minus destination address

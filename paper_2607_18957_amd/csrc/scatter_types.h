@@ -38,10 +38,6 @@ struct TileWin {
 };
 static_assert(sizeof(TileWin) == 8, "TileWin must stay 8 bytes");
 
-// Largest workgroup count of one launch of kBlock (256) threads: a dispatch
-// counts its grid in work-items, in 32 bits.
-constexpr uint32_t kMaxGridBlocks = 0xffffffffu / 256u;
-
 // Zero-fill range for the switch scrub: [begin, end) as device addresses.
 struct RangeDev {
     uint64_t begin;
