@@ -681,7 +681,20 @@ def main() -> int:
         log(f"tp shard {label}: {tp_plan.payload_bytes / t / 1e9:.2f} GB/s of shard bytes, "
             f"link {link_bytes / t / 1e9:.2f} GB/s")
 
-    # pageable blob: staged through the pinned ring by the host threads
+    # pageable blob: staged through the pinned ring by the host threads. Cold:
+    # a fresh plan whose first load allocates its ring and tables; prepared:
+    # a fresh plan whose ring and tables were allocated beforehand
+    # (ii_plan_prepare, as a cold-starting process would during its other
+    # initialisation); then warm loads.
+    for label, prep in (("pageable_cold", False), ("pageable_cold_prepared", True)):
+        p2 = ii.ii_plan(table)
+        if prep:
+            p2.prepare()
+        t1 = time.perf_counter()
+        ii.ii_load(p2, blob, dst, stream)
+        torch.cuda.synchronize(dev)
+        report(label, [time.perf_counter() - t1])
+        p2.free()
     timed_load(blob)  # warm: ring allocation, tables
     report("pageable", [timed_load(blob) for _ in range(args.e2e_reps)])
     # the shard: the host stage gathers only its bytes, so the link moves the payload

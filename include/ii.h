@@ -261,6 +261,18 @@ int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads,
                      uint32_t copy_streams);
 
 /*
+ * ii_plan_prepare -- allocate, on the current device, what the plan's loads
+ * would otherwise allocate on first use: the staging ring (pinned host slots,
+ * touched page by page so the first load does not fault them in; device
+ * slots; streams; host copy threads) and the plan's device tables. Optional:
+ * a cold-starting process can call it while other initialisation runs, so
+ * the first load starts moving bytes at once (Sec. 4.2 overlaps independent
+ * steps of the cold start). Idempotent. Errors: II_EINVAL (NULL plan, or a
+ * plan first used on another device), II_EBUSY, II_ENOMEM, II_EHIP.
+ */
+int ii_plan_prepare(ii_plan_t* plan);
+
+/*
  * Pipeline timeline. With tracing on (ii_plan_set_trace(plan, 1) or
  * $II_TRACE=1), every later ii_load / ii_switch on the plan records four
  * timing events per chunk k: before and after its host-to-device copy (on

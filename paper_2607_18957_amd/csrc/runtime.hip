@@ -261,6 +261,7 @@ static int ensure_ring(ii_plan_t* p) {
 #undef II_RING
     r->pool = new (std::nothrow) CopyPool(p->host_threads);
     if (!r->pool) return bail(fail(II_ENOMEM, "host copy pool allocation failed"));
+    for (uint32_t i = 0; i < D; ++i) r->pool->touch(r->hslot[i], C);
     return II_OK;
 }
 
@@ -861,6 +862,15 @@ extern "C" int ii_plan_trace(ii_plan_t* p, float* copy_start, float* copy_end,
         }
     }
     return II_OK;
+}
+
+extern "C" int ii_plan_prepare(ii_plan_t* p) {
+    if (!p) return fail(II_EINVAL, "ii_plan_prepare: plan is NULL");
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_plan_prepare: plan in use");
+    int rc = ensure_tables(p);
+    if (rc) return rc;
+    return ensure_ring(p);
 }
 
 extern "C" int ii_plan_release(ii_plan_t* p) {

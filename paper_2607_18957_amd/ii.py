@@ -68,6 +68,7 @@ _sig("ii_load_file", _c.c_int, _vp, _c.c_int, _u64, _vp, _vp)
 _sig("ii_switch", _c.c_int, _vp, _vp, _vp, _u64, _vp, _u64, _vp)
 _sig("ii_plan_set_ring", _c.c_int, _vp, _u32, _u32, _u32)
 _sig("ii_plan_release", _c.c_int, _vp)
+_sig("ii_plan_prepare", _c.c_int, _vp)
 _sig("ii_plan_set_trace", _c.c_int, _vp, _c.c_int)
 _sig("ii_plan_trace", _c.c_int, _vp, _vp, _vp, _vp, _vp)
 for _n in ("ii_plan_num_tensors", "ii_plan_num_chunks", "ii_plan_num_segments"):
@@ -299,6 +300,9 @@ class Plan:
                                                  ("copy_start", "copy_end", "scatter_start",
                                                   "scatter_end"))), "ii_plan_trace")
         return out
+
+    def prepare(self) -> None:
+        _check(_lib.ii_plan_prepare(self.handle), "ii_plan_prepare")
 
     def release(self) -> None:
         _check(_lib.ii_plan_release(self.handle), "ii_plan_release")

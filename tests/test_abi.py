@@ -110,6 +110,8 @@ def test_null_arguments():
     lib.ii_plan_free(None)
     lib.ii_load.argtypes = [ctypes.c_void_p] * 2 + [ctypes.c_uint64] + [ctypes.c_void_p] * 2
     assert lib.ii_load(None, None, 0, None, None) == ii.EINVAL
+    lib.ii_plan_prepare.argtypes = [ctypes.c_void_p]
+    assert lib.ii_plan_prepare(None) == ii.EINVAL
     assert "NULL" in ii.ii_last_error()
 
 

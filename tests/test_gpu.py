@@ -162,6 +162,40 @@ def test_llama70b_full_sampled(orc):
     del arena
 
 
+@pytest.mark.slow
+def test_image_more_tiles_than_one_dispatch(orc, monkeypatch):
+    """1 KiB tiles over 36 GiB: 37.7M workgroups, more than one dispatch can
+    count (2^32 work-items); the image kernel goes in batches. Every tensor
+    is compared whole with the oracle's, one at a time."""
+    monkeypatch.setenv("II_TILE_BYTES", "1024")
+    n, size = 9, 4 << 30
+    t = oracle_pins._T([1] * n, [(size,)] * n, [i * size + 512 * i for i in range(n)], [256] * n)
+    t.chunk_bytes = 64 << 20
+    plan = ii.ii_plan(t)
+    tiles = plan.tiles()
+    threads = 128
+    assert tiles["tile_bytes"] == 1024 and len(tiles["first"]) * threads > 0xffffffff
+    nb, off = plan.tensors()
+    total = int(t.src_offset[-1]) + size
+    blob = np.empty(total, np.uint8)
+    synth.fill(blob.ctypes.data, 0, total, 11, threads=16)
+    buf = torch.empty(plan.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
+    buf.fill_(0xA5)
+    image = torch.from_numpy(blob).to(DEV)
+    _say(f"many tiles: {len(tiles['first'])} tiles, image load")
+    ii.ii_load_device(plan, image, buf.data_ptr() + GUARD + off)
+    torch.cuda.synchronize()
+    del image
+    assert (buf[:GUARD].cpu().numpy() == 0xA5).all()
+    assert (buf[GUARD + plan.arena_bytes:].cpu().numpy() == 0xA5).all()
+    nbo = orc.nbytes(t)
+    for i in range(n):
+        want = orc.load(nbo[i:i + 1], t.src_offset[i:i + 1], blob)[0]
+        d = GUARD + int(off[i])
+        assert np.array_equal(buf[d:d + int(nb[i])].cpu().numpy(), want), i
+    _say("many tiles: bit-exact")
+
+
 @pytest.mark.parametrize("mode", ["pageable", "pinned", "image"])
 def test_tiny(orc, mode):
     _load_arena(orc, synth.tiny(), mode=mode)
@@ -601,35 +635,20 @@ def test_tp_shard_llama8b_full(orc):
     _say("llama8b tp1/4: bit-exact")
 
 
-@pytest.mark.slow
-def test_image_more_tiles_than_one_dispatch(orc, monkeypatch):
-    """1 KiB tiles over 36 GiB: 37.7M workgroups, more than one dispatch can
-    count (2^32 work-items); the image kernel goes in batches. Every tensor
-    is compared whole with the oracle's, one at a time."""
-    monkeypatch.setenv("II_TILE_BYTES", "1024")
-    n, size = 9, 4 << 30
-    t = oracle_pins._T([1] * n, [(size,)] * n, [i * size + 512 * i for i in range(n)], [256] * n)
-    t.chunk_bytes = 64 << 20
+def test_prepare_then_load(orc):
+    """ii_plan_prepare allocates the ring and tables ahead of the first load;
+    it is idempotent, the ring can no longer be resized, and loads give the
+    oracle's bytes."""
+    t = synth.tiny(chunk=1 << 20)
     plan = ii.ii_plan(t)
-    tiles = plan.tiles()
-    threads = 128
-    assert tiles["tile_bytes"] == 1024 and len(tiles["first"]) * threads > 0xffffffff
-    nb, off = plan.tensors()
-    total = int(t.src_offset[-1]) + size
-    blob = np.empty(total, np.uint8)
-    synth.fill(blob.ctypes.data, 0, total, 11, threads=16)
-    buf = torch.empty(plan.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
-    buf.fill_(0xA5)
-    image = torch.from_numpy(blob).to(DEV)
-    _say(f"many tiles: {len(tiles['first'])} tiles, image load")
-    ii.ii_load_device(plan, image, buf.data_ptr() + GUARD + off)
-    torch.cuda.synchronize()
-    del image
-    assert (buf[:GUARD].cpu().numpy() == 0xA5).all()
-    assert (buf[GUARD + plan.arena_bytes:].cpu().numpy() == 0xA5).all()
-    nbo = orc.nbytes(t)
-    for i in range(n):
-        want = orc.load(nbo[i:i + 1], t.src_offset[i:i + 1], blob)[0]
-        d = GUARD + int(off[i])
-        assert np.array_equal(buf[d:d + int(nb[i])].cpu().numpy(), want), i
-    _say("many tiles: bit-exact")
+    plan.set_ring(2, 2, 2)
+    plan.prepare()
+    plan.prepare()
+    with pytest.raises(ii.IIError) as e:
+        plan.set_ring(3, 2, 2)
+    assert e.value.name == "II_EBUSY"
+    _load_arena(orc, t, plan=plan)
+    _load_arena(orc, t, mode="image", plan=plan)
+    plan.release()
+    plan.prepare()
+    _load_arena(orc, t, plan=plan)
