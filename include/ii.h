@@ -113,6 +113,9 @@ typedef struct ii_plan_s ii_plan_t; /* opaque */
  * The ring loads skip chunks that hold no segment, and move of each other
  * chunk only its segment bytes (gathered on the host) or the range from its
  * first segment's start to its last segment's end (see ii_plan_copy_bytes).
+ * The scatter kernel's tiles take 4096 segment bytes each ($II_TILE_BYTES,
+ * read by ii_plan, overrides it: 1024..65536, rounded down to a multiple of
+ * 16).
  * Destination layout (used by ii_switch and by callers carving an arena): in
  * table order, tensor i starts at the smallest multiple of dst_align[i] at or
  * after the end of tensor i-1; arena_bytes is the end rounded up to the
