@@ -179,3 +179,22 @@ def test_packed_stress_with_gaps(orc):
     _, l, _ = plan.chunks()
     assert (pk["chunk_len"] < l).any()
     _run(orc, t, packed=True, arena_phase=7, src_phase=9)
+
+
+def test_offsets_near_2_32(orc):
+    """chunk_bytes = 2^32 - 16: segments at chunk offsets just below 2^32 - 16,
+    one of them split across the chunk boundary; both the chunk layout and
+    the packed layout. The blob is 4 GiB of untouched zero pages plus the
+    tensors' bytes."""
+    C = (1 << 32) - 16
+    for sizes, src in (([100, 300, 50], [0, (1 << 32) - 200, (1 << 32) + 100]),
+                       ([4096, 8200, 17], [5, (1 << 32) - 4111, (1 << 32) + 4200])):
+        t = oracle_pins._T([1] * 3, [(s,) for s in sizes], src, [1, 16, 256])
+        t.chunk_bytes = C
+        hi = max(s + n for s, n in zip(src, sizes))
+        t.blob = np.zeros(hi + 64, np.uint8)
+        rng = np.random.default_rng(0)
+        for s, n in zip(src, sizes):
+            t.blob[s:s + n] = rng.integers(0, 256, n, dtype=np.uint8)
+        for packed in (False, True):
+            _run(orc, t, arena_phase=3, src_phase=7, packed=packed)

@@ -652,3 +652,49 @@ def test_prepare_then_load(orc):
     plan.release()
     plan.prepare()
     _load_arena(orc, t, plan=plan)
+
+
+def test_many_segments_per_tile(orc):
+    """200,000 tensors of 1-32 bytes, packed with no destination padding:
+    a 4 KiB tile meets hundreds of segments, so the kernel stages its rows
+    in several LDS batches; every destination phase occurs."""
+    t = synth.stress(n=200_000, lo_bytes=1, hi_bytes=32, chunk=1 << 20, dst_align=1)
+    plan = ii.ii_plan(t)
+    tl = plan.tiles()
+    per_tile = (tl["last"].astype(np.int64) - tl["first"]).max()
+    assert per_tile > 2 * 128, per_tile
+    for mode in ("pageable", "pinned", "image"):
+        _load_arena(orc, t, mode=mode, plan=plan)
+
+
+@pytest.mark.slow
+def test_largest_chunk(orc):
+    """chunk_bytes at its maximum, 2^32 - 16: chunk offsets and tile windows
+    use the whole 32-bit range; the 8B set in 4 chunks through a ring of
+    three 4 GiB slots, and from the resident image, compared whole."""
+    t = synth.llama8b()
+    C = (1 << 32) - 16
+    plan = ii.ii_plan(t, C)
+    assert plan.num_chunks == 4
+    nb, off = plan.tensors()
+    blob = synth.blob(t)
+    want = np.empty(plan.arena_bytes, np.uint8)
+    orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob, want)
+    buf = torch.empty(plan.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
+    base = buf.data_ptr() + GUARD
+    for mode in ("pageable", "image"):
+        buf.fill_(0xA5)
+        _say(f"largest chunk: {mode}")
+        if mode == "pageable":
+            ii.ii_load(plan, blob, base + off)
+        else:
+            img = torch.from_numpy(blob).to(DEV)
+            ii.ii_load_device(plan, img, base + off)
+        torch.cuda.synchronize()
+        if mode == "image":
+            del img
+        got = buf.cpu().numpy()
+        assert (got[:GUARD] == 0xA5).all() and (got[GUARD + plan.arena_bytes:] == 0xA5).all()
+        assert np.array_equal(got[GUARD:GUARD + plan.arena_bytes], want), mode
+        del got
+    plan.free()
