@@ -68,8 +68,8 @@ struct ii_plan_s {
     // tiles (see TileDev), chunk by chunk
     uint32_t tile_bytes = ii::kDefaultTile;
     std::vector<ii::TileDev> tiles;
-    std::vector<ii::TileWin> tile_win;
-    std::vector<uint32_t> tile_chunk;        // chunk of each tile
+    std::vector<ii::TileWin> tile_win;       // plans with gaps only
+    std::vector<uint32_t> tile_chunk;        // chunk of each tile (plans with gaps only)
     std::vector<uint64_t> chunk_tile_begin;  // num_chunks + 1
     // ceil(chunk_bytes / tile_bytes) when no chunk has a gap between its
     // segments (every full chunk then has that many tiles and tile g is

@@ -307,40 +307,50 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         }
 
         // 6. tiles: per chunk, tile_bytes of segment bytes each (packed
-        // offsets), and the same bytes as a window of chunk offsets
+        // offsets), and -- for plans with gaps -- the same bytes as a window
+        // of chunk offsets. Built segment by segment: the tiles that start
+        // inside segment s begin their range at s, and every tile segment s
+        // reaches has s in its range, so whole runs of tiles are filled at
+        // once.
         uint32_t T = env_u32("II_TILE_BYTES", kDefaultTile, 1024, kMaxTile) & ~15u;
         p->tile_bytes = T;
         const std::vector<uint32_t>& po = p->seg_poff;
         p->chunk_tile_begin.assign(p->num_chunks + 1, 0);
+        for (size_t k = 0; k < p->num_chunks; ++k)
+            p->chunk_tile_begin[k + 1] = p->chunk_tile_begin[k] + (p->chunk_plen[k] + T - 1) / T;
+        const uint64_t G = p->chunk_tile_begin[p->num_chunks];
+        if (G > 0x7fffffffull) return fail(II_EINVAL, "ii_plan: more than 2^31 tiles");
+        p->tiles.resize(G);
+        if (p->packed_distinct) {
+            p->tile_win.resize(G);
+            p->tile_chunk.resize(G);
+        }
         for (size_t k = 0; k < p->num_chunks; ++k) {
             const uint64_t s0 = p->chunk_seg_begin[k], s1 = p->chunk_seg_begin[k + 1];
-            const uint64_t plen = p->chunk_plen[k], M = (plen + T - 1) / T;
-            // chunk offset of packed offset P (P < plen), given the segment
-            // g that holds it
-            auto raw = [&](uint64_t g, uint64_t P) { return p->seg_off[g] + (P - po[g]); };
-            uint64_t f = s0, l = s0;
-            for (uint64_t m = 0; m < M; ++m) {
-                const uint64_t P0 = m * T, P1 = std::min(plen, P0 + T);
-                while (f < s1 && (uint64_t)po[f] + p->seg_len[f] <= P0) ++f;
-                if (l < f) l = f;
-                while (l < s1 && po[l] < P1) ++l;
-                TileWin tw;
-                tw.w0 = (uint32_t)raw(f, P0);
-                if (P1 == plen) {
-                    tw.w1 = p->seg_off[s1 - 1] + p->seg_len[s1 - 1];
-                } else {
-                    // the segment holding P1: l if it starts there, else l - 1
-                    const uint64_t g = (l < s1 && po[l] == P1) ? l : l - 1;
-                    tw.w1 = (uint32_t)raw(g, P1);
-                }
-                p->tiles.push_back(TileDev{(uint32_t)f, (uint32_t)l});
-                p->tile_win.push_back(tw);
-                p->tile_chunk.push_back((uint32_t)k);
+            const uint64_t g0 = p->chunk_tile_begin[k];
+            TileDev* td = p->tiles.data() + g0;
+            for (uint64_t x = s0; x < s1; ++x) {
+                const uint64_t P0 = po[x], P1 = P0 + p->seg_len[x];
+                const uint64_t m0 = P0 / T, m1 = (P1 - 1) / T;
+                // segment x is the first to meet tile m0 if it starts there
+                if (P0 == m0 * T) td[m0].first = (uint32_t)x;
+                td[m0].last = (uint32_t)(x + 1);
+                if (m1 > m0) std::fill(td + m0 + 1, td + m1 + 1, TileDev{(uint32_t)x, (uint32_t)(x + 1)});
             }
-            p->chunk_tile_begin[k + 1] = p->tiles.size();
+            if (!p->packed_distinct) continue;
+            // windows: tile m starts at the chunk offset of packed byte m*T,
+            // which lies in segment first[m]; it ends where tile m+1 starts,
+            // the chunk's last tile at its last segment's end
+            const uint64_t M = p->chunk_tile_begin[k + 1] - g0;
+            TileWin* tw = p->tile_win.data() + g0;
+            for (uint64_t m = 0; m < M; ++m) {
+                const uint32_t f = td[m].first;
+                tw[m].w0 = (uint32_t)(p->seg_off[f] + (m * T - po[f]));
+                p->tile_chunk[g0 + m] = (uint32_t)k;
+            }
+            for (uint64_t m = 0; m + 1 < M; ++m) tw[m].w1 = tw[m + 1].w0;
+            if (M) tw[M - 1].w1 = p->seg_off[s1 - 1] + p->seg_len[s1 - 1];
         }
-        if (p->tiles.size() > 0x7fffffffull)
-            return fail(II_EINVAL, "ii_plan: more than 2^31 tiles");
         // no chunk has a gap: tile m of every chunk is the window [m*T,
         // (m+1)*T) of it, and full chunks have ceil(C / T) tiles each
         p->tiles_per_chunk = p->packed_distinct ? 0 : (uint32_t)((C + T - 1) / T);
@@ -418,13 +428,21 @@ extern "C" int ii_plan_tiles(const ii_plan_t* p, uint32_t* tile_bytes, uint64_t*
     if (!p) return fail(II_EINVAL, "ii_plan_tiles: plan is NULL");
     if (tile_bytes) *tile_bytes = p->tile_bytes;
     if (num_tiles) *num_tiles = p->tiles.size();
-    for (size_t g = 0; g < p->tiles.size(); ++g) {
-        if (chunk) chunk[g] = p->tile_chunk[g];
-        if (first) first[g] = p->tiles[g].first;
-        if (last) last[g] = p->tiles[g].last;
-        if (w0) w0[g] = p->tile_win[g].w0;
-        if (w1) w1[g] = p->tile_win[g].w1;
-    }
+    // gap-free plans keep no windows or chunk indices: tile m of chunk k is
+    // the window [m * tile_bytes, ...) of the chunk
+    for (size_t k = 0; k < p->num_chunks; ++k)
+        for (uint64_t g = p->chunk_tile_begin[k]; g < p->chunk_tile_begin[k + 1]; ++g) {
+            if (chunk) chunk[g] = (uint32_t)k;
+            if (first) first[g] = p->tiles[g].first;
+            if (last) last[g] = p->tiles[g].last;
+            const uint64_t m = g - p->chunk_tile_begin[k];
+            const uint64_t b = m * p->tile_bytes;
+            if (w0) w0[g] = p->packed_distinct ? p->tile_win[g].w0 : (uint32_t)b;
+            if (w1)
+                w1[g] = p->packed_distinct ? p->tile_win[g].w1
+                                           : (uint32_t)std::min<uint64_t>(p->chunk_len(k),
+                                                                           b + p->tile_bytes);
+        }
     return II_OK;
 }
 

@@ -38,7 +38,7 @@
 namespace ii {
 
 hipError_t launch_scatter_slot(const uint8_t* slot, const TileDev* tiles, const TileWin* wins,
-                               uint32_t ntiles, const SegDev* segs, bool packed,
+                               uint32_t ntiles, const SegDev* segs, bool implicit,
                                uint32_t tile_bytes, uint64_t plen, hipStream_t stream);
 hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const TileWin* wins,
                                 const uint32_t* tile_chunk, uint64_t ntiles, uint32_t num_chunks,
@@ -205,12 +205,12 @@ static int ensure_tables(ii_plan_t* p) {
         II_HIP(hipMalloc(&r->d_psegs, S * sizeof(SegDev)));
         II_HIP(hipHostMalloc(&r->h_psegs, S * sizeof(SegDev), 0));
     }
-    if (!p->tiles.empty() && !r->d_wins) {
+    if (!p->tile_win.empty() && !r->d_wins) {
         II_HIP(hipMalloc(&r->d_wins, p->tile_win.size() * sizeof(TileWin)));
         II_HIP(hipMemcpy(r->d_wins, p->tile_win.data(), p->tile_win.size() * sizeof(TileWin),
                          hipMemcpyHostToDevice));
     }
-    if (!p->tiles.empty() && !r->d_tile_chunk) {
+    if (!p->tile_chunk.empty() && !r->d_tile_chunk) {
         II_HIP(hipMalloc(&r->d_tile_chunk, p->tile_chunk.size() * sizeof(uint32_t)));
         II_HIP(hipMemcpy(r->d_tile_chunk, p->tile_chunk.data(),
                          p->tile_chunk.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
@@ -561,8 +561,12 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         II_HIP(hipStreamWaitEvent(r->scatter_s, r->copy_done[slot], 0));
         if (trace) II_HIP(hipEventRecord(r->tr_ss[j], r->scatter_s));
         const uint64_t t0 = p->chunk_tile_begin[k], nt = p->chunk_tile_begin[k + 1] - t0;
-        II_HIP(launch_scatter_slot(r->dslot[slot], r->d_tiles + t0, r->d_wins + t0, (uint32_t)nt,
-                                   packed ? r->d_psegs : r->d_segs, packed, p->tile_bytes,
+        // windows are implicit in a packed slot and in a plan without gaps
+        // (which keeps no window table)
+        const bool implicit = packed || !p->packed_distinct;
+        II_HIP(launch_scatter_slot(r->dslot[slot], r->d_tiles + t0,
+                                   implicit ? nullptr : r->d_wins + t0, (uint32_t)nt,
+                                   packed ? r->d_psegs : r->d_segs, implicit, p->tile_bytes,
                                    p->chunk_plen[k], r->scatter_s));
         II_HIP(hipEventRecord(r->scatter_done[slot], r->scatter_s));
         if (trace) II_HIP(hipEventRecord(r->tr_se[j], r->scatter_s));

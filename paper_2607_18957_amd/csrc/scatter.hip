@@ -167,18 +167,19 @@ __device__ __forceinline__ void scatter_tile(uint64_t cbase, uint64_t w0, uint64
 }
 
 // Ring path: one chunk, staged in a device slot that starts at `slot`; one
-// workgroup per tile of the chunk (`tiles` and `wins` point at the chunk's
-// first). Packed slot: tile m takes slot offsets [m * tile_bytes, ...) up to
-// plen; otherwise the slot holds the chunk at its own offsets and the tile's
-// window of chunk offsets applies.
+// workgroup per tile of the chunk (`tiles` points at the chunk's first).
+// implicit: tile m takes slot offsets [m * tile_bytes, ...) up to plen -- a
+// packed slot, or a chunk without gaps at its own offsets; otherwise the
+// slot holds a chunk with gaps at its own offsets and the tile's window of
+// chunk offsets (`wins`, the chunk's first) applies.
 __global__ __launch_bounds__(kBlock) void scatter_slot(
     const uint8_t* __restrict__ slot, const TileDev* __restrict__ tiles,
-    const TileWin* __restrict__ wins, const SegDev* __restrict__ segs, uint32_t packed,
+    const TileWin* __restrict__ wins, const SegDev* __restrict__ segs, uint32_t implicit,
     uint32_t tile_bytes, uint64_t plen) {
     const uint32_t g = blockIdx.x;
     const TileDev td = tiles[g];
     uint64_t w0, w1;
-    if (packed) {
+    if (implicit) {
         w0 = (uint64_t)g * tile_bytes;
         w1 = min(plen, w0 + tile_bytes);
     } else {
@@ -245,11 +246,12 @@ __global__ __launch_bounds__(kBlock) void zero_ranges(const RangeDev* __restrict
 }
 
 hipError_t launch_scatter_slot(const uint8_t* slot, const TileDev* tiles, const TileWin* wins,
-                               uint32_t ntiles, const SegDev* segs, bool packed,
+                               uint32_t ntiles, const SegDev* segs, bool implicit,
                                uint32_t tile_bytes, uint64_t plen, hipStream_t stream) {
     if (ntiles == 0) return hipSuccess;
+    if (!implicit && !wins) return hipErrorInvalidValue;
     hipLaunchKernelGGL(scatter_slot, dim3(ntiles), dim3(kBlock), 0, stream, slot, tiles, wins,
-                       segs, packed ? 1u : 0u, tile_bytes, plen);
+                       segs, implicit ? 1u : 0u, tile_bytes, plen);
     return hipGetLastError();
 }
 
@@ -258,6 +260,7 @@ hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const
                                 uint32_t per_chunk, const SegDev* segs, uint64_t chunk_bytes,
                                 uint64_t last_len, uint32_t tile_bytes, hipStream_t stream) {
     if (ntiles > 0xffffffffull) return hipErrorInvalidConfiguration;
+    if (!per_chunk && (!wins || !tile_chunk)) return hipErrorInvalidValue;
     // a dispatch counts its grid in work-items (32 bits): at most
     // kMaxGridBlocks workgroups of kBlock per launch
     for (uint64_t g0 = 0; g0 < ntiles; g0 += kMaxGridBlocks) {
