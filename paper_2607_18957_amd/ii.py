@@ -328,14 +328,19 @@ def _desc_array(table) -> tuple[np.ndarray, list]:
     d = np.zeros(n, dtype=_DESC)
     if n:
         if names is not None:
-            enc = [s.encode() + b"\0" for s in names]
-            buf = np.frombuffer(b"".join(enc), dtype=np.uint8).copy()
+            # one NUL-separated buffer; a name starts after each NUL (names
+            # are C strings, so they hold none themselves)
+            buf = np.frombuffer(("\0".join(names) + "\0").encode(), dtype=np.uint8).copy()
+            if int(np.count_nonzero(buf == 0)) != n:
+                raise ValueError("tensor names must not contain NUL characters")
             pos = np.zeros(n, dtype=np.uint64)
-            pos[1:] = np.cumsum([len(e) for e in enc[:-1]], dtype=np.uint64)
+            pos[1:] = np.flatnonzero(buf == 0)[:-1].astype(np.uint64) + np.uint64(1)
             d["name"] = np.uint64(buf.ctypes.data) + pos
             keep.append(buf)
         d["dtype"] = np.asarray(table.dtype, dtype=np.int32)
-        d["ndim"] = np.array([len(s) for s in table.shapes], dtype=np.int32)
+        nd = table.ndim() if hasattr(table, "ndim") else None
+        d["ndim"] = (np.asarray(nd, dtype=np.int32) if nd is not None else
+                     np.fromiter(map(len, table.shapes), dtype=np.int32, count=n))
         base = np.uint64(flat.ctypes.data) if flat.size else np.uint64(0)
         d["shape"] = np.where(d["ndim"] > 0, base + np.asarray(start, np.uint64) * np.uint64(8), 0)
         d["src_offset"] = np.asarray(table.src_offset, dtype=np.uint64)

@@ -20,6 +20,7 @@ regenerated independently and large blobs are filled in parallel.
 from __future__ import annotations
 
 import ctypes
+import itertools
 import math
 import os
 import subprocess
@@ -69,7 +70,7 @@ class Table:
         return len(self.names)
 
     def ndim(self) -> np.ndarray:
-        return np.array([len(s) for s in self.shapes], dtype=np.int32)
+        return np.fromiter(map(len, self.shapes), dtype=np.int32, count=self.n)
 
     def shape_flat(self) -> tuple[np.ndarray, np.ndarray]:
         """Flattened shapes (int64) and the start index of each tensor's dims."""
@@ -77,7 +78,7 @@ class Table:
         start = np.zeros(self.n, dtype=np.int64)
         if self.n:
             start[1:] = np.cumsum(nd[:-1], dtype=np.int64)
-        flat = np.fromiter((d for s in self.shapes for d in s), dtype=np.int64,
+        flat = np.fromiter(itertools.chain.from_iterable(self.shapes), dtype=np.int64,
                            count=int(nd.sum()))
         return flat, start
 
