@@ -162,7 +162,8 @@ void ii_plan_free(ii_plan_t* plan);
  *   dst_ptrs    n device addresses, one per table row (NULL allowed only for
  *               zero-size tensors); dst_ptrs[i] must be a multiple of
  *               dst_align[i]; the ranges [dst_ptrs[i], +nbytes[i]) must not
- *               overlap. Read during the call only; the memory they point to
+ *               overlap, and each must lie inside one device allocation or
+ *               in pinned host memory (checked, II_EINVAL; see ii_check_dst). Read during the call only; the memory they point to
  *               must stay allocated until `stream` passes this call.
  *   stream      HIP stream (0 = null stream). Writes into the destinations
  *               start only after all work already enqueued on `stream`, and
@@ -201,7 +202,9 @@ int ii_load_file(ii_plan_t* plan, int fd, uint64_t file_bytes, void* const* dst_
  * HBM): no staging and no host-to-device copy, every chunk is scattered
  * straight from the image by the same kernel, in one launch on `stream`.
  *
- *   dev_image    device address of blob byte 0 (any alignment).
+ *   dev_image    device address of blob byte 0 (any alignment); the span
+ *                [dev_image + lo, + hi) must lie inside one device allocation
+ *                or in pinned host memory (checked, II_EINVAL).
  *   image_bytes  size of the image; must be >= the plan's span end hi.
  *   dst_ptrs     as for ii_load; must not overlap [dev_image, +hi).
  *   stream       the kernel runs on this stream, after the work already on
@@ -262,6 +265,17 @@ int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint6
  */
 int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads,
                      uint32_t copy_streams);
+
+/*
+ * ii_check_dst -- the destination checks every load runs, without loading:
+ * each non-empty tensor's pointer is non-NULL and aligned to its dst_align,
+ * the ranges [dst_ptrs[i], +nbytes[i]) are pairwise disjoint, and each lies
+ * inside one device allocation (or in pinned host memory). Touches no
+ * device memory. Errors: II_EINVAL (NULL arguments, a pointer the device
+ * cannot write, with the tensor named in ii_last_error), II_EALIGN,
+ * II_EOVERLAP, II_EOVERFLOW.
+ */
+int ii_check_dst(const ii_plan_t* plan, void* const* dst_ptrs);
 
 /*
  * ii_plan_prepare -- allocate, on the current device, what the plan's loads

@@ -285,7 +285,42 @@ struct DstRange {
     size_t i;
 };
 
-// Check destination addresses: present, aligned and pairwise disjoint.
+// Whether the device can reach [b, e): inside one HIP device (or managed)
+// allocation, whose extent is returned in [*ab, *ae) so that later ranges
+// inside it need no query, or pinned host memory at both ends. Pageable host
+// memory, or memory HIP does not know, is not: a kernel writing or reading
+// there would fault the device.
+static bool accessible(uint64_t b, uint64_t e, uint64_t* ab, uint64_t* ae) {
+    hipPointerAttribute_t a;
+    if (hipPointerGetAttributes(&a, reinterpret_cast<void*>(b)) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    if (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged) {
+        hipDeviceptr_t base = nullptr;
+        size_t size = 0;
+        if (hipMemGetAddressRange(&base, &size, reinterpret_cast<hipDeviceptr_t>(b)) !=
+            hipSuccess) {
+            (void)hipGetLastError();
+            return true;  // device memory whose extent HIP does not report
+        }
+        *ab = reinterpret_cast<uint64_t>(base);
+        *ae = *ab + size;
+        return e <= *ae;
+    }
+    if (a.type == hipMemoryTypeHost) {
+        hipPointerAttribute_t z;
+        if (hipPointerGetAttributes(&z, reinterpret_cast<void*>(e - 1)) != hipSuccess) {
+            (void)hipGetLastError();
+            return false;
+        }
+        return z.type == hipMemoryTypeHost;
+    }
+    return false;
+}
+
+// Check destination addresses: present, aligned, pairwise disjoint and
+// reachable by the device.
 static int check_dst(const ii_plan_t* p, const uint64_t* dst) {
     const size_t n = p->nbytes.size();
     std::vector<DstRange> v;
@@ -306,6 +341,14 @@ static int check_dst(const ii_plan_t* p, const uint64_t* dst) {
         if (v[j].b < v[j - 1].e)
             return fail(II_EOVERLAP, "destinations of tensors %zu and %zu overlap", v[j - 1].i,
                         v[j].i);
+    uint64_t ab = 0, ae = 0;  // the device allocation found last
+    for (const DstRange& d : v) {
+        if (d.b >= ab && d.e <= ae) continue;
+        if (!accessible(d.b, d.e, &ab, &ae))
+            return fail(II_EINVAL, "dst_ptrs[%zu]=%#llx (+%llu bytes) is not memory the device "
+                        "can write: not inside one device allocation or pinned host memory",
+                        d.i, (unsigned long long)d.b, (unsigned long long)(d.e - d.b));
+    }
     return II_OK;
 }
 
@@ -331,6 +374,11 @@ static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, ui
         if (rc) return rc;
     }
     if (image_e > image_b && !(same && r->image_b == image_b && r->image_e == image_e)) {
+        uint64_t ab = 0, ae = 0;
+        if (!accessible(image_b, image_e, &ab, &ae))
+            return fail(II_EINVAL, "the image's span [%#llx, %#llx) is not memory the device can "
+                        "read: not inside one device allocation or pinned host memory",
+                        (unsigned long long)image_b, (unsigned long long)image_e);
         int rc = check_image(p, dst, image_b, image_e);
         if (rc) return rc;
     }
@@ -866,6 +914,12 @@ extern "C" int ii_plan_trace(ii_plan_t* p, float* copy_start, float* copy_end,
         }
     }
     return II_OK;
+}
+
+extern "C" int ii_check_dst(const ii_plan_t* p, void* const* dst_ptrs) {
+    if (!p) return fail(II_EINVAL, "ii_check_dst: plan is NULL");
+    if (p->nbytes.size() && !dst_ptrs) return fail(II_EINVAL, "ii_check_dst: dst_ptrs is NULL");
+    return check_dst(p, reinterpret_cast<const uint64_t*>(dst_ptrs));
 }
 
 extern "C" int ii_plan_prepare(ii_plan_t* p) {

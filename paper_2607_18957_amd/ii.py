@@ -69,6 +69,7 @@ _sig("ii_switch", _c.c_int, _vp, _vp, _vp, _u64, _vp, _u64, _vp)
 _sig("ii_plan_set_ring", _c.c_int, _vp, _u32, _u32, _u32)
 _sig("ii_plan_release", _c.c_int, _vp)
 _sig("ii_plan_prepare", _c.c_int, _vp)
+_sig("ii_check_dst", _c.c_int, _vp, _vp)
 _sig("ii_plan_set_trace", _c.c_int, _vp, _c.c_int)
 _sig("ii_plan_trace", _c.c_int, _vp, _vp, _vp, _vp, _vp)
 for _n in ("ii_plan_num_tensors", "ii_plan_num_chunks", "ii_plan_num_segments"):
@@ -404,3 +405,9 @@ def ii_switch(plan_old: Plan, plan_new: Plan, arena, arena_bytes: int, blob, str
     ptr, nbytes = _host(blob)
     _check(_lib.ii_switch(plan_old.handle, plan_new.handle, a or None, arena_bytes, ptr or None,
                           nbytes, _stream(stream)), "ii_switch")
+
+
+def ii_check_dst(plan: Plan, dst_ptrs) -> None:
+    """The destination checks of a load, without loading (raises IIError)."""
+    d = _ptrs(dst_ptrs)
+    _check(_lib.ii_check_dst(plan.handle, d.ctypes.data if d.size else None), "ii_check_dst")

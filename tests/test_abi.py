@@ -112,6 +112,8 @@ def test_null_arguments():
     assert lib.ii_load(None, None, 0, None, None) == ii.EINVAL
     lib.ii_plan_prepare.argtypes = [ctypes.c_void_p]
     assert lib.ii_plan_prepare(None) == ii.EINVAL
+    lib.ii_check_dst.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    assert lib.ii_check_dst(None, None) == ii.EINVAL
     assert "NULL" in ii.ii_last_error()
 
 

@@ -698,3 +698,49 @@ def test_largest_chunk(orc):
         assert np.array_equal(got[GUARD:GUARD + plan.arena_bytes], want), mode
         del got
     plan.free()
+
+
+def test_destinations_the_device_cannot_reach(orc):
+    """Destinations in pageable host memory are refused before anything is
+    enqueued (a kernel writing there would fault the device); pinned host
+    memory is a valid destination and receives the oracle's bytes."""
+    t = synth.tiny()
+    plan = ii.ii_plan(t)
+    nb, off = plan.tensors()
+    blob = synth.blob(t)
+    dev_arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=DEV)
+    ii.ii_check_dst(plan, dev_arena.data_ptr() + off)
+    pageable = np.zeros(plan.arena_bytes + 4096, np.uint8)
+    base = (pageable.ctypes.data + 4095) & ~4095  # aligned, so only reachability fails
+    bad = base + off
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_check_dst(plan, bad)
+    assert e.value.name == "II_EINVAL" and "not memory the device" in ii.ii_last_error()
+    # the loads run the same check before they enqueue anything
+    for fn, src in ((ii.ii_load, blob), (ii.ii_load_pertensor, blob)):
+        with pytest.raises(ii.IIError) as e:
+            fn(plan, src, bad)
+        assert e.value.name == "II_EINVAL"
+    img = torch.from_numpy(blob).to(DEV)
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_load_device(plan, img, bad)
+    assert e.value.name == "II_EINVAL"
+    torch.cuda.synchronize()
+    assert (pageable == 0).all()
+    # pinned host memory: written over the link by the same kernels
+    host = ii.ii_host_alloc(plan.arena_bytes)
+    arr = host.numpy()
+    arr[:] = 0x3C
+    for mode in ("pageable-blob", "image"):
+        arr[:] = 0x3C
+        if mode == "image":
+            ii.ii_load_device(plan, img, host.ptr + off)
+        else:
+            ii.ii_load(plan, blob, host.ptr + off)
+        torch.cuda.synchronize()
+        want = np.full(plan.arena_bytes, 0x3C, np.uint8)
+        orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob, want)
+        assert np.array_equal(arr[:plan.arena_bytes], want), mode
+    host.free()
+    # the plan is still usable for device destinations
+    _load_arena(orc, t, plan=plan)
