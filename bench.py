@@ -454,14 +454,21 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -
               f"bench.py value in the same run: {run['value']:.1f} GB/s, "
               f"roofline frac {run['roofline']['frac']:.4f}"]
     gaps = named("ii::scatter_image_gaps")
+    gap_lines = []
     if gaps and "tp_shard" in run:
         tp = run["tp_shard"]
-        lines += ["", f"scatter_image_gaps ({tp['table']}: rank 1 of 4 read out of the unsharded "
-                      f"file, {tp['payload_bytes']} B, {tp['segments']} segments) average per "
-                      f"launch: {float(gaps[0]['AverageNs']) / 1e6:.4f} ms (rocprofv3)",
-                  f"bench.py HIP-event mean in the same run: {tp['kernel']['ms']:.4f} ms, "
-                  f"{tp['kernel']['GBps']:.1f} GB/s algorithmic, frac "
-                  f"{tp['kernel']['frac_of_hbm_peak']:.4f}"]
+        gap_lines = [
+            f"# scatter_image_gaps, {tp['table']}: rank 1 of 4 of the llama8b-shaped set read",
+            f"# out of its unsharded file ({tp['payload_bytes']} B, {tp['segments']} segments),",
+            "# resident image, one GPU",
+            f"# command 1: {PROFILE_CMDS['trace']}",
+            f"# command 2: {PROFILE_CMDS['fetch']}",
+            f"# command 3: {PROFILE_CMDS['write']}", "",
+            f"average per launch: {float(gaps[0]['AverageNs']) / 1e6:.4f} ms (rocprofv3, "
+            f"{gaps[0]['Calls']} launches)",
+            f"bench.py HIP-event mean in the same run: {tp['kernel']['ms']:.4f} ms, "
+            f"{tp['kernel']['GBps']:.1f} GB/s algorithmic, frac "
+            f"{tp['kernel']['frac_of_hbm_peak']:.4f}"]
     open(os.path.join(ROOT, "profiles", "scatter_image_llama8b_kernel_stats.txt"), "w").write(
         "\n".join(lines) + "\n")
 
@@ -512,10 +519,15 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -
                            "fetch_bytes": gf, "write_bytes": gw, "bytes_per_launch": gf + gw,
                            "algorithmic_bytes": alg, "dispatches": fetch[k][1]}
         json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
-        t += [f"scatter_image_gaps        {fetch[k][1]} dispatches (grid {k[1]}), {tp['table']}",
-              f"  FETCH_SIZE per dispatch {fetch[k][0]:.1f} KiB  -> {gf:.0f} B",
-              f"  WRITE_SIZE per dispatch {write[k][0]:.1f} KiB  -> {gw:.0f} B",
-              f"  measured / algorithmic         {(gf + gw) / alg:.4f} (algorithmic {alg} B)"]
+        gap_lines += ["", "counters (KiB per dispatch, scaled as for scatter_image):",
+                      f"  {fetch[k][1]} dispatches (grid {k[1]} work-items)",
+                      f"  FETCH_SIZE per dispatch {fetch[k][0]:.1f} KiB  -> {gf:.0f} B",
+                      f"  WRITE_SIZE per dispatch {write[k][0]:.1f} KiB  -> {gw:.0f} B",
+                      f"  measured HBM bytes per launch  {gf + gw:.0f}",
+                      f"  algorithmic bytes per launch   {alg} (2 x payload + segment and tile "
+                      "tables)",
+                      f"  measured / algorithmic         {(gf + gw) / alg:.4f}",
+                      f"kernel source hash        {kernel_source_hash()}"]
     slot = [k for k in fetch if k[0].split("(")[0] == "ii::scatter_slot"]
     if slot:
         k = slot[0]
@@ -524,7 +536,10 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -
               f"write {write[k][0] * 1024 * w_scale:.0f} B"]
     open(os.path.join(ROOT, "profiles", "scatter_image_llama8b_counters.txt"), "w").write(
         "\n".join(t) + "\n")
-    print("\n".join(lines + [""] + t))
+    if gap_lines:
+        open(os.path.join(ROOT, "profiles", "scatter_image_gaps_llama8b_tp1of4.txt"), "w").write(
+            "\n".join(gap_lines) + "\n")
+    print("\n".join(lines + [""] + t + [""] + gap_lines))
 
 
 def main() -> int:
