@@ -744,3 +744,63 @@ def test_destinations_the_device_cannot_reach(orc):
     host.free()
     # the plan is still usable for device destinations
     _load_arena(orc, t, plan=plan)
+
+
+def test_concurrent_plans_and_busy_plan(orc):
+    """Two plans loading at the same time from two host threads on two
+    streams give each its own oracle bytes; two threads on one plan either
+    load or get II_EBUSY, never a mix, and the plan stays usable."""
+    import threading
+    ta, tb = synth.tiny(chunk=1 << 20), synth.stress(n=30_000, chunk=1 << 20)
+    pa, pb = ii.ii_plan(ta), ii.ii_plan(tb)
+    ba, bb = synth.blob(ta), synth.blob(tb)
+    wa = np.empty(pa.arena_bytes, np.uint8)
+    orc.arena(orc.nbytes(ta), ta.src_offset, ta.dst_align, ba, wa)
+    wb = np.empty(pb.arena_bytes, np.uint8)
+    orc.arena(orc.nbytes(tb), tb.src_offset, tb.dst_align, bb, wb)
+    aa = torch.zeros(pa.arena_bytes, dtype=torch.uint8, device=DEV)
+    ab = torch.zeros(pb.arena_bytes, dtype=torch.uint8, device=DEV)
+    sa, sb = torch.cuda.Stream(DEV), torch.cuda.Stream(DEV)
+    torch.cuda.synchronize()
+    errors = []
+
+    def run(plan, blob, arena, stream, reps):
+        try:
+            _, off = plan.tensors()
+            for _ in range(reps):
+                ii.ii_load(plan, blob, arena.data_ptr() + off, stream)
+            stream.synchronize()
+        except Exception as e:  # noqa: BLE001 - reported below
+            errors.append(e)
+
+    th = [threading.Thread(target=run, args=(pa, ba, aa, sa, 20)),
+          threading.Thread(target=run, args=(pb, bb, ab, sb, 5))]
+    for x in th:
+        x.start()
+    for x in th:
+        x.join()
+    assert not errors, errors
+    assert np.array_equal(aa.cpu().numpy(), wa) and np.array_equal(ab.cpu().numpy(), wb)
+
+    # one plan, two threads at once
+    ab.zero_()
+    torch.cuda.synchronize()
+    results = []
+
+    def one(stream):
+        _, off = pb.tensors()
+        try:
+            ii.ii_load(pb, bb, ab.data_ptr() + off, stream)
+            stream.synchronize()
+            results.append("II_OK")
+        except ii.IIError as e:
+            results.append(e.name)
+
+    th = [threading.Thread(target=one, args=(s,)) for s in (sa, sb)]
+    for x in th:
+        x.start()
+    for x in th:
+        x.join()
+    assert sorted(results) in (["II_OK", "II_OK"], ["II_EBUSY", "II_OK"]), results
+    assert np.array_equal(ab.cpu().numpy(), wb)
+    _load_arena(orc, tb, plan=pb)
