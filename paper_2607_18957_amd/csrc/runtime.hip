@@ -1,26 +1,32 @@
-// Load pipeline: pinned staging ring, bulk host-to-device copies on a
-// dedicated copy stream, per-chunk scatter on a dedicated scatter stream,
+// Load pipeline: pinned staging ring, bulk host-to-device copies on
+// dedicated copy streams, per-chunk scatter on a dedicated scatter stream,
 // hipEvent edges between them, and the C-ABI entry points that drive it.
 //
 // The chunk lifecycle of InstantInfer's refined tensor materialisation
-// (arXiv 2607.18957, Sec. 4.2) maps onto the ring as follows.
-//   InDisk -> InMem   host threads copy chunk k from the blob into pinned
-//                     slot k mod D (skipped when the blob is pinned). The
-//                     slot is reused only once the copy that last read it
-//                     has finished: host wait on copy_done[slot].
-//   InMem  -> InGPU   one hipMemcpyAsync per chunk into device slot k mod D on
-//                     the copy stream, after scatter_done[slot] (the device
-//                     slot is free); records copy_done[slot]. One copy stream
-//                     keeps the bulk copies back to back and in chunk order,
-//                     the paper's (C_i,InGPU)->(C_i+1,InMem) edge, and avoids
-//                     the bus congestion of unrestricted concurrent copies.
+// (arXiv 2607.18957, Sec. 4.2) maps onto the ring as follows; j counts the
+// chunks that hold at least one segment (the others are never touched).
+//   InDisk -> InMem   host threads bring chunk j's bytes into pinned slot
+//                     j mod D: a copy of its used range, or a gather of only
+//                     its segments when it has gaps (pageable blob or file;
+//                     a pinned blob is copied by DMA straight from itself
+//                     unless the chunk is mostly gaps). The slot is reused
+//                     only once the copy that last read it has finished: host
+//                     wait on copy_done[slot].
+//   InMem  -> InGPU   one hipMemcpyAsync per chunk into device slot j mod D
+//                     on copy stream j mod 2 (1 with a single copy stream:
+//                     copies back to back in chunk order, the paper's
+//                     (C_i,InGPU)->(C_i+1,InMem) edge), after
+//                     scatter_done[slot] (the device slot is free); records
+//                     copy_done[slot].
 //   InGPU  -> tensors the scatter stream waits for copy_done[slot] and runs
-//                     the scatter kernel for chunk k, moving its tensor pieces
-//                     from Alloc to Loaded; records scatter_done[slot].
-//   Destroyed         scatter_done[slot] releases the slot to chunk k + D.
+//                     the scatter kernel over the chunk's tiles, moving its
+//                     tensor pieces from Alloc to Loaded; records
+//                     scatter_done[slot].
+//   Destroyed         scatter_done[slot] releases the slot to chunk j + D.
 // The caller's stream gates the first write into destination memory (entry
 // event) and waits for the last scatter (done event), so the load is ordered
-// on it like any other stream work.
+// on it like any other stream work. Destinations are checked (aligned,
+// disjoint, reachable by the device) before anything is enqueued.
 #include <hip/hip_runtime.h>
 
 #include <fcntl.h>
