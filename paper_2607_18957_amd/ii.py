@@ -411,3 +411,22 @@ def ii_check_dst(plan: Plan, dst_ptrs) -> None:
     """The destination checks of a load, without loading (raises IIError)."""
     d = _ptrs(dst_ptrs)
     _check(_lib.ii_check_dst(plan.handle, d.ctypes.data if d.size else None), "ii_check_dst")
+
+
+# element type codes -> torch dtypes (storage only; no arithmetic is done here)
+_TORCH_DTYPES = {1: "uint8", 2: "int8", 3: "float8_e4m3fn", 4: "float8_e5m2", 5: "bfloat16",
+                 6: "float16", 7: "float32", 8: "int32", 9: "float64", 10: "int64"}
+
+
+def arena_views(plan: Plan, table, arena) -> dict:
+    """Name -> tensor view of a loaded arena (a uint8 torch tensor laid out
+    as plan.tensors() says), with the table's dtype and shape. No copy."""
+    import torch
+    nb, off = plan.tensors()
+    names = getattr(table, "names", None) or [plan.name(i) for i in range(plan.num_tensors)]
+    out = {}
+    for i, (name, shape) in enumerate(zip(names, table.shapes)):
+        dt = getattr(torch, _TORCH_DTYPES[int(table.dtype[i])])
+        b = arena[int(off[i]):int(off[i]) + int(nb[i])]
+        out[name] = b.view(dt).view(tuple(int(x) for x in shape))
+    return out
