@@ -667,14 +667,15 @@ def pin_rows_check(orc):
         raise AssertionError("a strided scalar must be rejected")
 
 
-PINS = [pin_esize, pin_sizes, pin_chunks, pin_appendix_counts, pin_segments_bytewise,
-        pin_coverage, pin_layout, pin_check, pin_load, pin_arena, pin_switch, pin_empty,
-        pin_rows_contiguous, pin_rows_numpy_shards, pin_rows_bytewise, pin_rows_check]
+# cheapest first (pin_esize imports torch), so a broken oracle fails fast
+PINS = [pin_sizes, pin_appendix_counts, pin_check, pin_load, pin_arena, pin_switch, pin_empty,
+        pin_segments_bytewise, pin_coverage, pin_rows_check, pin_rows_contiguous,
+        pin_rows_bytewise, pin_chunks, pin_layout, pin_rows_numpy_shards, pin_esize]
 
 
-def run_all(so_path: str, quick: bool = True) -> list[str]:
-    """Run every pin against the oracle library at so_path; return the names
-    of the pins that failed."""
+def run_all(so_path: str, quick: bool = True, stop_first: bool = False) -> list[str]:
+    """Run the pins against the oracle library at so_path; return the names
+    of the pins that failed (only the first one with stop_first)."""
     import oracle
     orc = oracle.Oracle(so_path)
     failed = []
@@ -686,11 +687,13 @@ def run_all(so_path: str, quick: bool = True) -> list[str]:
                 pin(orc)
         except Exception as e:  # noqa: BLE001 - any failure counts as caught
             failed.append(f"{pin.__name__}: {type(e).__name__}: {str(e)[:120]}")
+            if stop_first:
+                break
     return failed
 
 
 if __name__ == "__main__":
     import sys
-    bad = run_all(sys.argv[1], quick=True)
+    bad = run_all(sys.argv[1], quick=True, stop_first="--all" not in sys.argv)
     print("\n".join(bad) if bad else "all pins pass")
     sys.exit(1 if bad else 0)

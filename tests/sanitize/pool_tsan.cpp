@@ -110,7 +110,7 @@ int main() {
         std::vector<uint32_t> off, poff, len;
         uint64_t s = 0, total = 0;
         uint32_t x = 12345;
-        while (s < (8u << 20)) {
+        while (s < (2u << 20)) {
             x = x * 1103515245u + 12345u;
             const uint32_t gap = (x >> 8) % 700, run = 1 + (x >> 16) % 9000;
             s += gap;

@@ -152,7 +152,7 @@ def test_exhaustive_tiny_tables(orc):
                     _compare(orc, t)
 
 
-@settings(max_examples=150, deadline=None)
+@settings(max_examples=100, deadline=None)
 @given(st.data())
 def test_random_tables(orc, data):
     n = data.draw(st.integers(0, 40))
