@@ -35,7 +35,8 @@ extern "C" {
 /* ---- status codes ------------------------------------------------------ */
 enum {
     II_OK = 0,
-    II_EINVAL = 1,    /* NULL argument, bad chunk size, bad dtype/shape/alignment */
+    II_EINVAL = 1,    /* NULL argument, bad chunk size, bad dtype/shape/alignment,
+                         memory the device cannot reach */
     II_EOVERFLOW = 2, /* a byte size or offset does not fit in 64 bits */
     II_EOVERLAP = 3,  /* source ranges overlap, or destination ranges overlap */
     II_EALIGN = 4,    /* a destination pointer is not aligned to its dst_align */
@@ -140,10 +141,14 @@ void ii_plan_free(ii_plan_t* plan);
 
 /*
  * ii_load -- materialise every tensor of the plan from a host blob into
- * device memory (Sec. 4.2). For each chunk in order: stage it into a pinned
- * host slot (skipped when the blob itself is pinned), copy it to a device
- * slot with one hipMemcpyAsync, then scatter it into its tensors with the
- * device kernel. Chunk k+1's copy overlaps chunk k's scatter; a slot is
+ * device memory (Sec. 4.2). For each chunk that holds a segment, in order:
+ * bring its bytes into a pinned host slot (its used range, or only its
+ * segments' bytes, packed, when it has gaps between segments; a pinned
+ * blob's chunk is instead copied by DMA straight from the blob unless more
+ * than a quarter of it is gaps), copy it to a device slot with one
+ * hipMemcpyAsync, then scatter it into its tensors with the device kernel.
+ * Chunks holding no segment are not touched. Chunk k+1's copy overlaps
+ * chunk k's scatter; a slot is
  * reused only after the scatter that read it has finished (Sec. 4.2:
  * (C_i,InMem)->(C_i+1,InDisk), (C_i,InGPU)->(C_i+1,InMem),
  * (C_i,InGPU)->(T_j,Alloc), (T_j,Loaded)->(C_i,InGPU)).
@@ -163,8 +168,10 @@ void ii_plan_free(ii_plan_t* plan);
  *               zero-size tensors); dst_ptrs[i] must be a multiple of
  *               dst_align[i]; the ranges [dst_ptrs[i], +nbytes[i]) must not
  *               overlap, and each must lie inside one device allocation or
- *               in pinned host memory (checked, II_EINVAL; see ii_check_dst). Read during the call only; the memory they point to
- *               must stay allocated until `stream` passes this call.
+ *               in pinned host memory (checked, II_EINVAL; see
+ *               ii_check_dst). Read during the call only; the memory they
+ *               point to must stay allocated until `stream` passes this
+ *               call.
  *   stream      HIP stream (0 = null stream). Writes into the destinations
  *               start only after all work already enqueued on `stream`, and
  *               complete before any work enqueued on `stream` afterwards.
@@ -181,12 +188,14 @@ int ii_load(ii_plan_t* plan, const void* host_blob, uint64_t blob_bytes, void* c
 /*
  * ii_load_file -- the same materialisation with the blob read from a file
  * (the model file on storage or on tmpfs; Sec. 4.2 InDisk -> InMem, Sec. 5):
- * the host threads read each chunk's bytes with pread straight into a pinned
- * slot, then the copy and scatter steps run as in ii_load. If fd was opened
+ * the host threads read each chunk's bytes (only its segments' bytes, run by
+ * run, when it has gaps) with pread straight into a pinned slot, then the
+ * copy and scatter steps run as in ii_load. If fd was opened
  * with O_DIRECT, every read starts and ends on a 4096-byte boundary and
  * bypasses the page cache; those reads land in a page-aligned host buffer
- * (device-pinned pages cannot be targets of direct I/O) from which the host
- * threads copy the chunk into the pinned slot.
+ * (device-pinned pages cannot be targets of direct I/O), read ahead by
+ * several threads, from which the host threads copy (or gather) the chunk
+ * into the pinned slot.
  *   fd          open for reading; file byte x is blob byte x. Read during the
  *               call only; the call returns once every chunk has been read.
  *   file_bytes  size of the file; must be >= the plan's span end hi.
@@ -218,8 +227,10 @@ int ii_load_device(ii_plan_t* plan, const void* dev_image, uint64_t image_bytes,
 /*
  * ii_load_pertensor -- the same result as ii_load by the naive per-tensor
  * pipeline of Sec. 4.2 ("Naive CFA Model"): one host-to-device copy per
- * tensor (a tensor larger than chunk_bytes is copied in chunk_bytes pieces),
- * in table order, straight into its destination; the host staging of tensor
+ * tensor (a tensor larger than chunk_bytes is copied in chunk_bytes pieces;
+ * a tensor given as rows is gathered row by row into the staging slot, or
+ * from a pinned blob copied with one 2-D copy), in table order, straight
+ * into its destination; the host staging of tensor
  * i+1 into the plan's pinned ring overlaps the copy of tensor i, and the
  * copies run one after another on one copy stream ((T_i,InMem) ->
  * (T_i+1,InDisk) and (T_i,InGPU) -> (T_i+1,InMem)). No scatter kernel runs.
@@ -254,8 +265,9 @@ int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint6
 /*
  * Ring configuration, before the plan's first load or after
  * ii_plan_release. depth = number of chunk slots in flight (1..8; default 3
- * or $II_RING_DEPTH); host_threads = threads copying a pageable blob into
- * the pinned slots (1..64; default min(8, cores) or $II_HOST_THREADS);
+ * or $II_RING_DEPTH); host_threads = threads that read, copy or gather
+ * chunk bytes into the pinned slots (pageable blobs, files, gathered chunks;
+ * 1..64; default min(8, cores) or $II_HOST_THREADS);
  * copy_streams = host-to-device copy streams the chunks alternate between
  * (1..min(2, depth); default 2 or $II_COPY_STREAMS). With 1, chunk copies run
  * strictly one after another in chunk order; with 2, the copies of chunks k
