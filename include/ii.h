@@ -255,9 +255,14 @@ int ii_load_pertensor(ii_plan_t* plan, const void* host_blob, uint64_t blob_byte
  *   plan_old     layout of what the arena holds now (only its layout is used).
  *   plan_new     the table to load; its ring and tables are used as in ii_load.
  *   arena        device address, aligned to plan_new's largest dst_align.
- *   arena_bytes  must be >= both plans' arena_bytes, else II_EARENA.
+ *   arena_bytes  must be >= both plans' arena_bytes, else II_EARENA; the
+ *                whole range [arena, arena + arena_bytes) must lie inside
+ *                one device allocation (or in pinned host memory), else
+ *                II_EINVAL, since the scrub may write anywhere in the old
+ *                layout.
  *   host_blob_new, blob_bytes, stream   as for ii_load.
- * Errors: as ii_load, plus II_EARENA.
+ * Errors: as ii_load, plus II_EARENA; all checks run before anything is
+ * enqueued.
  */
 int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint64_t arena_bytes,
               const void* host_blob_new, uint64_t blob_bytes, hipStream_t stream);

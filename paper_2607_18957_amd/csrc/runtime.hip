@@ -856,6 +856,15 @@ extern "C" int ii_switch(const ii_plan_t* po, ii_plan_t* pn, void* arena, uint64
     if (a & (pn->max_align - 1))
         return fail(II_EALIGN, "ii_switch: arena not aligned to %llu",
                     (unsigned long long)pn->max_align);
+    // the scrub writes anywhere in the old layout, so the whole arena the
+    // caller declares must be memory the device can write
+    uint64_t arena_end, ab = 0, ae = 0;
+    if (__builtin_add_overflow(a, arena_bytes, &arena_end))
+        return fail(II_EOVERFLOW, "ii_switch: arena + arena_bytes overflows");
+    if (arena_bytes && !accessible(a, arena_end, &ab, &ae))
+        return fail(II_EINVAL, "ii_switch: the arena [%#llx, +%llu bytes) is not memory the "
+                    "device can write: not inside one device allocation or pinned host memory",
+                    (unsigned long long)a, (unsigned long long)arena_bytes);
     if (pn->num_chunks && !host_blob_new) return fail(II_EINVAL, "ii_switch: host blob is NULL");
     if (blob_bytes < pn->hi)
         return fail(II_ERANGE, "ii_switch: blob has %llu bytes, plan needs %llu",

@@ -11,12 +11,14 @@
 // Work split. A chunk's segment bytes are cut into tiles of tile_bytes (4 KiB
 // by default), in segment order with gaps between segments skipped; one
 // 128-thread workgroup (two wavefronts) owns one tile, two 16-byte units
-// per lane. Measured on the 8B set against 256 threads x 8 KiB, 64 x 2 KiB
-// and other shapes: two units per lane in small workgroups is fastest. The planner stores, per tile, the segment rows
-// whose bytes meet it and the tile's window of chunk offsets, so a
+// per lane. Measured on a Llama-8B-shaped set against 256 threads x 8 KiB,
+// 64 x 2 KiB and other shapes: two units per lane in small workgroups is
+// fastest. The planner stores, per tile, the segment rows whose bytes meet
+// it (and, for tables with gaps, the tile's window of chunk offsets), so a
 // workgroup reads only its own rows, and no workgroup is launched for bytes
 // no tensor needs (the gaps a sharded table leaves in the file). In a
-// packed staging slot the window is simply the tile's share of slot offsets.
+// packed staging slot, and in a chunk without gaps, the window is simply
+// the tile's share of the slot or chunk.
 //
 // Units. Destination memory is written in 16-byte blocks aligned to 16
 // bytes, so every store of a block that a segment covers completely is one
@@ -38,10 +40,10 @@
 // address a. The lane loads the aligned 16-byte words at a & ~15 and
 // (a & ~15) + 16 -- each only if it holds a byte the unit needs, so no load
 // touches a 16-byte word outside the source data -- and assembles the block
-// with byte funnel shifts (v_alignbyte). Blocks a segment covers only partly (its first and last
-// block, or a segment shorter than 16 bytes) are written with 8/4/2/1-byte
-// stores of exactly the covered bytes: padding and neighbouring tensors are
-// never read-modify-written.
+// with byte funnel shifts (v_alignbyte). Blocks a segment covers only partly
+// (its first and last block, or a segment shorter than 16 bytes) are
+// written with 8/4/2/1-byte stores of exactly the covered bytes: padding and
+// neighbouring tensors are never read-modify-written.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>

@@ -471,6 +471,37 @@ def test_switch_small(orc):
     assert e.value.name == "II_EARENA"
 
 
+def test_switch_arena_must_cover_declared_bytes(orc):
+    """ii_switch checks, before it enqueues anything, that the whole declared
+    arena is memory the device can write (the scrub may write anywhere in the
+    old layout): an arena_bytes beyond the allocation is II_EINVAL and leaves
+    the arena as it was; the same switch with an old layout that fits goes
+    through. The old tensor sits at the start of the arena in both layouts,
+    so no byte outside the allocation would be written even without the
+    check."""
+    old_fit = synth._packed(["w"], ["u8"], [(4096,)], [0], 0, 1 << 20, 11, 1 << 16, "old-fit")
+    old_big = synth._packed(["w"], ["u8"], [(4096,)], [0], 0, 256 << 20, 11, 1 << 16, "old-big")
+    new = synth._packed(["w"], ["u8"], [(2048,)], [0], 0, 256, 12, 1 << 16, "new")
+    po_fit, po_big, pn = ii.ii_plan(old_fit), ii.ii_plan(old_big), ii.ii_plan(new)
+    assert po_fit.arena_bytes == 1 << 20 and po_big.arena_bytes == 256 << 20
+    buf, _ = _canary_buffer(8 << 20)  # one allocation far smaller than 256 MiB
+    blob_o, blob_n = synth.blob(old_fit), synth.blob(new)
+    ii.ii_load(po_fit, blob_o, buf.data_ptr() + po_fit.tensors()[1])
+    torch.cuda.synchronize()
+    before = buf.cpu().numpy().copy()
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_switch(po_big, pn, buf, po_big.arena_bytes, blob_n)
+    assert e.value.name == "II_EINVAL"
+    torch.cuda.synchronize()
+    assert np.array_equal(buf.cpu().numpy(), before)
+    ii.ii_switch(po_fit, pn, buf, po_fit.arena_bytes, blob_n)
+    torch.cuda.synchronize()
+    want = before.copy()
+    orc.switch(orc.nbytes(old_fit), old_fit.dst_align, orc.nbytes(new), new.src_offset,
+               new.dst_align, blob_n, want)
+    assert np.array_equal(buf.cpu().numpy(), want)
+
+
 @pytest.mark.slow
 def test_llama8b_full(orc):
     """The benchmarked workload at full size (16.06 GB, 291 tensors, 240
