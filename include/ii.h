@@ -162,7 +162,9 @@ void ii_plan_free(ii_plan_t* plan);
  *               blobs are read only during the call; a pinned blob
  *               (hipHostMalloc / ii_host_alloc) is read by DMA after the call
  *               returns and must stay valid and unchanged until `stream`
- *               reaches the point after this call.
+ *               reaches the point after this call. A blob counts as pinned
+ *               when the first and the last byte of the span [lo, hi) are
+ *               pinned; otherwise it is handled as pageable.
  *   blob_bytes  size of the blob; must be >= the plan's span end hi.
  *   dst_ptrs    n device addresses, one per table row (NULL allowed only for
  *               zero-size tensors); dst_ptrs[i] must be a multiple of

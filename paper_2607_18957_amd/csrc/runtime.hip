@@ -451,6 +451,15 @@ static bool is_pinned_host(const void* ptr) {
     return a.type == hipMemoryTypeHost;
 }
 
+// Whether the blob bytes a load reads, [blob + lo, blob + hi), are pinned
+// host memory at both ends, so that copies may read them by DMA. A blob
+// pinned only in part (or whose declared size reaches past its pinned
+// allocation) is treated as pageable: the host stage copies it, and no DMA
+// reads outside pinned memory.
+static bool pinned_span(const ii_plan_t* p, const uint8_t* blob) {
+    return p->hi > p->lo && is_pinned_host(blob + p->lo) && is_pinned_host(blob + p->hi - 1);
+}
+
 static bool is_device_ptr(const void* ptr) {
     hipPointerAttribute_t a;
     hipError_t e = hipPointerGetAttributes(&a, ptr);
@@ -508,7 +517,7 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
     if (rc) return rc;
     Runtime* r = p->rt;
     const uint8_t* blob = src.blob;
-    const bool pinned = src.fd < 0 && is_pinned_host(blob);
+    const bool pinned = src.fd < 0 && pinned_span(p, blob);
     // The host stage gathers packed chunks whenever it copies anyway, and
     // for a pinned blob also where most of a chunk's used range is gaps.
 
@@ -671,7 +680,7 @@ static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
     Runtime* r = p->rt;
     rc = check_dst(p, dst);
     if (rc) return rc;
-    const bool pinned = is_pinned_host(blob);
+    const bool pinned = pinned_span(p, blob);
     hipStream_t cs = r->copy_s[0];
     II_HIP(hipEventRecord(r->entry, stream));
     II_HIP(hipStreamWaitEvent(cs, r->entry, 0));

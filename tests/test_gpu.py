@@ -78,6 +78,12 @@ def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=N
         hb = ii.ii_host_alloc(blob.size)
         hb.numpy()[:] = blob
         ii.ii_load(plan, hb, base + off, s)
+    elif mode == "pinned-span":
+        # only the span [lo, hi) is pinned; blob byte 0 lies before it
+        lo, hi = plan.span
+        hb = ii.ii_host_alloc(max(1, hi - lo))
+        hb.numpy()[:hi - lo] = blob[lo:hi]
+        ii.ii_load(plan, (hb.ptr - lo, hi), base + off, s)
     elif mode == "image":
         img = torch.from_numpy(blob).to(DEV)
         ii.ii_load_device(plan, img, base + off, s)
@@ -664,6 +670,18 @@ def test_tp_shard_llama8b_full(orc):
         assert np.array_equal(got[GUARD:GUARD + plan.arena_bytes], want), mode
         del got
     _say("llama8b tp1/4: bit-exact")
+
+
+@pytest.mark.parametrize("make", [lambda: synth.tiny(chunk=1 << 16, header=4096),
+                                  lambda: synth.tiny_tp(1, 4, chunk=1 << 16)],
+                         ids=["tiny-header", "tiny-tp1of4"])
+def test_blob_pinned_over_its_span_only(orc, make):
+    """A load reads only the blob's span [lo, hi): a blob pinned over that
+    span alone (its header bytes outside any pinned allocation) takes the
+    pinned path and gives the same bytes."""
+    t = make()
+    assert t.src_offset.min() > 0
+    _load_arena(orc, t, mode="pinned-span", depth=2, threads=2)
 
 
 def test_prepare_then_load(orc):
