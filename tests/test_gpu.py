@@ -509,11 +509,16 @@ def test_switch_arena_must_cover_declared_bytes(orc):
 
 
 @pytest.mark.slow
-def test_llama8b_full(orc):
+@pytest.mark.parametrize("header", [0, 1000], ids=["H0", "H1000"])
+def test_llama8b_full(orc, header):
     """The benchmarked workload at full size (16.06 GB, 291 tensors, 240
     chunks of 64 MiB, ring depth 3): pageable ring path and resident-image
-    path, whole arena compared with the oracle, guard bands checked."""
-    t = synth.llama8b()
+    path, whole arena compared with the oracle, guard bands checked. With a
+    1000-byte header every source offset is 8 mod 16 against 256-aligned
+    destinations: every unit of every large tensor takes the two-word
+    funnel-shift path."""
+    t = synth.llama8b(header=header)
+    assert header == 0 or (t.src_offset % 16 == 8).all()
     plan = ii.ii_plan(t)
     nb, off = plan.tensors()
     assert plan.arena_bytes == plan.payload_bytes == 16_060_522_496
@@ -525,7 +530,7 @@ def test_llama8b_full(orc):
     base = buf.data_ptr() + GUARD
     for mode in ("pageable", "image"):
         buf.fill_(0xA5)
-        _say(f"llama8b: {mode} load")
+        _say(f"llama8b H{header}: {mode} load")
         if mode == "pageable":
             ii.ii_load(plan, blob, base + off)
         else:
