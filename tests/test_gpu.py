@@ -334,6 +334,50 @@ def test_separate_tensor_buffers(orc):
                 assert got[0] == 0x5A
 
 
+@pytest.mark.parametrize("depth,copy_streams", [(1, 1), (2, 1), (2, 2), (3, 2)])
+def test_ring_race_stress(orc, depth, copy_streams):
+    """Slot reuse under pressure (the data-safety rule of Sec. 4.2): 4 KiB
+    chunks (thousands of slot reuses per load), eight loads of four
+    different blobs (pageable and pinned) into four arenas back to back
+    without host syncs, while a second stream keeps the compute units busy
+    with unrelated kernels so that scatters lag behind copies. A copy that
+    overwrote a device slot before the scatter reading it had finished, or a
+    scatter that ran before its copy, would leave wrong bytes."""
+    t = synth.stress(n=3000, chunk=4096, dst_align=16)
+    plan = ii.ii_plan(t)
+    plan.set_ring(depth, 2, copy_streams)
+    _, off = plan.tensors()
+    blobs = [synth.blob(t.blob_bytes, seed=300 + i) for i in range(4)]
+    pins = []
+    for i in (1, 3):
+        hb = ii.ii_host_alloc(blobs[i].size)
+        hb.numpy()[:] = blobs[i]
+        pins.append(hb)
+    srcs = [blobs[0], pins[0], blobs[2], pins[1]]
+    arenas = [torch.zeros(plan.arena_bytes, dtype=torch.uint8, device=DEV) for _ in range(4)]
+    hog = torch.ones(64 << 20, dtype=torch.float32, device=DEV)
+    side = torch.cuda.Stream(DEV)
+    s = torch.cuda.current_stream(DEV)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(side):
+        for _ in range(3000):
+            hog.mul_(1.0)
+    for _ in range(2):
+        for src, a in zip(srcs, arenas):
+            ii.ii_load(plan, src, a.data_ptr() + off, s)
+    s.synchronize()
+    side.synchronize()
+    _say(f"race stress depth {depth} copy streams {copy_streams}: {plan.num_chunks} chunks x 8 loads")
+    nbo = orc.nbytes(t)
+    for i, a in enumerate(arenas):
+        want = np.zeros(plan.arena_bytes, np.uint8)
+        orc.arena(nbo, t.src_offset, t.dst_align, blobs[i], want)
+        got = a.cpu().numpy()
+        if not np.array_equal(got, want):
+            bad = np.flatnonzero(got != want)
+            raise AssertionError(f"arena {i}: {bad.size} bytes differ, first at {int(bad[0])}")
+
+
 def test_back_to_back_loads_no_sync(orc):
     """Two loads on one plan into different arenas with no host sync between
     them: slot reuse carries across calls."""
