@@ -40,7 +40,7 @@
 // address a. The lane loads the aligned 16-byte words at a & ~15 and
 // (a & ~15) + 16 -- each only if it holds a byte the unit needs, so no load
 // touches a 16-byte word outside the source data -- and assembles the block
-// with byte funnel shifts (v_alignbyte). Blocks a segment covers only partly
+// with funnel shifts (v_alignbit_b32). Blocks a segment covers only partly
 // (its first and last block, or a segment shorter than 16 bytes) are
 // written with 8/4/2/1-byte stores of exactly the covered bytes: padding and
 // neighbouring tensors are never read-modify-written.
