@@ -15,6 +15,7 @@ import pytest
 
 import emu
 import oracle_pins
+import random_tables
 from paper_2607_18957_amd import ii, synth
 
 
@@ -198,3 +199,13 @@ def test_offsets_near_2_32(orc):
             t.blob[s:s + n] = rng.integers(0, 256, n, dtype=np.uint8)
         for packed in (False, True):
             _run(orc, t, arena_phase=3, src_phase=7, packed=packed)
+
+
+def test_random_tables(orc):
+    """The GPU suite's seeded random tables (mixed types, gaps, interleaved
+    column blocks, random alignments and chunk sizes), 1000 of them -- the
+    GPU test's 150 first -- in the resident-image and the packed-slot
+    layout."""
+    for case, t, depth, cs in random_tables.cases(2026, 1000):
+        _run(orc, t)
+        _run(orc, t, packed=True)

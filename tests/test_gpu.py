@@ -23,6 +23,7 @@ if not torch.cuda.is_available():  # collected on CPU machines, never run there
 from paper_2607_18957_amd import ii, synth  # noqa: E402  (fails loudly if libii.so is missing)
 
 import oracle_pins  # noqa: E402
+import random_tables  # noqa: E402
 
 DEV = torch.device("cuda:0")
 GUARD = 4096
@@ -904,52 +905,17 @@ def test_concurrent_plans_and_busy_plan(orc):
     _load_arena(orc, tb, plan=pb)
 
 
-def _random_table(rng):
-    """A seeded random table: groups of contiguous tensors of mixed types
-    and groups of interleaved column blocks (strided rows), with gaps, in a
-    shuffled table order, random destination alignments."""
-    width = {1: 1, 5: 2, 7: 4, 9: 8}
-    shapes, codes, src, stride = [], [], [], []
-    pos = int(rng.integers(0, 64))
-    for _ in range(int(rng.integers(1, 5))):
-        if rng.random() < 0.5:
-            R = int(rng.integers(1, 64))
-            ws = [int(x) for x in rng.integers(1, 300, int(rng.integers(1, 4)))]
-            row = sum(ws) + int(rng.integers(0, 100))
-            col = 0
-            for w in ws:
-                shapes.append((R, w)); codes.append(1); src.append(pos + col); stride.append(row)
-                col += w
-            pos += R * row + int(rng.integers(0, 50))
-        else:
-            for _ in range(int(rng.integers(1, 20))):
-                c = int(rng.choice([1, 5, 7, 9]))
-                n = int(rng.integers(0, 5000))
-                shapes.append((n,)); codes.append(c); src.append(pos); stride.append(0)
-                pos += n * width[c] + int(rng.integers(0, 40))
-    order = rng.permutation(len(shapes))
-    t = oracle_pins._T([codes[i] for i in order], [shapes[i] for i in order],
-                       [src[i] for i in order],
-                       [int(rng.choice([1, 2, 16, 256, 4096])) for _ in order])
-    t.src_row_stride = np.array([stride[i] for i in order], np.uint64)
-    t.names = [f"r{i}" for i in range(len(order))]
-    t.name = "random"
-    t.chunk_bytes = 16 * int(rng.integers(1, 65536))
-    t.blob = np.frombuffer(rng.bytes(pos + 64), dtype=np.uint8).copy()
-    return t
-
-
 def test_random_tables_every_mode(orc):
-    """150 seeded random tables (mixed types, gaps, interleaved column blocks,
+    """Seeded random tables (mixed types, gaps, interleaved column blocks,
     alignments 1..4096, chunks of 16 B .. 1 MiB, ring depths 1..3, one or two
-    copy streams), each in every load mode, against the oracle."""
-    rng = np.random.default_rng(2026)
-    for case in range(150):
-        t = _random_table(rng)
-        depth = int(rng.integers(1, 4))
-        cs = int(rng.integers(1, min(depth, 2) + 1))
-        _say(f"random table {case}: N={t.n} chunk={t.chunk_bytes} depth={depth} streams={cs}")
-        for mode in ("pageable", "pinned", "image", "pertensor"):
+    copy streams), each in every load mode, against the oracle: 150 tables,
+    or $II_RANDOM_TABLES (the same sequence, longer)."""
+    count = int(os.environ.get("II_RANDOM_TABLES", "150"))
+    for case, t, depth, cs in random_tables.cases(2026, count):
+        if case % 50 == 0:
+            _say(f"random table {case}: N={t.n} chunk={t.chunk_bytes} depth={depth} streams={cs}")
+        for mode in ("pageable", "pinned", "image", "pertensor", "pertensor-pinned",
+                     "pinned-span"):
             plan = ii.ii_plan(t)
             plan.set_ring(depth, 2, cs)
             _load_arena(orc, t, mode=mode, blob=t.blob, plan=plan)
