@@ -709,32 +709,43 @@ def main() -> int:
     h2d = h2d_peak(torch, dev, plan.chunk_bytes)
     log(f"H2D peak {h2d['GBps']:.2f} GB/s ({h2d['variant']})")
     e2e = {"h2d_peak_GBps": h2d["GBps"], "h2d_peak_variant": h2d["variant"]}
-    def timed_load(src) -> float:
-        t1 = time.perf_counter()
-        ii.ii_load(plan, src, dst, stream)
+    # process CPU time (every thread: host copy pool, HIP runtime) over wall
+    # time of the timed loads: the host cores a load keeps busy
+    cpu_log = []
+
+    def cores(n):
+        c, w = (sum(x) for x in zip(*cpu_log[-n:])) if len(cpu_log) >= n else (0.0, 0.0)
+        cpu_log.clear()
+        return c / w if w else None
+
+    def timed(fn, p, src, d) -> float:
+        c1, t1 = time.process_time(), time.perf_counter()
+        fn(p, src, d, stream)
         torch.cuda.synchronize(dev)
-        return time.perf_counter() - t1
+        w = time.perf_counter() - t1
+        cpu_log.append((time.process_time() - c1, w))
+        return w
+
+    def timed_load(src) -> float:
+        return timed(ii.ii_load, plan, src, dst)
 
     def report(label, times):
         t = statistics.median(times)
         e2e[label] = {"GBps": payload / t / 1e9, "tensors_per_s": table.n / t,
                       "frac_of_h2d_peak": payload / t / 1e9 / h2d["GBps"], "median_s": t,
-                      "runs": len(times)}
+                      "runs": len(times), "host_cores": cores(len(times))}
         log(f"e2e {label}: {payload / t / 1e9:.2f} GB/s "
             f"({100 * payload / t / 1e9 / h2d['GBps']:.1f}% of H2D peak)")
 
     def tp_load(src) -> float:
-        t1 = time.perf_counter()
-        ii.ii_load(tp_plan, src, tp_dst, stream)
-        torch.cuda.synchronize(dev)
-        return time.perf_counter() - t1
+        return timed(ii.ii_load, tp_plan, src, tp_dst)
 
     def tp_report(label, times, link_bytes):
         t = statistics.median(times)
         tp[label] = {"GBps": tp_plan.payload_bytes / t / 1e9, "link_bytes": link_bytes,
                      "link_GBps": link_bytes / t / 1e9,
                      "frac_of_h2d_peak": tp_plan.payload_bytes / t / 1e9 / h2d["GBps"],
-                     "median_s": t, "runs": len(times)}
+                     "median_s": t, "runs": len(times), "host_cores": cores(len(times))}
         log(f"tp shard {label}: {tp_plan.payload_bytes / t / 1e9:.2f} GB/s of shard bytes, "
             f"link {link_bytes / t / 1e9:.2f} GB/s")
 
