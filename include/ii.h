@@ -112,8 +112,9 @@ typedef struct ii_plan_s ii_plan_t; /* opaque */
  * hi)). A segment is one tensor's piece of one chunk (for a tensor given as
  * rows, one row's piece of one chunk), ordered by offset in the chunk.
  * The ring loads skip chunks that hold no segment, and move of each other
- * chunk only its segment bytes (gathered on the host) or the range from its
- * first segment's start to its last segment's end (see ii_plan_copy_bytes).
+ * chunk only its segment bytes (gathered on the host, or copied from a
+ * pinned blob row group by row group) or the range from its first segment's
+ * start to its last segment's end (see ii_plan_copy_bytes).
  * The scatter kernel's tiles take 4096 segment bytes each ($II_TILE_BYTES,
  * read by ii_plan, overrides it: 1024..65536, rounded down to a multiple of
  * 16).
@@ -337,14 +338,19 @@ size_t ii_plan_num_segments(const ii_plan_t* plan);
 uint64_t ii_plan_chunk_bytes(const ii_plan_t* plan);
 uint64_t ii_plan_payload_bytes(const ii_plan_t* plan); /* sum of nbytes */
 uint64_t ii_plan_arena_bytes(const ii_plan_t* plan);
-/* bytes one ii_load from a pinned blob moves from host to device. Per chunk
- * that holds segments: its used range -- first segment's start to last
- * segment's end, rounded out to 256-byte boundaries inside the chunk --
- * which is copied in place, unless more than a quarter of that range is
- * gaps between segments; such a chunk is gathered through the staging slot
- * and moves only its segment bytes. hi - lo for a table whose tensors tile
- * their span. Loads from a pageable blob or a file gather every chunk with
- * gaps and move payload_bytes. */
+/* bytes one ii_load from a pinned blob moves from host to device. A table
+ * whose tensors tile their span: per chunk, its used range -- first
+ * segment's start to last segment's end, rounded out to 256-byte boundaries
+ * inside the chunk -- copied in place (hi - lo in all). A table with gaps
+ * between segments: per chunk that holds segments, only its segment bytes
+ * when its runs (segments adjacent in the file, merged) form at most 2
+ * groups of one run length and one spacing ($II_PINNED_GROUPS_MAX, 0..64)
+ * -- each group is one 1-D or 2-D copy straight from the blob (the rows of
+ * a column block) -- or when more
+ * than a quarter of its used range is gaps (it is then gathered on the host
+ * through the staging slot); otherwise its used range in place. Loads from
+ * a pageable blob or a file gather every chunk with gaps and move
+ * payload_bytes. */
 uint64_t ii_plan_copy_bytes(const ii_plan_t* plan);
 /* Packed staging layout (loads from a pageable blob or a file gather only
  * the segments' bytes of a chunk into its pinned slot, back to back in

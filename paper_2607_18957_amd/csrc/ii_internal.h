@@ -18,6 +18,26 @@ constexpr uint32_t kDefaultTile = 4u << 10;  // segment bytes per workgroup (<= 
 constexpr uint32_t kMaxCopyStreams = 2;       // host-to-device copy streams of a ring
 constexpr uint64_t kIoAlign = 4096;           // block alignment of direct-I/O file reads
 constexpr uint64_t kCopyAlign = 256;          // host-to-device copies start and end on these
+constexpr uint32_t kMaxDmaGroups = 2;         // most copies a pinned chunk is moved with
+
+// How a load from a pinned blob moves one chunk of a plan with gaps.
+enum PinnedMove : uint8_t {
+    kPinnedInPlace = 0,  // one copy of the used range, gaps included, at chunk offsets
+    kPinnedGroups = 1,   // one 1-D or 2-D copy per run group, into the packed layout
+    kPinnedGather = 2,   // host gather into the pinned slot, then one copy
+};
+
+// Runs of a chunk that share one length and one source distance between
+// consecutive starts: count rows of len bytes, the first at chunk offset
+// off, every stride bytes, landing back to back at packed offset poff --
+// what one 2-D host-to-device copy moves (a single run has count 1).
+struct DmaGroup {
+    uint32_t off;
+    uint32_t poff;
+    uint32_t len;
+    uint32_t count;
+    uint32_t stride;
+};
 
 struct Runtime;  // device-side state (runtime.hip)
 
@@ -57,10 +77,13 @@ struct ii_plan_s {
     // adjacent in the chunk (one memcpy): chunk offset run_off, slot offset
     // run_poff, run_len.
     bool packed_distinct = false;  // false: packed layout == chunk layout for every chunk
-    // per chunk: a load from a pinned blob gathers this chunk through the
-    // staging slot too (its used range is more than a quarter gaps), instead
-    // of copying the used range in place
-    std::vector<uint8_t> chunk_gather_pinned;
+    // per chunk: how a load from a pinned blob moves it (PinnedMove) --
+    // by copies of its run groups when it has at most kMaxDmaGroups of them,
+    // else gathered on the host when more than a quarter of its used range
+    // is gaps, else its used range in place
+    std::vector<uint8_t> chunk_pinned;
+    std::vector<uint64_t> chunk_group_begin;  // num_chunks + 1 (plans with gaps)
+    std::vector<ii::DmaGroup> groups;
     std::vector<uint32_t> seg_poff;
     std::vector<uint64_t> chunk_plen;
     std::vector<uint64_t> chunk_run_begin;  // num_chunks + 1

@@ -8,12 +8,16 @@
 //   InDisk -> InMem   host threads bring chunk j's bytes into pinned slot
 //                     j mod D: a copy of its used range, or a gather of only
 //                     its segments when it has gaps (pageable blob or file;
-//                     a pinned blob is copied by DMA straight from itself
-//                     unless the chunk is mostly gaps). The slot is reused
-//                     only once the copy that last read it has finished: host
-//                     wait on copy_done[slot].
-//   InMem  -> InGPU   one hipMemcpyAsync per chunk into device slot j mod D
-//                     on copy stream j mod 2 (1 with a single copy stream:
+//                     a pinned blob is copied by DMA straight from itself,
+//                     row group by row group when a chunk with gaps has few
+//                     of them, and gathered on the host only when it has
+//                     many and is mostly gaps). The slot is reused only once
+//                     the copy that last read it has finished: host wait on
+//                     copy_done[slot].
+//   InMem  -> InGPU   one hipMemcpyAsync per chunk (or one per row group,
+//                     2-D for rows at a fixed stride) into device slot
+//                     j mod D on copy stream j mod 2 (1 with a single copy
+//                     stream:
 //                     copies back to back in chunk order, the paper's
 //                     (C_i,InGPU)->(C_i+1,InMem) edge), after
 //                     scatter_done[slot] (the device slot is free); records
@@ -571,8 +575,11 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         p->chunk_used(k, &u0, &u1);
         const uint64_t cbeg = p->lo + (uint64_t)k * C;  // blob / file offset of the chunk
         const uint64_t at = cbeg + u0;                   // ... and of its used range
-        const bool packed = p->packed_distinct && (!pinned || p->chunk_gather_pinned[k]);
-        const bool staged = !pinned || packed;           // through the pinned slot
+        // a pinned blob's chunk of a plan with gaps: moved in place, by
+        // copies of its run groups, or gathered on the host
+        const uint8_t how = pinned && p->packed_distinct ? p->chunk_pinned[k] : kPinnedInPlace;
+        const bool packed = p->packed_distinct && (!pinned || how != kPinnedInPlace);
+        const bool staged = !pinned || how == kPinnedGather;  // through the pinned slot
         // packed: the slot receives the chunk's runs back to back from offset
         // 0; otherwise the used range keeps its chunk offsets
         const uint64_t r0 = p->chunk_run_begin[k], nr = p->chunk_run_begin[k + 1] - r0;
@@ -616,7 +623,22 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         hipStream_t cs = r->copy_s[j % r->ncopy];
         if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(cs, r->scatter_done[slot], 0));
         if (trace) II_HIP(hipEventRecord(r->tr_cs[j], cs));
-        II_HIP(hipMemcpyAsync(r->dslot[slot] + doff, from, len, hipMemcpyHostToDevice, cs));
+        if (pinned && how == kPinnedGroups) {
+            // one copy per run group straight from the pinned blob into the
+            // packed layout: rows of a group land back to back
+            for (uint64_t gi = p->chunk_group_begin[k]; gi < p->chunk_group_begin[k + 1]; ++gi) {
+                const DmaGroup& g = p->groups[gi];
+                uint8_t* to = r->dslot[slot] + g.poff;
+                const uint8_t* at = blob + cbeg + g.off;
+                if (g.count == 1)
+                    II_HIP(hipMemcpyAsync(to, at, g.len, hipMemcpyHostToDevice, cs));
+                else
+                    II_HIP(hipMemcpy2DAsync(to, g.len, at, g.stride, g.len, g.count,
+                                            hipMemcpyHostToDevice, cs));
+            }
+        } else {
+            II_HIP(hipMemcpyAsync(r->dslot[slot] + doff, from, len, hipMemcpyHostToDevice, cs));
+        }
         II_HIP(hipEventRecord(r->copy_done[slot], cs));
         if (trace) II_HIP(hipEventRecord(r->tr_ce[j], cs));
         r->copy_rec[slot] = 1;

@@ -7,20 +7,19 @@
 // checks the structural invariants that need no oracle: segments tile each
 // tensor exactly, lie inside their chunk and inside one row, and are
 // ordered; tiles take tile_bytes of segment bytes each with contiguous
-// windows; the copied bytes lie between the payload and the span. Any sanitizer report or failed check exits non-zero.
+// windows; the copied bytes lie between the payload and the span; a pinned
+// chunk's group copies rebuild the packed layout of its runs. Any sanitizer
+// report or failed check exits non-zero.
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <vector>
 
 #include "ii.h"
+#include "ii_internal.h"
 
 namespace ii {
-struct ii_unused;
-}
-struct ii_plan_s;
-namespace ii {
-void runtime_destroy(ii_plan_s*) {}  // no device state in a host-only build
+void runtime_destroy(ii_plan_t*) {}  // no device state in a host-only build
 }
 
 static uint64_t rng_state = 88172645463325252ull;
@@ -191,6 +190,57 @@ int main(int argc, char** argv) {
                 }
             }
             CHECK(g == G);
+            // pinned-blob moves: a grouped chunk's copies (rows of len bytes
+            // every stride bytes, landing back to back) rebuild exactly the
+            // packed layout the host gather makes from the chunk's runs;
+            // copy_bytes sums what each chunk's move carries
+            {
+                const ii_plan_s* ip = p;
+                uint64_t moved = 0;
+                for (size_t k = 0; k < K; ++k) {
+                    uint64_t ub, ue;
+                    ip->chunk_used(k, &ub, &ue);
+                    if (!ip->packed_distinct) {
+                        moved += ue - ub;
+                        continue;
+                    }
+                    const uint8_t how = ip->chunk_pinned[k];
+                    const uint64_t g0 = ip->chunk_group_begin[k], g1 = ip->chunk_group_begin[k + 1];
+                    const uint64_t r0 = ip->chunk_run_begin[k], r1 = ip->chunk_run_begin[k + 1];
+                    moved += how == ii::kPinnedInPlace ? ue - ub : plen[k];
+                    if (how != ii::kPinnedGroups) {
+                        CHECK(g0 == g1);
+                        if (how == ii::kPinnedGather) CHECK(4 * (ue - ub - plen[k]) > ue - ub);
+                        continue;
+                    }
+                    const char* gm = getenv("II_PINNED_GROUPS_MAX");
+                    CHECK(g1 - g0 <= (gm && *gm ? strtoull(gm, nullptr, 10) : ii::kMaxDmaGroups));
+                    std::vector<uint8_t> chunk(cl[k]), a(plen[k], 0xEE), b(plen[k], 0xDD);
+                    for (uint64_t x = 0; x < cl[k]; ++x) chunk[x] = (uint8_t)(x * 131 + k * 7 + 1);
+                    for (uint64_t r = r0; r < r1; ++r) {
+                        CHECK((uint64_t)ip->run_off[r] + ip->run_len[r] <= cl[k]);
+                        CHECK((uint64_t)ip->run_poff[r] + ip->run_len[r] <= plen[k]);
+                        for (uint32_t y = 0; y < ip->run_len[r]; ++y)
+                            a[ip->run_poff[r] + y] = chunk[ip->run_off[r] + y];
+                    }
+                    uint64_t rows = 0;
+                    for (uint64_t gi = g0; gi < g1; ++gi) {
+                        const ii::DmaGroup& gr = ip->groups[gi];
+                        CHECK(gr.count >= 1 && gr.len > 0);
+                        if (gr.count > 1) CHECK(gr.stride > gr.len);
+                        CHECK((uint64_t)gr.off + (uint64_t)(gr.count - 1) * gr.stride + gr.len <= cl[k]);
+                        CHECK((uint64_t)gr.poff + (uint64_t)gr.count * gr.len <= plen[k]);
+                        for (uint32_t q = 0; q < gr.count; ++q)
+                            for (uint32_t y = 0; y < gr.len; ++y)
+                                b[gr.poff + (uint64_t)q * gr.len + y] =
+                                    chunk[gr.off + (uint64_t)q * gr.stride + y];
+                        rows += gr.count;
+                    }
+                    CHECK(rows == r1 - r0);
+                    CHECK(a == b);
+                }
+                CHECK(moved == ii_plan_copy_bytes(p));
+            }
             ii_plan_free(p);
         }
     }

@@ -230,12 +230,37 @@ def test_empty_plan():
 
 # -- tables given as rows (tensor-parallel shards) ----------------------------
 
-def _expected_copy_bytes(op, align=256):
-    """Bytes a load from a pinned blob moves: per chunk that holds segments,
-    the used range (first segment start to last segment end, rounded out to
-    `align` inside the chunk), or only the segment bytes where more than a
-    quarter of the used range is gaps (when any chunk of the table has
-    gaps)."""
+def _run_groups(offs, lens):
+    """Runs of one chunk's segments (adjacent ones merged) and the number of
+    groups they form: consecutive runs of one length, equally spaced."""
+    runs = []
+    for o, l in zip(offs, lens):
+        if runs and runs[-1][0] + runs[-1][1] == o:
+            runs[-1][1] += l
+        else:
+            runs.append([o, l])
+    groups, j = 0, 0
+    while j < len(runs):
+        groups += 1
+        q, stride = j + 1, None
+        while q < len(runs) and runs[q][1] == runs[j][1]:
+            d = runs[q][0] - runs[q - 1][0]
+            if stride is not None and d != stride:
+                break
+            stride = d
+            q += 1
+        j = q
+    return runs, groups
+
+
+def _expected_copy_bytes(op, align=256, max_groups=2):
+    """Bytes a load from a pinned blob moves. A table without gaps: per chunk
+    that holds segments, the used range (first segment start to last segment
+    end, rounded out to `align` inside the chunk). A table with gaps: per
+    chunk, only its segment bytes when its runs form at most `max_groups`
+    groups of equal length and spacing (one 1-D or 2-D copy each) or when
+    more than a quarter of its used range is gaps (gathered on the host),
+    else its used range."""
     total = 0
     ch, off, ln = op["seg_chunk"], op["seg_chunk_off"].astype(np.int64), op["seg_len"].astype(np.int64)
     dense = all(int(ln[ch == k].sum()) == int(op["chunk_len"][k])
@@ -245,7 +270,11 @@ def _expected_copy_bytes(op, align=256):
         b = int(off[m].min()) // align * align
         e = min(int(op["chunk_len"][k]), -(-int((off[m] + ln[m]).max()) // align) * align)
         payload = int(ln[m].sum())
-        total += payload if (not dense and 4 * (e - b - payload) > e - b) else e - b
+        if dense:
+            total += e - b
+            continue
+        _, groups = _run_groups([int(x) for x in off[m]], [int(x) for x in ln[m]])
+        total += payload if (groups <= max_groups or 4 * (e - b - payload) > e - b) else e - b
     return total
 
 

@@ -4,6 +4,8 @@ structural invariants), and the host copy pool with ThreadSanitizer."""
 import os
 import subprocess
 
+import pytest
+
 import sanitize
 
 
@@ -13,13 +15,22 @@ def _bin(path):
     return path
 
 
-def test_planner_asan_ubsan():
-    r = subprocess.run([_bin(sanitize.PLAN_BIN), "3000"], capture_output=True, text=True,
-                       timeout=600)
+@pytest.mark.parametrize("groups_max,iters", [(None, 3000), ("64", 1000)],
+                         ids=["default", "groups64"])
+def test_planner_asan_ubsan(groups_max, iters):
+    """The default planner, and one that moves every pinned chunk of up to 64
+    run groups by group copies (so that the group layout check meets many
+    groups per chunk)."""
+    env = dict(os.environ)
+    env.pop("II_PINNED_GROUPS_MAX", None)
+    if groups_max:
+        env["II_PINNED_GROUPS_MAX"] = groups_max
+    r = subprocess.run([_bin(sanitize.PLAN_BIN), str(iters)], capture_output=True, text=True,
+                       timeout=600, env=env)
     assert r.returncode == 0, r.stdout + r.stderr
     assert r.stdout.startswith("OK"), r.stdout
     plans = int(r.stdout.split("plans=")[1].split()[0])
-    assert plans > 12000  # most tables are valid and fully checked
+    assert plans > 4 * iters  # most tables are valid and fully checked
 
 
 def test_copy_pool_tsan():
