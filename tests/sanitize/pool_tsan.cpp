@@ -105,14 +105,23 @@ int main() {
     }
     // gathers: many runs (rows of a sharded tensor) from memory and from the
     // file, split across threads by destination bytes; every byte checked
-    // against a one-run-at-a-time copy, nothing written past the end
-    {
+    // against a one-run-at-a-time copy, nothing written past the end. Run
+    // patterns: rows of up to 9000 bytes with short gaps; thousands of tiny
+    // runs (a file batch fills its iovecs and starts another); and groups of
+    // runs separated by gaps longer than a file batch reads through
+    struct Pattern { uint64_t span; uint32_t gap_mod, run_mod, big_gap_every; };
+    const Pattern patterns[] = {{6u << 20, 700, 9000, 0}, {96u << 10, 32, 16, 0},
+                                {8u << 20, 700, 9000, 200}};
+    for (const Pattern& pat : patterns) {
         std::vector<uint32_t> off, poff, len;
         uint64_t s = 0, total = 0;
         uint32_t x = 12345;
-        while (s < (2u << 20)) {
+        while (s < pat.span) {
             x = x * 1103515245u + 12345u;
-            const uint32_t gap = (x >> 8) % 700, run = 1 + (x >> 16) % 9000;
+            uint32_t gap = (x >> 8) % pat.gap_mod;
+            const uint32_t run = 1 + (x >> 16) % pat.run_mod;
+            if (pat.big_gap_every && off.size() % pat.big_gap_every == pat.big_gap_every - 1)
+                gap += 300u << 10;
             s += gap;
             off.push_back((uint32_t)s);
             poff.push_back((uint32_t)total);
@@ -120,6 +129,7 @@ int main() {
             s += run;
             total += run;
         }
+        if (4096 + s > fsz || total >= dst.size()) return 3;  // inside the file and dst
         const int64_t skews[] = {0, (int64_t)off[0], -64};  // b0[0] at, past, before offset 0
         for (uint32_t threads : {1u, 3u, 8u}) {
             ii::CopyPool pool(threads);

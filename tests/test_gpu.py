@@ -79,6 +79,18 @@ def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=N
         hb = ii.ii_host_alloc(blob.size)
         hb.numpy()[:] = blob
         ii.ii_load(plan, hb, base + off, s)
+    elif mode == "file":
+        # buffered reads from a tmpfs file (run batches read with preadv)
+        import tempfile
+        fd, path = tempfile.mkstemp(dir="/dev/shm" if os.path.isdir("/dev/shm") else None)
+        try:
+            with os.fdopen(os.dup(fd), "wb") as fh:
+                fh.write(memoryview(blob))
+            ii.ii_load_file(plan, fd, base + off, s, file_bytes=blob.size)
+            s.synchronize()
+        finally:
+            os.close(fd)
+            os.unlink(path)
     elif mode == "pinned-span":
         # only the span [lo, hi) is pinned; blob byte 0 lies before it
         lo, hi = plan.span
@@ -908,14 +920,15 @@ def test_concurrent_plans_and_busy_plan(orc):
 def test_random_tables_every_mode(orc):
     """Seeded random tables (mixed types, gaps, interleaved column blocks,
     alignments 1..4096, chunks of 16 B .. 1 MiB, ring depths 1..3, one or two
-    copy streams), each in every load mode, against the oracle: 150 tables,
-    or $II_RANDOM_TABLES (the same sequence, longer)."""
+    copy streams), each in every load mode (a tmpfs file included), against
+    the oracle: 150 tables, or $II_RANDOM_TABLES (the same sequence,
+    longer)."""
     count = int(os.environ.get("II_RANDOM_TABLES", "150"))
     for case, t, depth, cs in random_tables.cases(2026, count):
         if case % 50 == 0:
             _say(f"random table {case}: N={t.n} chunk={t.chunk_bytes} depth={depth} streams={cs}")
         for mode in ("pageable", "pinned", "image", "pertensor", "pertensor-pinned",
-                     "pinned-span"):
+                     "pinned-span", "file"):
             plan = ii.ii_plan(t)
             plan.set_ring(depth, 2, cs)
             _load_arena(orc, t, mode=mode, blob=t.blob, plan=plan)
