@@ -422,6 +422,12 @@ def all_configs(torch, dev, ii, synth) -> dict:
             synth.fill(pinned.ptr, 0, blob.size, t.seed)
             row["pinned_first"] = rate(plan, e2e(plan, pinned, dst, 1)[0])
             row["pinned"] = rate(plan, statistics.median(e2e(plan, pinned, dst, reps)))
+            # the same pinned blob read by the image kernel over the link
+            # (ii_load_device on host memory: no ring, no copy engine)
+            img = (pinned.ptr, blob.size)
+            e2e(plan, img, dst, 1, ii.ii_load_device)
+            row["pinned_kernel_reads"] = rate(
+                plan, statistics.median(e2e(plan, img, dst, reps, ii.ii_load_device)))
             pinned.free()
         if cid == "C2":
             # the naive per-tensor pipeline on the same table: what merging saves

@@ -216,7 +216,10 @@ int ii_load_file(ii_plan_t* plan, int fd, uint64_t file_bytes, void* const* dst_
  *
  *   dev_image    device address of blob byte 0 (any alignment); the span
  *                [dev_image + lo, + hi) must lie inside one device allocation
- *                or in pinned host memory (checked, II_EINVAL).
+ *                or in pinned host memory (checked, II_EINVAL). From pinned
+ *                host memory the kernel reads the blob over the host link
+ *                itself: no ring and no copy engine, one launch -- the
+ *                lowest latency for small loads.
  *   image_bytes  size of the image; must be >= the plan's span end hi.
  *   dst_ptrs     as for ii_load; must not overlap [dev_image, +hi).
  *   stream       the kernel runs on this stream, after the work already on

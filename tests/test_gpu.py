@@ -100,6 +100,11 @@ def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=N
     elif mode == "image":
         img = torch.from_numpy(blob).to(DEV)
         ii.ii_load_device(plan, img, base + off, s)
+    elif mode == "image-pinned":
+        # the image kernel reading a pinned host blob over the link
+        hb = ii.ii_host_alloc(blob.size)
+        hb.numpy()[:] = blob
+        ii.ii_load_device(plan, (hb.ptr, blob.size), base + off, s)
     elif mode == "pertensor":
         ii.ii_load_pertensor(plan, blob, base + off, s)
     elif mode == "pertensor-pinned":
@@ -215,7 +220,7 @@ def test_image_more_tiles_than_one_dispatch(orc, monkeypatch):
     _say("many tiles: bit-exact")
 
 
-@pytest.mark.parametrize("mode", ["pageable", "pinned", "image"])
+@pytest.mark.parametrize("mode", ["pageable", "pinned", "image", "image-pinned"])
 def test_tiny(orc, mode):
     _load_arena(orc, synth.tiny(), mode=mode)
 
@@ -227,7 +232,7 @@ def test_tiny_padded_and_offset(orc, mode):
     _load_arena(orc, synth.tiny(dst_align=1, header=5), mode=mode)
 
 
-@pytest.mark.parametrize("mode", ["pageable", "pinned", "image"])
+@pytest.mark.parametrize("mode", ["pageable", "pinned", "image", "image-pinned"])
 def test_stress_full(orc, mode):
     """100,000 tensors, 64 B - 64 KiB, 94% of them at a different phase in the
     source than in the destination, 16 MiB chunks."""
@@ -927,8 +932,8 @@ def test_random_tables_every_mode(orc):
     for case, t, depth, cs in random_tables.cases(2026, count):
         if case % 50 == 0:
             _say(f"random table {case}: N={t.n} chunk={t.chunk_bytes} depth={depth} streams={cs}")
-        for mode in ("pageable", "pinned", "image", "pertensor", "pertensor-pinned",
-                     "pinned-span", "file"):
+        for mode in ("pageable", "pinned", "image", "image-pinned", "pertensor",
+                     "pertensor-pinned", "pinned-span", "file"):
             plan = ii.ii_plan(t)
             plan.set_ring(depth, 2, cs)
             _load_arena(orc, t, mode=mode, blob=t.blob, plan=plan)
