@@ -614,8 +614,8 @@ def main() -> int:
                          "8B, 70B, switch) and print one JSON line of results")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
-              "(multi-GPU loading is a design note, not built)", file=sys.stderr)
+        print(f"bench.py: the loader runs on one GPU; --gpus {args.gpus} is not supported "
+              "(loading across GPUs is designed but not implemented)", file=sys.stderr)
         return 2
 
     import torch
