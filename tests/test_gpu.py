@@ -922,6 +922,22 @@ def test_concurrent_plans_and_busy_plan(orc):
     _load_arena(orc, tb, plan=pb)
 
 
+def test_pinned_group_copies_any_count(orc, monkeypatch):
+    """Pinned blobs with every chunk of up to 64 run groups moved by group
+    copies ($II_PINNED_GROUPS_MAX=64; the default stops at 2): the random
+    tables' interleaved column blocks then take dozens of 1-D and 2-D copies
+    per chunk, into the same packed slot layout the host gather makes."""
+    monkeypatch.setenv("II_PINNED_GROUPS_MAX", "64")
+    for case, t, depth, cs in random_tables.cases(2026, 150):
+        for mode in ("pinned", "pinned-span"):
+            plan = ii.ii_plan(t)
+            plan.set_ring(depth, 2, cs)
+            _load_arena(orc, t, mode=mode, blob=t.blob, plan=plan)
+            plan.free()
+    for t in (synth.tiny_tp(1, 4, chunk=65552), synth.tiny_tp(3, 8, chunk=1 << 16)):
+        _load_arena(orc, t, mode="pinned")
+
+
 def test_random_tables_every_mode(orc):
     """Seeded random tables (mixed types, gaps, interleaved column blocks,
     alignments 1..4096, chunks of 16 B .. 1 MiB, ring depths 1..3, one or two

@@ -330,6 +330,28 @@ def test_tp_shards_tiny(orc, size):
             _compare_rows(orc, t, chunk)
 
 
+@pytest.mark.parametrize("groups_max", [0, 1, 64])
+def test_pinned_copy_bytes_by_group_limit(orc, monkeypatch, groups_max):
+    """What a pinned-blob load moves, for every limit on the run groups a
+    chunk may be copied in ($II_PINNED_GROUPS_MAX): column-block shards and
+    interleaved column blocks, against the count made from the oracle's
+    segments."""
+    monkeypatch.setenv("II_PINNED_GROUPS_MAX", str(groups_max))
+    rng = random.Random(groups_max)
+    tables = [synth.tiny_tp(1, 4), synth.tiny_tp(0, 2), synth.tiny_tp(5, 8)]
+    for _ in range(20):
+        tables.append(_column_blocks(rng, rng.randint(1, 6), rng.randint(1, 40),
+                                     rng.randint(0, 50), rng.randint(0, 40), rng.randint(0, 4)))
+    for t in tables:
+        for chunk in (getattr(t, "chunk_bytes", 0) or 4096, 4096 + 16, 1 << 16):
+            plan = ii.ii_plan(t, chunk)
+            nb = orc.nbytes(t)
+            op = orc.plan_rows(nb, t.src_offset, orc.rows(t, nb),
+                               np.asarray(t.src_row_stride, np.uint64), chunk)
+            assert plan.copy_bytes == _expected_copy_bytes(op, max_groups=groups_max), chunk
+            plan.free()
+
+
 def test_tp_shard_llama8b(orc):
     t = synth.llama8b_tp(1, 4)
     plan = _compare_rows(orc, t)
