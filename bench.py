@@ -793,6 +793,13 @@ def main() -> int:
     tp_load(pinned)
     tp_report("e2e_pinned", [tp_load(pinned) for _ in range(args.e2e_reps)],
               tp_plan.copy_bytes)
+    # the same pinned blob read by the gaps kernel itself (ii_load_device on
+    # host memory): only the shard's rows cross the link, no ring
+    pinned_img = (pinned.ptr, blob.size)
+    timed(ii.ii_load_device, tp_plan, pinned_img, tp_dst)
+    tp_report("e2e_pinned_kernel_reads",
+              [timed(ii.ii_load_device, tp_plan, pinned_img, tp_dst)
+               for _ in range(args.e2e_reps)], tp_plan.payload_bytes)
     e2e["ring"] = {"depth": 3, "copy_streams": 2, "chunk_bytes": plan.chunk_bytes}
     e2e["host_threads"] = int(os.environ.get("II_HOST_THREADS", min(8, os.cpu_count() or 1)))
     pinned.free()
