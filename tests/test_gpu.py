@@ -635,7 +635,7 @@ def test_switch_llama8b_to_mistral7b(orc):
 
 # -- tensor-parallel shards: tables given as rows ------------------------------
 
-@pytest.mark.parametrize("mode", ["pageable", "pinned", "image", "pertensor",
+@pytest.mark.parametrize("mode", ["pageable", "pinned", "image", "image-pinned", "pertensor",
                                   "pertensor-pinned"])
 def test_tp_shards_tiny(orc, mode):
     """Every rank's shard of the unsharded tiny file, in every load mode:
