@@ -5,7 +5,6 @@ import os
 import subprocess
 import sys
 
-
 import bench
 from paper_2607_18957_amd import ii, synth
 
