@@ -144,10 +144,13 @@ void ii_plan_free(ii_plan_t* plan);
  * ii_load -- materialise every tensor of the plan from a host blob into
  * device memory (Sec. 4.2). For each chunk that holds a segment, in order:
  * bring its bytes into a pinned host slot (its used range, or only its
- * segments' bytes, packed, when it has gaps between segments; a pinned
- * blob's chunk is instead copied by DMA straight from the blob unless more
- * than a quarter of it is gaps), copy it to a device slot with one
- * hipMemcpyAsync, then scatter it into its tensors with the device kernel.
+ * segments' bytes, packed, when it has gaps between segments), copy it to a
+ * device slot with one hipMemcpyAsync, then scatter it into its tensors
+ * with the device kernel. A pinned blob's chunk skips the host slot: it is
+ * copied straight from the blob -- its used range in one copy, or, when it
+ * has gaps, its run groups in one 1-D or 2-D copy each (see
+ * ii_plan_copy_bytes; a chunk of many groups that is mostly gaps is still
+ * gathered through the host slot).
  * Chunks holding no segment are not touched. Chunk k+1's copy overlaps
  * chunk k's scatter; a slot is
  * reused only after the scatter that read it has finished (Sec. 4.2:
@@ -191,9 +194,10 @@ int ii_load(ii_plan_t* plan, const void* host_blob, uint64_t blob_bytes, void* c
 /*
  * ii_load_file -- the same materialisation with the blob read from a file
  * (the model file on storage or on tmpfs; Sec. 4.2 InDisk -> InMem, Sec. 5):
- * the host threads read each chunk's bytes (only its segments' bytes, run by
- * run, when it has gaps) with pread straight into a pinned slot, then the
- * copy and scatter steps run as in ii_load. If fd was opened
+ * the host threads read each chunk's bytes (only its segments' bytes when it
+ * has gaps: each thread's runs in batched preadv calls, run bytes straight
+ * into place, gaps under 256 KiB into a scratch buffer) into a pinned slot,
+ * then the copy and scatter steps run as in ii_load. If fd was opened
  * with O_DIRECT, every read starts and ends on a 4096-byte boundary and
  * bypasses the page cache; those reads land in a page-aligned host buffer
  * (device-pinned pages cannot be targets of direct I/O), read ahead by
@@ -267,7 +271,8 @@ int ii_load_pertensor(ii_plan_t* plan, const void* host_blob, uint64_t blob_byte
  *                II_EINVAL, since the scrub may write anywhere in the old
  *                layout.
  *   host_blob_new, blob_bytes, stream   as for ii_load.
- * Errors: as ii_load, plus II_EARENA; all checks run before anything is
+ * Errors: as ii_load, plus II_EARENA, and II_EOVERFLOW when arena +
+ * arena_bytes does not fit in 64 bits; all checks run before anything is
  * enqueued.
  */
 int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint64_t arena_bytes,
@@ -349,16 +354,16 @@ uint64_t ii_plan_arena_bytes(const ii_plan_t* plan);
  * when its runs (segments adjacent in the file, merged) form at most 2
  * groups of one run length and one spacing ($II_PINNED_GROUPS_MAX, 0..64)
  * -- each group is one 1-D or 2-D copy straight from the blob (the rows of
- * a column block) -- or when more
- * than a quarter of its used range is gaps (it is then gathered on the host
- * through the staging slot); otherwise its used range in place. Loads from
- * a pageable blob or a file gather every chunk with gaps and move
- * payload_bytes. */
+ * a column block) -- or when more than a quarter of its used range is gaps
+ * (it is then gathered on the host through the staging slot); otherwise its
+ * used range in place. Loads from a pageable blob or a file gather every
+ * chunk with gaps and move payload_bytes. */
 uint64_t ii_plan_copy_bytes(const ii_plan_t* plan);
 /* Packed staging layout (loads from a pageable blob or a file gather only
  * the segments' bytes of a chunk into its pinned slot, back to back in
- * segment order): per segment its offset in the slot (num_segments), per
- * chunk the bytes staged (num_chunks). For a table whose tensors tile their
+ * segment order; a pinned blob's group copies land in the same layout): per
+ * segment its offset in the slot (num_segments), per chunk the bytes staged
+ * (num_chunks). For a table whose tensors tile their
  * span this equals the chunk layout. NULL skips a field. Errors: II_EINVAL
  * (NULL plan). */
 int ii_plan_packing(const ii_plan_t* plan, uint32_t* seg_off, uint64_t* chunk_len);
