@@ -166,6 +166,41 @@ class Oracle:
             raise OracleError(rc, "load")
         return outs
 
+    def load_into(self, nbytes, src_offset, blob: np.ndarray, outs) -> None:
+        """The sequential loader into caller buffers (contiguous uint8 numpy
+        arrays of at least nbytes[i] bytes each), e.g. one reused buffer per
+        tensor when a set is too large to hold twice."""
+        nb, so = _u64(nbytes), _u64(src_offset)
+        assert len(outs) == len(nb)
+        for o, n in zip(outs, nb):
+            assert o.dtype == np.uint8 and o.flags.c_contiguous and o.size >= int(n)
+        ptrs = (ctypes.c_void_p * max(1, len(nb)))(*[o.ctypes.data for o in outs])
+        rc = self.lib.orc_load_into(len(nb), nb, so, blob.ctypes.data, blob.size,
+                                    ctypes.cast(ptrs, ctypes.c_void_p))
+        if rc:
+            raise OracleError(rc, "load")
+
+    def load_alloc(self, nbytes, src_offset, dst_align, blob: np.ndarray) -> list:
+        """The allocate-and-copy loader, its buffers read back: per tensor
+        (address of the buffer it allocated, copy of its nbytes bytes);
+        address 0 for empty tensors. The buffers are freed again."""
+        nb = _u64(nbytes)
+        ptrs = (ctypes.c_void_p * max(1, len(nb)))()
+        rc = self.lib.orc_load_alloc(len(nb), nb, _u64(src_offset), _u64(dst_align),
+                                     blob.ctypes.data, blob.size, ctypes.cast(ptrs, _vp))
+        try:
+            if rc:
+                raise OracleError(rc, "load_alloc")
+            out = []
+            for i, n in enumerate(nb):
+                a = ptrs[i] or 0
+                data = (np.frombuffer(ctypes.string_at(a, int(n)), dtype=np.uint8).copy()
+                        if a and n else np.empty(0, np.uint8))
+                out.append((a, data))
+            return out
+        finally:
+            self.lib.orc_free(len(nb), ctypes.cast(ptrs, _vp))
+
     def load_alloc_timed(self, nbytes, src_offset, dst_align, blob: np.ndarray) -> None:
         """Allocate-and-copy loader (what a plain program runs); frees the
         buffers again. Used to time the CPU baseline."""

@@ -23,6 +23,9 @@ What pins what (InstantInfer, arXiv 2607.18957):
   * loader result      -- special cases that reduce to one plain copy of the
                           blob (Theorem 2: the result equals the sequential
                           program's; a dense same-order table is one copy);
+                          position-tagged blobs for both loaders, and for the
+                          allocating one the alignment and distinctness of
+                          every buffer it returns;
   * switch             -- degenerate cases that reduce to a plain load, to
                           no change, or to pure clearing (Sec. 4.3 reading);
   * tables given as rows (tensor-parallel shards, Sec. 2.2 / Sec. 6.1) --
@@ -360,6 +363,52 @@ def pin_load(orc):
         raise AssertionError("range error not reported")
 
 
+def pin_load_alloc(orc):
+    """The allocate-and-copy loader (the one the CPU baseline times): every
+    non-empty tensor gets a buffer of its own, aligned to max(16, dst_align),
+    holding exactly its source bytes; empty tensors get none."""
+    rng = np.random.default_rng(15)
+    # one tensor = one plain copy of its slice, at every alignment
+    blob = rng.integers(0, 256, size=100_000, dtype=np.uint8)
+    for s, n, a in [(0, 1, 1), (13, 4096, 16), (99_000, 1000, 4096), (7, 33, 65536), (5, 0, 8)]:
+        ((addr, out),) = orc.load_alloc([n], [s], [a], blob)
+        assert out.tobytes() == blob.tobytes()[s:s + n]
+        assert (addr == 0) == (n == 0)
+        assert addr % max(16, a) == 0
+    # permuted order with gaps and mixed alignments: position tags say where
+    # each byte came from
+    tags = np.arange(20_000, dtype=np.uint32)
+    tb = tags.view(np.uint8)
+    n = 24
+    sizes = [4 * int(x) for x in rng.integers(0, 300, size=n)]
+    sizes[-1] = max(sizes[-1], 4)           # the last tensor is never empty
+    aligns = [int(x) for x in rng.choice([1, 2, 16, 64, 256, 4096], size=n)]
+    perm = rng.permutation(n)
+    src, pos = [0] * n, 0
+    for i in perm:
+        src[i] = pos
+        pos += sizes[i] + 4 * int(rng.integers(0, 3))
+    got = orc.load_alloc(sizes, src, aligns, tb)
+    assert len(got) == n
+    live = []
+    for i, (addr, out) in enumerate(got):
+        if sizes[i] == 0:
+            assert addr == 0 and out.size == 0, i
+            continue
+        assert addr and addr % max(16, aligns[i]) == 0, (i, addr, aligns[i])
+        assert np.array_equal(out.view(np.uint32),
+                              np.arange(src[i] // 4, src[i] // 4 + sizes[i] // 4)), i
+        live.append(addr)
+    assert len(set(live)) == len(live)      # one buffer per tensor
+    # a source range past the blob end is an error
+    try:
+        orc.load_alloc([10], [99_995], [16], blob)
+    except Exception as e:
+        assert getattr(e, "code", None) == ERANGE
+    else:
+        raise AssertionError("range error not reported")
+
+
 def pin_arena(orc):
     rng = np.random.default_rng(6)
     blob = rng.integers(0, 256, size=40_000, dtype=np.uint8)
@@ -668,7 +717,7 @@ def pin_rows_check(orc):
 
 
 # cheapest first (pin_esize imports torch), so a broken oracle fails fast
-PINS = [pin_sizes, pin_appendix_counts, pin_check, pin_load, pin_arena, pin_switch, pin_empty,
+PINS = [pin_sizes, pin_appendix_counts, pin_check, pin_load, pin_load_alloc, pin_arena, pin_switch, pin_empty,
         pin_segments_bytewise, pin_coverage, pin_rows_check, pin_rows_contiguous,
         pin_rows_bytewise, pin_chunks, pin_layout, pin_rows_numpy_shards, pin_esize]
 

@@ -49,6 +49,13 @@ MUTANTS = [
      "return ORC_ERANGE;\n        memcpy(out[i], blob + src_offset[i] + 1, nbytes[i] - 1);"),
     ("load skips the last tensor", "for (size_t i = 0; i < n; ++i) {\n        if (nbytes[i] == 0)\n            continue;\n        if (src_offset[i] > blob_len || nbytes[i] > blob_len - src_offset[i])\n            return ORC_ERANGE;\n        memcpy(out[i]",
      "for (size_t i = 0; i + 1 < n; ++i) {\n        if (nbytes[i] == 0)\n            continue;\n        if (src_offset[i] > blob_len || nbytes[i] > blob_len - src_offset[i])\n            return ORC_ERANGE;\n        memcpy(out[i]"),
+    ("alloc load reads one byte late",
+     "return ORC_EINVAL;\n        memcpy(out[i], blob + src_offset[i], nbytes[i]);",
+     "return ORC_EINVAL;\n        memcpy(out[i], blob + src_offset[i] + 1, nbytes[i] - 1);"),
+    ("alloc load skips the last tensor", "for (size_t i = 0; i < n; ++i) {\n        if (nbytes[i] == 0)\n            continue;\n        if (src_offset[i] > blob_len || nbytes[i] > blob_len - src_offset[i])\n            return ORC_ERANGE;\n        uint64_t a",
+     "for (size_t i = 0; i + 1 < n; ++i) {\n        if (nbytes[i] == 0)\n            continue;\n        if (src_offset[i] > blob_len || nbytes[i] > blob_len - src_offset[i])\n            return ORC_ERANGE;\n        uint64_t a"),
+    ("alloc ignores dst_align", "uint64_t a = dst_align[i] < 16 ? 16 : dst_align[i];",
+     "uint64_t a = 16;"),
     ("arena writes at source offset", "memcpy(arena + off[i], blob + src_offset[i], nbytes[i]);",
      "memcpy(arena + src_offset[i], blob + src_offset[i], nbytes[i]);"),
     ("switch clears half of each old tensor", "memset(arena + off[i], 0, nbytes_old[i]);",
