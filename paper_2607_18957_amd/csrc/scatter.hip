@@ -192,10 +192,10 @@ __global__ __launch_bounds__(kBlock) void scatter_slot(
     scatter_tile(reinterpret_cast<uint64_t>(slot), w0, w1, td.first, td.last, segs);
 }
 
-// Resident-image path: every tile of every chunk (launched in batches of at
-// most kMaxGridBlocks workgroups, tile g0 first); `span` is the
-// device address of the blob's span byte lo, so chunk k starts at span +
-// k * chunk_bytes. This kernel serves tables whose segments fill every chunk
+// Resident-image path: every tile of every chunk in one dispatch (a grid of
+// gy rows of gx workgroups, see grid_shape; tile g = y * gx + x, none past
+// ntiles); `span` is the device address of the blob's span byte lo, so chunk
+// k starts at span + k * chunk_bytes. This kernel serves tables whose segments fill every chunk
 // with no gap: every chunk but the last has per_chunk = ceil(chunk_bytes /
 // tile_bytes) tiles, tile g is tile g % per_chunk of chunk g / per_chunk,
 // and its window is that share of the chunk, so a workgroup reads only its
@@ -203,8 +203,9 @@ __global__ __launch_bounds__(kBlock) void scatter_slot(
 __global__ __launch_bounds__(kBlock) void scatter_image(
     const uint8_t* __restrict__ span, const TileDev* __restrict__ tiles,
     const SegDev* __restrict__ segs, uint64_t chunk_bytes, uint64_t last_len,
-    uint32_t num_chunks, uint32_t per_chunk, uint32_t tile_bytes, uint32_t g0) {
-    const uint32_t g = g0 + blockIdx.x;
+    uint32_t num_chunks, uint32_t per_chunk, uint32_t tile_bytes, uint32_t ntiles) {
+    const uint32_t g = blockIdx.y * gridDim.x + blockIdx.x;
+    if (g >= ntiles) return;
     const TileDev td = tiles[g];
     const uint32_t k = g / per_chunk;
     const uint64_t clen = (k + 1 == num_chunks) ? last_len : chunk_bytes;
@@ -220,8 +221,9 @@ __global__ __launch_bounds__(kBlock) void scatter_image(
 __global__ __launch_bounds__(kBlock) void scatter_image_gaps(
     const uint8_t* __restrict__ span, const TileDev* __restrict__ tiles,
     const TileWin* __restrict__ wins, const uint32_t* __restrict__ tile_chunk,
-    const SegDev* __restrict__ segs, uint64_t chunk_bytes, uint32_t g0) {
-    const uint32_t g = g0 + blockIdx.x;
+    const SegDev* __restrict__ segs, uint64_t chunk_bytes, uint32_t ntiles) {
+    const uint32_t g = blockIdx.y * gridDim.x + blockIdx.x;
+    if (g >= ntiles) return;
     const TileDev td = tiles[g];
     const TileWin tw = wins[g];
     const uint64_t cbase = reinterpret_cast<uint64_t>(span) + (uint64_t)tile_chunk[g] * chunk_bytes;
@@ -261,23 +263,19 @@ hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const
                                 const uint32_t* tile_chunk, uint64_t ntiles, uint32_t num_chunks,
                                 uint32_t per_chunk, const SegDev* segs, uint64_t chunk_bytes,
                                 uint64_t last_len, uint32_t tile_bytes, hipStream_t stream) {
-    if (ntiles > 0xffffffffull) return hipErrorInvalidConfiguration;
+    if (ntiles == 0) return hipSuccess;
+    if (ntiles > 0x7fffffffull) return hipErrorInvalidConfiguration;
     if (!per_chunk && (!wins || !tile_chunk)) return hipErrorInvalidValue;
-    // a dispatch counts its grid in work-items (32 bits): at most
-    // kMaxGridBlocks workgroups of kBlock per launch
-    for (uint64_t g0 = 0; g0 < ntiles; g0 += kMaxGridBlocks) {
-        const uint32_t n = (uint32_t)std::min<uint64_t>(kMaxGridBlocks, ntiles - g0);
-        if (per_chunk)
-            hipLaunchKernelGGL(scatter_image, dim3(n), dim3(kBlock), 0, stream, span, tiles, segs,
-                               chunk_bytes, last_len, num_chunks, per_chunk, tile_bytes,
-                               (uint32_t)g0);
-        else
-            hipLaunchKernelGGL(scatter_image_gaps, dim3(n), dim3(kBlock), 0, stream, span, tiles,
-                               wins, tile_chunk, segs, chunk_bytes, (uint32_t)g0);
-        const hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
+    uint32_t gx, gy;
+    grid_shape(ntiles, &gx, &gy);
+    if (per_chunk)
+        hipLaunchKernelGGL(scatter_image, dim3(gx, gy), dim3(kBlock), 0, stream, span, tiles, segs,
+                           chunk_bytes, last_len, num_chunks, per_chunk, tile_bytes,
+                           (uint32_t)ntiles);
+    else
+        hipLaunchKernelGGL(scatter_image_gaps, dim3(gx, gy), dim3(kBlock), 0, stream, span, tiles,
+                           wins, tile_chunk, segs, chunk_bytes, (uint32_t)ntiles);
+    return hipGetLastError();
 }
 
 hipError_t launch_zero(const RangeDev* ranges, uint32_t n, hipStream_t stream) {

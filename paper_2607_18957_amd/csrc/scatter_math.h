@@ -27,6 +27,16 @@ constexpr uint32_t kMaxTile = 64u << 10;   // largest tile a workgroup takes
 // work-items, in 32 bits.
 constexpr uint32_t kMaxGridBlocks = 0xffffffffu / kBlock;
 
+// One dispatch over n workgroups (n < 2^32): a dispatch counts each grid
+// dimension in 32-bit work-items, so the grid is gy rows of gx workgroups,
+// gx * kBlock <= 2^32 - 1, and workgroup (x, y) takes index y * gx + x;
+// indices from n up to gx * gy - 1 (fewer than gy of them) have no work.
+II_HD void grid_shape(uint64_t n, uint32_t* gx, uint32_t* gy) {
+    const uint64_t y = n ? (n + kMaxGridBlocks - 1) / kMaxGridBlocks : 1;
+    *gy = (uint32_t)y;
+    *gx = (uint32_t)(n ? (n + y - 1) / y : 1);
+}
+
 struct SegRow {
     uint64_t delta;  // source address minus destination address
     uint64_t dbeg;   // destination range [dbeg, dend)

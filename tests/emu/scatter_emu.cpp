@@ -238,4 +238,19 @@ int emu_scatter(uint64_t num_chunks, uint64_t chunk_bytes, uint64_t lo, uint64_t
     return 0;
 }
 
+// The image launch's grid for n workgroups (grid_shape): no dimension may
+// count more than 2^32 - 1 work-items, the indices y * gx + x must cover
+// [0, n), and fewer than gy of them may lie past it. Returns 0 if so.
+int emu_grid_check(uint64_t n, uint32_t* gx_out, uint32_t* gy_out) {
+    uint32_t gx, gy;
+    grid_shape(n, &gx, &gy);
+    *gx_out = gx;
+    *gy_out = gy;
+    const uint64_t cover = (uint64_t)gx * gy;
+    if ((uint64_t)gx * kBlock > 0xffffffffull || (uint64_t)gy * 1 > 0xffffffffull) return 1;
+    if (cover < n || (n && cover - n >= gy) || gx == 0 || gy == 0) return 1;
+    if (cover - 1 > 0xffffffffull) return 1;  // the kernel forms indices in 32 bits
+    return 0;
+}
+
 }  // extern "C"

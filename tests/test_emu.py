@@ -209,3 +209,20 @@ def test_random_tables(orc):
     for case, t, depth, cs in random_tables.cases(2026, 1000):
         _run(orc, t)
         _run(orc, t, packed=True)
+
+
+def test_image_grid_shape():
+    """The resident-image kernel goes in one dispatch whatever the tile count
+    (the Llama-70B-shaped set has 34.4M tiles, more than 2^32 work-items in
+    one dimension): the grid's rows of workgroups cover every tile once."""
+    import ctypes
+    lib = emu._load()
+    lib.emu_grid_check.argtypes = [ctypes.c_uint64, ctypes.POINTER(ctypes.c_uint32),
+                                   ctypes.POINTER(ctypes.c_uint32)]
+    m = 0xffffffff // 128
+    for n in [0, 1, 2, 127, m - 1, m, m + 1, 2 * m, 2 * m + 1, 34_447_854, 3 * m + 5,
+              (1 << 31) - 1]:
+        gx, gy = ctypes.c_uint32(), ctypes.c_uint32()
+        assert lib.emu_grid_check(n, ctypes.byref(gx), ctypes.byref(gy)) == 0, n
+        assert gy.value == max(1, -(-n // m)), n
+        assert gx.value * 128 <= 0xffffffff and gx.value * gy.value >= n, n
