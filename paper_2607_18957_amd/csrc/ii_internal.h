@@ -39,6 +39,12 @@ struct DmaGroup {
     uint32_t stride;
 };
 
+// A destination range [b, e) of tensor i (the destination checks).
+struct DstRange {
+    uint64_t b, e;
+    size_t i;
+};
+
 struct Runtime;  // device-side state (runtime.hip)
 
 void set_error(const char* fmt, ...);

@@ -38,12 +38,13 @@
 #include <algorithm>
 #include <cerrno>
 #include <cmath>
-#include <memory>
 #include <cstring>
+#include <memory>
 #include <vector>
 
 #include "copy_pool.h"
 #include "ii_internal.h"
+#include "reach.h"
 
 namespace ii {
 
@@ -66,6 +67,62 @@ hipError_t launch_zero(const RangeDev* ranges, uint32_t n, hipStream_t stream);
         }                                                                              \
     } while (0)
 
+// ---------------------------------------------------------------------------
+// Failure injection, for tests of the error contract: with
+// $II_TEST_FAIL_AT = "<site>:<n>" the n-th HIP call of one kind within one
+// entry-point call returns an error instead of being made -- host_alloc
+// (pinned host allocations), dev_alloc (device allocations), h2d
+// (host-to-device copies and uploads), launch (kernel launches). Nothing is
+// enqueued for the failing call, so the device sees no fault; the call then
+// unwinds exactly as after a real runtime error.
+enum InjectSite { kSiteHostAlloc, kSiteDevAlloc, kSiteH2D, kSiteLaunch, kNumSites };
+
+struct Inject {
+    int site = -1;
+    long at = 0, seen = 0;
+};
+static thread_local Inject g_inject;
+
+// Read $II_TEST_FAIL_AT at the entry of a call; counts restart from zero.
+static void inject_arm() {
+    static const char* const names[kNumSites] = {"host_alloc", "dev_alloc", "h2d", "launch"};
+    g_inject = Inject{};
+    const char* s = getenv("II_TEST_FAIL_AT");
+    const char* colon = s ? strchr(s, ':') : nullptr;
+    if (!colon) return;
+    const long n = strtol(colon + 1, nullptr, 10);
+    for (int i = 0; i < kNumSites; ++i)
+        if ((size_t)(colon - s) == strlen(names[i]) && !strncmp(s, names[i], colon - s) && n > 0)
+            g_inject = Inject{i, n, 0};
+}
+
+static bool injected(int site) { return g_inject.site == site && ++g_inject.seen == g_inject.at; }
+
+template <class T>
+static hipError_t dev_alloc(T** p, size_t n) {
+    return injected(kSiteDevAlloc) ? hipErrorOutOfMemory
+                                   : hipMalloc(reinterpret_cast<void**>(p), n);
+}
+template <class T>
+static hipError_t host_alloc(T** p, size_t n) {
+    return injected(kSiteHostAlloc) ? hipErrorOutOfMemory
+                                    : hipHostMalloc(reinterpret_cast<void**>(p), n, 0);
+}
+static hipError_t h2d(void* d, const void* s, size_t n, hipStream_t st) {
+    return injected(kSiteH2D) ? hipErrorUnknown
+                              : hipMemcpyAsync(d, s, n, hipMemcpyHostToDevice, st);
+}
+static hipError_t h2d_2d(void* d, size_t dpitch, const void* s, size_t spitch, size_t w,
+                         size_t h, hipStream_t st) {
+    return injected(kSiteH2D) ? hipErrorUnknown
+                              : hipMemcpy2DAsync(d, dpitch, s, spitch, w, h,
+                                                 hipMemcpyHostToDevice, st);
+}
+static hipError_t h2d_sync(void* d, const void* s, size_t n) {
+    return injected(kSiteH2D) ? hipErrorUnknown : hipMemcpy(d, s, n, hipMemcpyHostToDevice);
+}
+static bool launch_injected() { return injected(kSiteLaunch); }
+
 struct Runtime {
     int device = -1;
     // device tables
@@ -77,11 +134,12 @@ struct Runtime {
     // segment rows with packed staging offsets (plans with packed_distinct)
     SegDev* d_psegs = nullptr;
     SegDev* h_psegs = nullptr;
-    bool tiles_ready = false;
+    bool tiles_ready = false, wins_ready = false, tile_chunk_ready = false;  // uploaded
     hipEvent_t tables_idle = nullptr;   // after the last kernel that read d_segs
     hipEvent_t upload_done = nullptr;   // after the last read of h_segs
     bool tables_used = false, uploaded = false;
     std::vector<uint64_t> cached_dst;   // destination addresses d_segs was built for
+    std::vector<DstRange> cached_ranges;  // ... their ranges, sorted by address
     bool cached_valid = false;
     uint64_t image_b = 0, image_e = 0;  // source image range last checked against them
     // scrub ranges
@@ -195,41 +253,42 @@ static int ensure_tables(ii_plan_t* p) {
     if (r->device != dev)
         return fail(II_EINVAL, "plan was first used on device %d, current device is %d",
                     r->device, dev);
-    if (!r->tables_idle) {
-        II_HIP(hipEventCreateWithFlags(&r->tables_idle, hipEventDisableTiming));
-        II_HIP(hipEventCreateWithFlags(&r->upload_done, hipEventDisableTiming));
-        II_HIP(hipEventCreateWithFlags(&r->ranges_idle, hipEventDisableTiming));
-    }
+    for (hipEvent_t* e : {&r->tables_idle, &r->upload_done, &r->ranges_idle})
+        if (!*e) II_HIP(hipEventCreateWithFlags(e, hipEventDisableTiming));
     if (!r->live_ready) {
         r->live.clear();
         for (size_t k = 0; k < p->num_chunks; ++k)
             if (p->chunk_seg_begin[k] < p->chunk_seg_begin[k + 1]) r->live.push_back((uint32_t)k);
         r->live_ready = true;
     }
+    // Each table is allocated and uploaded separately, and counted as ready
+    // only once its upload returned: a call that failed half-way (one
+    // allocation made, the next refused) leaves nothing a later load would
+    // take for initialised.
     const size_t S = p->seg_len.size();
-    if (S && !r->d_segs) {
-        II_HIP(hipMalloc(&r->d_segs, S * sizeof(SegDev)));
-        II_HIP(hipHostMalloc(&r->h_segs, S * sizeof(SegDev), 0));
+    if (S && !r->d_segs) II_HIP(dev_alloc(&r->d_segs, S * sizeof(SegDev)));
+    if (S && !r->h_segs) II_HIP(host_alloc(&r->h_segs, S * sizeof(SegDev)));
+    if (S && p->packed_distinct) {
+        if (!r->d_psegs) II_HIP(dev_alloc(&r->d_psegs, S * sizeof(SegDev)));
+        if (!r->h_psegs) II_HIP(host_alloc(&r->h_psegs, S * sizeof(SegDev)));
     }
-    if (S && p->packed_distinct && !r->d_psegs) {
-        II_HIP(hipMalloc(&r->d_psegs, S * sizeof(SegDev)));
-        II_HIP(hipHostMalloc(&r->h_psegs, S * sizeof(SegDev), 0));
+    // synchronous, once per plan: the tile tables never change afterwards
+    if (!p->tile_win.empty() && !r->wins_ready) {
+        if (!r->d_wins) II_HIP(dev_alloc(&r->d_wins, p->tile_win.size() * sizeof(TileWin)));
+        II_HIP(h2d_sync(r->d_wins, p->tile_win.data(), p->tile_win.size() * sizeof(TileWin)));
+        r->wins_ready = true;
     }
-    if (!p->tile_win.empty() && !r->d_wins) {
-        II_HIP(hipMalloc(&r->d_wins, p->tile_win.size() * sizeof(TileWin)));
-        II_HIP(hipMemcpy(r->d_wins, p->tile_win.data(), p->tile_win.size() * sizeof(TileWin),
-                         hipMemcpyHostToDevice));
+    if (!p->tile_chunk.empty() && !r->tile_chunk_ready) {
+        if (!r->d_tile_chunk)
+            II_HIP(dev_alloc(&r->d_tile_chunk, p->tile_chunk.size() * sizeof(uint32_t)));
+        II_HIP(h2d_sync(r->d_tile_chunk, p->tile_chunk.data(),
+                        p->tile_chunk.size() * sizeof(uint32_t)));
+        r->tile_chunk_ready = true;
     }
-    if (!p->tile_chunk.empty() && !r->d_tile_chunk) {
-        II_HIP(hipMalloc(&r->d_tile_chunk, p->tile_chunk.size() * sizeof(uint32_t)));
-        II_HIP(hipMemcpy(r->d_tile_chunk, p->tile_chunk.data(),
-                         p->tile_chunk.size() * sizeof(uint32_t), hipMemcpyHostToDevice));
-    }
-    if (!p->tiles.empty() && !r->d_tiles) {
-        II_HIP(hipMalloc(&r->d_tiles, p->tiles.size() * sizeof(TileDev)));
-        // synchronous, once per plan: the tile windows never change afterwards
-        II_HIP(hipMemcpy(r->d_tiles, p->tiles.data(), p->tiles.size() * sizeof(TileDev),
-                         hipMemcpyHostToDevice));
+    if (!p->tiles.empty() && !r->tiles_ready) {
+        if (!r->d_tiles) II_HIP(dev_alloc(&r->d_tiles, p->tiles.size() * sizeof(TileDev)));
+        II_HIP(h2d_sync(r->d_tiles, p->tiles.data(), p->tiles.size() * sizeof(TileDev)));
+        r->tiles_ready = true;
     }
     return II_OK;
 }
@@ -257,8 +316,8 @@ static int ensure_ring(ii_plan_t* p) {
     } while (0)
     const uint64_t C = p->chunk_bytes;
     for (uint32_t i = 0; i < D; ++i) {
-        II_RING(hipHostMalloc(&r->hslot[i], C, 0));
-        II_RING(hipMalloc(&r->dslot[i], C));
+        II_RING(host_alloc(&r->hslot[i], C));
+        II_RING(dev_alloc(&r->dslot[i], C));
         II_RING(hipEventCreateWithFlags(&r->copy_done[i], hipEventDisableTiming));
         II_RING(hipEventCreateWithFlags(&r->scatter_done[i], hipEventDisableTiming));
     }
@@ -290,50 +349,44 @@ static int ensure_trace(Runtime* r, size_t K) {
 // ---------------------------------------------------------------------------
 // argument checks
 
-struct DstRange {
-    uint64_t b, e;
-    size_t i;
-};
-
-// Whether the device can reach [b, e): inside one HIP device (or managed)
-// allocation, whose extent is returned in [*ab, *ae) so that later ranges
-// inside it need no query, or pinned host memory at both ends. Pageable host
-// memory, or memory HIP does not know, is not: a kernel writing or reading
-// there would fault the device.
-static bool accessible(uint64_t b, uint64_t e, uint64_t* ab, uint64_t* ae) {
+// What HIP reports about the allocation holding address x.
+static AllocInfo alloc_info(uint64_t x) {
+    AllocInfo info;
     hipPointerAttribute_t a;
-    if (hipPointerGetAttributes(&a, reinterpret_cast<void*>(b)) != hipSuccess) {
+    if (hipPointerGetAttributes(&a, reinterpret_cast<void*>(x)) != hipSuccess) {
         (void)hipGetLastError();
-        return false;
+        return info;
     }
-    if (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged) {
-        hipDeviceptr_t base = nullptr;
-        size_t size = 0;
-        if (hipMemGetAddressRange(&base, &size, reinterpret_cast<hipDeviceptr_t>(b)) !=
-            hipSuccess) {
-            (void)hipGetLastError();
-            return true;  // device memory whose extent HIP does not report
-        }
-        *ab = reinterpret_cast<uint64_t>(base);
-        *ae = *ab + size;
-        return e <= *ae;
+    if (a.type == hipMemoryTypeDevice || a.type == hipMemoryTypeManaged)
+        info.kind = AllocInfo::kDevice;
+    else if (a.type == hipMemoryTypeHost)
+        info.kind = AllocInfo::kPinnedHost;
+    else
+        return info;
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, reinterpret_cast<hipDeviceptr_t>(x)) != hipSuccess) {
+        (void)hipGetLastError();
+        return info;
     }
-    if (a.type == hipMemoryTypeHost) {
-        hipPointerAttribute_t z;
-        if (hipPointerGetAttributes(&z, reinterpret_cast<void*>(e - 1)) != hipSuccess) {
-            (void)hipGetLastError();
-            return false;
-        }
-        return z.type == hipMemoryTypeHost;
-    }
-    return false;
+    info.extent = true;
+    info.base = reinterpret_cast<uint64_t>(base);
+    info.size = size;
+    return info;
 }
 
-// Check destination addresses: present, aligned, pairwise disjoint and
-// reachable by the device.
-static int check_dst(const ii_plan_t* p, const uint64_t* dst) {
+// Whether the device can reach [b, e): the whole range inside one device
+// allocation or one pinned host allocation (reach.h). A kernel or a DMA
+// touching pageable memory, unknown memory, or a range that runs from one
+// allocation into whatever lies past its end would fault the device.
+static bool accessible(uint64_t b, uint64_t e) { return reachable(alloc_info(b), b, e); }
+
+// Destination ranges of the non-empty tensors, sorted by address, after
+// checking that each is present, aligned and disjoint from the others.
+static int dst_ranges(const ii_plan_t* p, const uint64_t* dst, std::vector<DstRange>* out) {
     const size_t n = p->nbytes.size();
-    std::vector<DstRange> v;
+    std::vector<DstRange>& v = *out;
+    v.clear();
     v.reserve(n);
     for (size_t i = 0; i < n; ++i) {
         if (!p->nbytes[i]) continue;
@@ -351,15 +404,25 @@ static int check_dst(const ii_plan_t* p, const uint64_t* dst) {
         if (v[j].b < v[j - 1].e)
             return fail(II_EOVERLAP, "destinations of tensors %zu and %zu overlap", v[j - 1].i,
                         v[j].i);
-    uint64_t ab = 0, ae = 0;  // the device allocation found last
-    for (const DstRange& d : v) {
-        if (d.b >= ab && d.e <= ae) continue;
-        if (!accessible(d.b, d.e, &ab, &ae))
-            return fail(II_EINVAL, "dst_ptrs[%zu]=%#llx (+%llu bytes) is not memory the device "
-                        "can write: not inside one device allocation or pinned host memory",
-                        d.i, (unsigned long long)d.b, (unsigned long long)(d.e - d.b));
-    }
     return II_OK;
+}
+
+// Every range (sorted by address) reachable by the device: one allocation
+// query per allocation the ranges fall in.
+static int check_reach(const std::vector<DstRange>& v) {
+    const size_t j = first_unreachable(v, alloc_info);
+    if (j == v.size()) return II_OK;
+    return fail(II_EINVAL, "dst_ptrs[%zu]=%#llx (+%llu bytes) is not memory the device can "
+                "write: not inside one device allocation or one pinned host allocation",
+                v[j].i, (unsigned long long)v[j].b, (unsigned long long)(v[j].e - v[j].b));
+}
+
+// Check destination addresses: present, aligned, pairwise disjoint and
+// reachable by the device.
+static int check_dst(const ii_plan_t* p, const uint64_t* dst) {
+    std::vector<DstRange> v;
+    int rc = dst_ranges(p, dst, &v);
+    return rc ? rc : check_reach(v);
 }
 
 // No destination may overlap the source image [b, e) (one linear pass).
@@ -371,8 +434,11 @@ static int check_image(const ii_plan_t* p, const uint64_t* dst, uint64_t b, uint
 }
 
 // Make d_segs hold this load's resolved destination addresses. The upload is
-// ordered on `s`, after every kernel that read the previous table. Checks run
-// only for destinations (and a source image range) not seen before.
+// ordered on `s`, after every kernel that read the previous table. The
+// checks that depend only on the addresses (present, aligned, disjoint) run
+// for destinations not seen before; reachability -- whether the memory is
+// still allocated -- is checked on every call, one query per allocation,
+// since a freed arena may be passed again at the same addresses.
 static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, uint64_t image_b,
                             uint64_t image_e) {
     Runtime* r = p->rt;
@@ -380,17 +446,25 @@ static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, ui
     const bool same = r->cached_valid && r->cached_dst.size() == n &&
                       (n == 0 || memcmp(r->cached_dst.data(), dst, n * sizeof(uint64_t)) == 0);
     if (!same) {
-        int rc = check_dst(p, dst);
-        if (rc) return rc;
+        r->cached_valid = false;
+        try {
+            int rc = dst_ranges(p, dst, &r->cached_ranges);
+            if (rc) return rc;
+        } catch (const std::bad_alloc&) {
+            return fail(II_ENOMEM, "destination check: host allocation failed");
+        }
     }
-    if (image_e > image_b && !(same && r->image_b == image_b && r->image_e == image_e)) {
-        uint64_t ab = 0, ae = 0;
-        if (!accessible(image_b, image_e, &ab, &ae))
+    int rc = check_reach(r->cached_ranges);
+    if (rc) return rc;
+    if (image_e > image_b) {
+        if (!accessible(image_b, image_e))
             return fail(II_EINVAL, "the image's span [%#llx, %#llx) is not memory the device can "
-                        "read: not inside one device allocation or pinned host memory",
+                        "read: not inside one device allocation or one pinned host allocation",
                         (unsigned long long)image_b, (unsigned long long)image_e);
-        int rc = check_image(p, dst, image_b, image_e);
-        if (rc) return rc;
+        if (!(same && r->image_b == image_b && r->image_e == image_e)) {
+            rc = check_image(p, dst, image_b, image_e);
+            if (rc) return rc;
+        }
     }
     if (same) {
         r->image_b = image_b;
@@ -406,10 +480,8 @@ static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, ui
             for (size_t i = 0; i < S; ++i)
                 r->h_psegs[i] = SegDev{p->seg_poff[i], p->seg_len[i], r->h_segs[i].dst};
         if (r->tables_used) II_HIP(hipStreamWaitEvent(s, r->tables_idle, 0));
-        II_HIP(hipMemcpyAsync(r->d_segs, r->h_segs, S * sizeof(SegDev), hipMemcpyHostToDevice, s));
-        if (p->packed_distinct)
-            II_HIP(hipMemcpyAsync(r->d_psegs, r->h_psegs, S * sizeof(SegDev),
-                                  hipMemcpyHostToDevice, s));
+        II_HIP(h2d(r->d_segs, r->h_segs, S * sizeof(SegDev), s));
+        if (p->packed_distinct) II_HIP(h2d(r->d_psegs, r->h_psegs, S * sizeof(SegDev), s));
         II_HIP(hipEventRecord(r->upload_done, s));
         r->uploaded = true;
     }
@@ -432,36 +504,30 @@ static int launch_scrub(ii_plan_t* p, const std::vector<RangeDev>& ranges, hipSt
         r->d_ranges = nullptr;
         r->h_ranges = nullptr;
         r->ranges_cap = 0;
-        II_HIP(hipMalloc(&r->d_ranges, ranges.size() * sizeof(RangeDev)));
-        II_HIP(hipHostMalloc(&r->h_ranges, ranges.size() * sizeof(RangeDev), 0));
+        II_HIP(dev_alloc(&r->d_ranges, ranges.size() * sizeof(RangeDev)));
+        II_HIP(host_alloc(&r->h_ranges, ranges.size() * sizeof(RangeDev)));
         r->ranges_cap = ranges.size();
     }
     memcpy(r->h_ranges, ranges.data(), ranges.size() * sizeof(RangeDev));
-    II_HIP(hipMemcpyAsync(r->d_ranges, r->h_ranges, ranges.size() * sizeof(RangeDev),
-                          hipMemcpyHostToDevice, s));
-    II_HIP(launch_zero(r->d_ranges, (uint32_t)ranges.size(), s));
+    II_HIP(h2d(r->d_ranges, r->h_ranges, ranges.size() * sizeof(RangeDev), s));
+    II_HIP(launch_injected() ? hipErrorLaunchFailure
+                             : launch_zero(r->d_ranges, (uint32_t)ranges.size(), s));
     II_HIP(hipEventRecord(r->ranges_idle, s));
     r->ranges_used = true;
     return II_OK;
 }
 
-static bool is_pinned_host(const void* ptr) {
-    hipPointerAttribute_t a;
-    hipError_t e = hipPointerGetAttributes(&a, ptr);
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return false;
-    }
-    return a.type == hipMemoryTypeHost;
-}
-
-// Whether the blob bytes a load reads, [blob + lo, blob + hi), are pinned
-// host memory at both ends, so that copies may read them by DMA. A blob
-// pinned only in part (or whose declared size reaches past its pinned
-// allocation) is treated as pageable: the host stage copies it, and no DMA
-// reads outside pinned memory.
+// Whether the blob bytes a load reads, [blob + lo, blob + hi), lie inside one
+// pinned host allocation, so that copies may read them by DMA. A blob pinned
+// only in part (or whose span reaches past its pinned allocation) is treated
+// as pageable: the host stage copies it, and no DMA reads outside pinned
+// memory.
 static bool pinned_span(const ii_plan_t* p, const uint8_t* blob) {
-    return p->hi > p->lo && is_pinned_host(blob + p->lo) && is_pinned_host(blob + p->hi - 1);
+    if (p->hi <= p->lo) return false;
+    const uint64_t b = reinterpret_cast<uint64_t>(blob) + p->lo;
+    const uint64_t e = reinterpret_cast<uint64_t>(blob) + p->hi;
+    const AllocInfo a = alloc_info(b);
+    return a.kind == AllocInfo::kPinnedHost && reachable(a, b, e);
 }
 
 static bool is_device_ptr(const void* ptr) {
@@ -631,13 +697,12 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
                 uint8_t* to = r->dslot[slot] + g.poff;
                 const uint8_t* at = blob + cbeg + g.off;
                 if (g.count == 1)
-                    II_HIP(hipMemcpyAsync(to, at, g.len, hipMemcpyHostToDevice, cs));
+                    II_HIP(h2d(to, at, g.len, cs));
                 else
-                    II_HIP(hipMemcpy2DAsync(to, g.len, at, g.stride, g.len, g.count,
-                                            hipMemcpyHostToDevice, cs));
+                    II_HIP(h2d_2d(to, g.len, at, g.stride, g.len, g.count, cs));
             }
         } else {
-            II_HIP(hipMemcpyAsync(r->dslot[slot] + doff, from, len, hipMemcpyHostToDevice, cs));
+            II_HIP(h2d(r->dslot[slot] + doff, from, len, cs));
         }
         II_HIP(hipEventRecord(r->copy_done[slot], cs));
         if (trace) II_HIP(hipEventRecord(r->tr_ce[j], cs));
@@ -649,7 +714,8 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         // windows are implicit in a packed slot and in a plan without gaps
         // (which keeps no window table)
         const bool implicit = packed || !p->packed_distinct;
-        II_HIP(launch_scatter_slot(r->dslot[slot], r->d_tiles + t0,
+        II_HIP(launch_injected() ? hipErrorLaunchFailure
+                                 : launch_scatter_slot(r->dslot[slot], r->d_tiles + t0,
                                    implicit ? nullptr : r->d_wins + t0, (uint32_t)nt,
                                    packed ? r->d_psegs : r->d_segs, implicit, p->tile_bytes,
                                    p->chunk_plen[k], r->scatter_s));
@@ -676,7 +742,8 @@ static int run_device(ii_plan_t* p, const uint8_t* image, const uint64_t* dst, h
     rc = prepare_segments(p, dst, stream, ib + p->lo, ib + p->hi);
     if (rc) return rc;
     const uint64_t last_len = p->num_chunks ? p->chunk_len(p->num_chunks - 1) : 0;
-    II_HIP(launch_scatter_image(image + p->lo, r->d_tiles, r->d_wins, r->d_tile_chunk,
+    II_HIP(launch_injected() ? hipErrorLaunchFailure
+                             : launch_scatter_image(image + p->lo, r->d_tiles, r->d_wins, r->d_tile_chunk,
                                 p->tiles.size(), (uint32_t)p->num_chunks, p->tiles_per_chunk,
                                 r->d_segs, p->chunk_bytes, last_len, p->tile_bytes, stream));
     II_HIP(hipEventRecord(r->tables_idle, stream));
@@ -728,11 +795,10 @@ static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
         const uint64_t rb = n / p->rows[i], stride = p->row_stride[i];
         if (pinned) {
             if (p->rows[i] > 1)
-                II_HIP(hipMemcpy2DAsync(reinterpret_cast<void*>(dst[i]), rb, src, stride, rb,
-                                        p->rows[i], hipMemcpyHostToDevice, cs));
+                II_HIP(h2d_2d(reinterpret_cast<void*>(dst[i]), rb, src, stride, rb, p->rows[i],
+                              cs));
             else
-                II_HIP(hipMemcpyAsync(reinterpret_cast<void*>(dst[i]), src, n,
-                                      hipMemcpyHostToDevice, cs));
+                II_HIP(h2d(reinterpret_cast<void*>(dst[i]), src, n, cs));
             continue;
         }
         for (uint64_t x = 0; x < n;) {
@@ -748,8 +814,7 @@ static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
                 r->pool->copy(stage + (y - x), src + q * stride + c, m);
                 y += m;
             }
-            II_HIP(hipMemcpyAsync(reinterpret_cast<void*>(dst[i] + x), stage, len,
-                                  hipMemcpyHostToDevice, cs));
+            II_HIP(h2d(reinterpret_cast<void*>(dst[i] + x), stage, len, cs));
             used += len;
             x += len;
         }
@@ -780,6 +845,7 @@ extern "C" int ii_load_pertensor(ii_plan_t* p, const void* host_blob, uint64_t b
         return fail(II_EINVAL, "ii_load_pertensor: host_blob is device memory");
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_load_pertensor: plan in use");
+    inject_arm();
     int rc = run_pertensor(p, static_cast<const uint8_t*>(host_blob),
                            reinterpret_cast<const uint64_t*>(dst_ptrs), stream);
     return rc ? drain(p, stream, rc) : II_OK;
@@ -798,6 +864,7 @@ extern "C" int ii_load(ii_plan_t* p, const void* host_blob, uint64_t blob_bytes,
         return fail(II_EINVAL, "ii_load: host_blob is device memory (use ii_load_device)");
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_load: plan in use");
+    inject_arm();
     Source src;
     src.blob = static_cast<const uint8_t*>(host_blob);
     int rc = run_ring(p, src, reinterpret_cast<const uint64_t*>(dst_ptrs), stream, nullptr);
@@ -822,6 +889,7 @@ extern "C" int ii_load_file(ii_plan_t* p, int fd, uint64_t file_bytes, void* con
     }
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_load_file: plan in use");
+    inject_arm();
     int rc = run_ring(p, src, reinterpret_cast<const uint64_t*>(dst_ptrs), stream, nullptr);
     return rc ? drain(p, stream, rc) : II_OK;
 }
@@ -837,6 +905,7 @@ extern "C" int ii_load_device(ii_plan_t* p, const void* dev_image, uint64_t imag
                     (unsigned long long)image_bytes, (unsigned long long)p->hi);
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_load_device: plan in use");
+    inject_arm();
     int rc = run_device(p, static_cast<const uint8_t*>(dev_image),
                         reinterpret_cast<const uint64_t*>(dst_ptrs), stream);
     return rc ? drain(p, stream, rc) : II_OK;
@@ -889,10 +958,10 @@ extern "C" int ii_switch(const ii_plan_t* po, ii_plan_t* pn, void* arena, uint64
                     (unsigned long long)pn->max_align);
     // the scrub writes anywhere in the old layout, so the whole arena the
     // caller declares must be memory the device can write
-    uint64_t arena_end, ab = 0, ae = 0;
+    uint64_t arena_end;
     if (__builtin_add_overflow(a, arena_bytes, &arena_end))
         return fail(II_EOVERFLOW, "ii_switch: arena + arena_bytes overflows");
-    if (arena_bytes && !accessible(a, arena_end, &ab, &ae))
+    if (arena_bytes && !accessible(a, arena_end))
         return fail(II_EINVAL, "ii_switch: the arena [%#llx, +%llu bytes) is not memory the "
                     "device can write: not inside one device allocation or pinned host memory",
                     (unsigned long long)a, (unsigned long long)arena_bytes);
@@ -904,6 +973,7 @@ extern "C" int ii_switch(const ii_plan_t* po, ii_plan_t* pn, void* arena, uint64
         return fail(II_EINVAL, "ii_switch: host blob is device memory");
     BusyGuard g(pn);
     if (!g.ok) return fail(II_EBUSY, "ii_switch: plan in use");
+    inject_arm();
     std::vector<uint64_t> dst(pn->nbytes.size());
     for (size_t i = 0; i < dst.size(); ++i) dst[i] = a + pn->dst_offset[i];
     std::vector<RangeDev> scrub = scrub_ranges(po, pn, a);
@@ -972,6 +1042,7 @@ extern "C" int ii_plan_prepare(ii_plan_t* p) {
     if (!p) return fail(II_EINVAL, "ii_plan_prepare: plan is NULL");
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_plan_prepare: plan in use");
+    inject_arm();
     int rc = ensure_tables(p);
     if (rc) return rc;
     return ensure_ring(p);

@@ -1,5 +1,6 @@
-"""Host-only sanitizer builds of the planner (ASan + UBSan) and the host
-copy pool (TSan). Built with g++ from the library's own sources."""
+"""Host-only sanitizer builds of the planner (ASan + UBSan), the host copy
+pool (TSan) and the reachability decision of the loads (ASan + UBSan, against
+a fake memory map). Built with g++ from the library's own sources."""
 from __future__ import annotations
 
 import os
@@ -11,6 +12,7 @@ CSRC = os.path.join(ROOT, "paper_2607_18957_amd", "csrc")
 INC = os.path.join(ROOT, "include")
 PLAN_BIN = os.path.join(HERE, "plan_fuzz")
 POOL_BIN = os.path.join(HERE, "pool_tsan")
+REACH_BIN = os.path.join(HERE, "reach_check")
 
 
 def build() -> None:
@@ -20,3 +22,5 @@ def build() -> None:
                                     os.path.join(CSRC, "plan.cpp")])
     subprocess.check_call(common + ["-fsanitize=thread", "-pthread", "-o", POOL_BIN,
                                     os.path.join(HERE, "pool_tsan.cpp")])
+    subprocess.check_call(common + ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                                    "-o", REACH_BIN, os.path.join(HERE, "reach_check.cpp")])

@@ -9,6 +9,7 @@ the Mistral-7B-shaped set runs whole.
 """
 import os
 import sys
+import time
 
 import numpy as np
 import pytest
@@ -123,67 +124,92 @@ def _load_arena(orc, table, *, mode="pageable", depth=None, threads=None, blob=N
     return plan
 
 
+def _compare_tensors_streamed(orc, label, buf, base_off, table, nb, off, blob):
+    """Every tensor of `table` read back from HBM (buf is the device buffer,
+    tensor i at byte base_off + off[i]) and compared byte for byte with the
+    oracle's copy of that tensor, one tensor at a time: a reused pinned
+    host buffer for the readback and a reused buffer for the oracle, so a
+    set too large to hold twice in host memory is still compared whole."""
+    big = int(nb.max())
+    host = torch.empty(big, dtype=torch.uint8, pin_memory=True)
+    hview = host.numpy()
+    want = np.empty(big, np.uint8)
+    nbo = orc.nbytes(table)
+    total = 0
+    for i in range(table.n):
+        n = int(nb[i])
+        if not n:
+            continue
+        d = base_off + int(off[i])
+        host[:n].copy_(buf[d:d + n])
+        orc.load_into(nbo[i:i + 1], table.src_offset[i:i + 1], blob, [want])
+        a, b = hview[:n], want[:n]
+        if n % 8 == 0:
+            a, b = a.view(np.uint64), b.view(np.uint64)
+        if not np.array_equal(a, b):
+            bad = np.flatnonzero(hview[:n] != want[:n])
+            raise AssertionError(f"{label}: tensor {i} ({table.names[i]}): {bad.size} bytes "
+                                 f"differ, first at {int(bad[0])}")
+        total += n
+        if (i + 1) % 100 == 0:
+            _say(f"{label}: {i + 1}/{table.n} tensors compared ({total} bytes)")
+    del host
+    return total
+
+
 @pytest.mark.slow
-@pytest.mark.timeout(900)
-def test_llama70b_full_sampled(orc):
+@pytest.mark.timeout(1200)
+def test_llama70b_full(orc):
     """The Llama-70B-shaped set at full size: 141 GB blob, 256 MiB chunks,
-    141 GB of destinations in HBM. The blob is pageable host memory staged
-    through the pinned ring (a single 141 GB pinned allocation exceeds what
-    the host lets one process pin). The oracle cannot hold a second copy, so
-    it runs on a sub-table (24 whole tensors, every kind and both ends of the
-    file) and every other tensor is checked in random 4 KiB windows plus its
-    first and last bytes. Both the ring path from the pageable blob and the
-    resident-image path (141 GB image and 141 GB arena in HBM at once)."""
+    141 GB of destinations in HBM between 4 KiB guard bands. The blob is
+    pageable host memory staged through the pinned ring (a single 141 GB
+    pinned allocation exceeds what the host lets one process pin). Both the
+    ring path from the pageable blob and the resident-image path (141 GB
+    image and 141 GB arena in HBM at once; 34.4M tiles, more work-items than
+    one grid dimension counts, in one dispatch) are compared with the oracle
+    on every byte of every tensor, one tensor at a time, and the guard bands
+    are checked. The layout has no padding (every size is a multiple of 256),
+    so the tensors cover the arena."""
     import time
     t = synth.llama70b()
     plan = ii.ii_plan(t)
     nb, off = plan.tensors()
-    assert plan.payload_bytes == 141_107_412_992 and plan.num_chunks == 526
+    assert plan.payload_bytes == plan.arena_bytes == 141_107_412_992 and plan.num_chunks == 526
     _say("llama70b: blob")
     blob = np.empty(t.blob_bytes, np.uint8)
     synth.fill(blob.ctypes.data, 0, t.blob_bytes, t.seed, threads=16)
-    arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=DEV)
-    _say("llama70b: load")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ii.ii_load(plan, blob, arena.data_ptr() + off)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    _say(f"llama70b: {plan.payload_bytes / dt / 1e9:.1f} GB/s end to end (pageable, first load)")
-    rng = np.random.default_rng(70)
-    whole = sorted(set([0, 1, 2, 3, 4, 5, 6, 7, 8, 9, t.n - 3, t.n - 2, t.n - 1] +
-                       list(rng.choice(t.n, size=11, replace=False))))
-    outs = orc.load(orc.nbytes(t)[whole], t.src_offset[whole], blob)
+    buf = torch.empty(plan.arena_bytes + 2 * GUARD, dtype=torch.uint8, device=DEV)
+    guard = torch.from_numpy(synth.canary(GUARD, seed=70)).to(DEV)
 
-    def check(label):
-        for i, o in zip(whole, outs):
-            got = arena[int(off[i]):int(off[i]) + o.size].cpu().numpy()
-            assert np.array_equal(got, o), f"{label}: tensor {i} ({t.names[i]})"
-        for i in range(t.n):
-            n, s, d = int(nb[i]), int(t.src_offset[i]), int(off[i])
-            for j in [0, max(0, n - 4096)] + [int(x) for x in rng.integers(0, max(1, n - 4096), 2)]:
-                m = min(4096, n - j)
-                got = arena[d + j:d + j + m].cpu().numpy()
-                assert np.array_equal(got, blob[s + j:s + j + m]), (label, i, j)
-    check("pageable")
-    _say(f"llama70b: {len(whole)} whole tensors and {t.n} sampled tensors bit-exact (pageable)")
-    # the resident-image path: 34.4M tiles of 128 threads, more work-items
-    # than one dispatch can count (2^32), so the kernel goes in two launches
-    tb = plan.tiles()
-    assert len(tb["first"]) * 128 > 0xffffffff
-    arena.fill_(0x5A)
-    _say("llama70b: image")
-    image = torch.from_numpy(blob).to(DEV)
-    ii.ii_load_device(plan, image, arena.data_ptr() + off)
-    torch.cuda.synchronize()
-    del image
-    check("image")
-    # the last tensor's last bytes are written by the last launch
-    i = t.n - 1
-    n, s, d = int(nb[i]), int(t.src_offset[i]), int(off[i])
-    assert np.array_equal(arena[d + n - 65536:d + n].cpu().numpy(), blob[s + n - 65536:s + n])
-    _say(f"llama70b: {len(whole)} whole tensors and {t.n} sampled tensors bit-exact (image)")
-    del arena
+    def guards_intact(label):
+        head, tail = buf[:GUARD], buf[GUARD + plan.arena_bytes:]
+        assert torch.equal(head, guard) and torch.equal(tail, guard), f"{label}: guard band"
+
+    for mode in ("pageable", "image"):
+        buf[:GUARD].copy_(guard)
+        buf[GUARD + plan.arena_bytes:].copy_(guard)
+        buf[GUARD:GUARD + plan.arena_bytes].fill_(0x5A if mode == "image" else 0xA5)
+        torch.cuda.synchronize()
+        _say(f"llama70b: {mode} load")
+        t0 = time.perf_counter()
+        if mode == "pageable":
+            ii.ii_load(plan, blob, buf.data_ptr() + GUARD + off)
+        else:
+            image = torch.from_numpy(blob).to(DEV)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            ii.ii_load_device(plan, image, buf.data_ptr() + GUARD + off)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        if mode == "image":
+            del image
+            torch.cuda.empty_cache()
+        _say(f"llama70b: {mode} {plan.payload_bytes / dt / 1e9:.1f} GB/s; comparing every tensor")
+        guards_intact(mode)
+        n = _compare_tensors_streamed(orc, mode, buf, GUARD, t, nb, off, blob)
+        assert n == plan.payload_bytes
+        _say(f"llama70b: {mode}: all {t.n} tensors ({n} bytes) bit-exact")
+    del buf
 
 
 @pytest.mark.slow
@@ -954,3 +980,248 @@ def test_random_tables_every_mode(orc):
             plan.set_ring(depth, 2, cs)
             _load_arena(orc, t, mode=mode, blob=t.blob, plan=plan)
             plan.free()
+
+
+# -- the switch dependency of Sec. 4.3 under pending work ---------------------
+
+def _busy(n):
+    """n 4096 x 4096 float32 products on the current stream: unrelated
+    device work of bounded length, standing in for the old model still
+    running on the stream."""
+    a = torch.ones(4096, 4096, dtype=torch.float32, device=DEV) / 4096.0
+    for _ in range(n):
+        a = a @ a
+    return a
+
+
+def test_switch_waits_for_pending_work(orc):
+    """(M1, GMemFreed) -> (M2, EnvReady): with the old model's work still
+    pending on the stream -- a run of matrix products, then a copy of the
+    arena into a snapshot -- ii_switch on the same stream stages the new
+    model and copies its first chunks into the ring at once, but writes the
+    arena (scrub and scatters) only after that work: the snapshot holds the
+    old arena exactly, the final arena is the oracle's switch, and the
+    trace shows the first ring-depth chunks copied long before the first
+    scatter. Also reports how much of the pending work the switch overlaps."""
+    import time
+    old = synth.tiny(chunk=1 << 20)
+    new = synth.transformer("tiny-b", 4, 256, 1024, 256, 4096, seed=21, chunk=1 << 20)
+    po, pn = ii.ii_plan(old), ii.ii_plan(new)
+    depth = 3
+    pn.set_ring(depth, 4, 2)
+    pn.prepare()
+    blob_o, blob_n = synth.blob(old), synth.blob(new)
+    size = po.arena_bytes
+    buf, can = _canary_buffer(size + 2 * GUARD)
+    base = buf.data_ptr() + GUARD
+    s = torch.cuda.current_stream(DEV)
+    loaded = can.copy()
+    orc.arena(orc.nbytes(old), old.src_offset, old.dst_align, blob_o,
+              loaded[GUARD:GUARD + size])
+    final = loaded.copy()
+    orc.switch(orc.nbytes(old), old.dst_align, orc.nbytes(new), new.src_offset, new.dst_align,
+               blob_n, final[GUARD:GUARD + size])
+
+    def reload():
+        ii.ii_load(po, blob_o, base + po.tensors()[1], s)
+        s.synchronize()
+
+    # timings: pending work alone, switch alone, both
+    reload()
+    ii.ii_switch(po, pn, base, size, blob_n, s)   # warm: tables uploaded
+    s.synchronize()
+    reps = 24
+    _busy(2)
+    s.synchronize()
+    t0 = time.perf_counter()
+    _busy(reps)
+    s.synchronize()
+    t_busy = time.perf_counter() - t0
+    reload()
+    t0 = time.perf_counter()
+    ii.ii_switch(po, pn, base, size, blob_n, s)
+    s.synchronize()
+    t_switch = time.perf_counter() - t0
+
+    reload()
+    snap = torch.empty_like(buf)
+    pn.set_trace(True)
+    s.synchronize()
+    t0 = time.perf_counter()
+    _busy(reps)
+    snap.copy_(buf)
+    ii.ii_switch(po, pn, base, size, blob_n, s)
+    s.synchronize()
+    t_both = time.perf_counter() - t0
+    tr = pn.trace()
+    pn.set_trace(False)
+    assert np.array_equal(snap.cpu().numpy(), loaded), "a write reached the arena before the " \
+        "work enqueued ahead of the switch had finished"
+    assert np.array_equal(buf.cpu().numpy(), final)
+    cs, ce, ss = tr["copy_start"], tr["copy_end"], tr["scatter_start"]
+    K = pn.num_chunks
+    _say(f"switch under pending work: busy {t_busy * 1e3:.1f} ms, switch {t_switch * 1e3:.2f} ms, "
+         f"both {t_both * 1e3:.1f} ms, overlap {(t_busy + t_switch - t_both) * 1e3:.2f} ms; "
+         f"first {depth} copies end {ce[depth - 1]:.2f} ms, first scatter starts {ss[0]:.2f} ms "
+         f"(times from the end of the pending work), K={K}")
+    # the first `depth` chunks were copied while the old work ran: their
+    # copies ended well before the first arena write, which itself waited
+    # for that work (the busy run is tens of milliseconds)
+    assert K > depth
+    assert (ce[:depth] < ss[0] - 0.25 * t_busy * 1e3).all()
+    # no later chunk's copy can start before the scatter that frees its slot
+    assert (cs[depth:] >= ss[:K - depth] - 1e-3).all()
+
+
+# -- the error contract, with failures injected into HIP calls ----------------
+
+_INJECT_CASES = [
+    ("host_alloc", 1, "pageable"), ("host_alloc", 3, "pageable"),
+    ("dev_alloc", 1, "pageable"), ("dev_alloc", 4, "pageable"),
+    ("h2d", 1, "pageable"), ("h2d", 8, "pageable"), ("h2d", 8, "pinned"),
+    ("launch", 1, "pageable"), ("launch", 9, "pageable"), ("launch", 5, "pinned"),
+    ("h2d", 1, "image"), ("launch", 1, "image"),
+    ("launch", 1, "switch"), ("launch", 4, "switch"), ("h2d", 6, "switch"),
+    ("h2d", 3, "pertensor"),
+]
+
+
+@pytest.mark.parametrize("site,nth,mode", _INJECT_CASES,
+                         ids=[f"{m}-{s}{n}" for s, n, m in _INJECT_CASES])
+def test_injected_failure(orc, monkeypatch, site, nth, mode):
+    """A HIP call made to fail part-way through a load (allocations on a
+    fresh plan, a chunk copy or a scatter launch in the middle of the ring,
+    the scrub of a switch): the call returns II_ENOMEM or II_EHIP, nothing
+    touches the destination after it returned, the guard bands are intact,
+    and the next call on the same plan is bit-exact."""
+    t = synth.tiny(chunk=1 << 20)                  # 17 chunks
+    plan = ii.ii_plan(t)
+    plan.set_ring(3, 2, 2)
+    _, off = plan.tensors()
+    blob = synth.blob(t)
+    buf, can = _canary_buffer(plan.arena_bytes + 2 * GUARD)
+    base = buf.data_ptr() + GUARD
+    s = torch.cuda.current_stream(DEV)
+    pinned = None
+    if mode == "pinned":
+        pinned = ii.ii_host_alloc(blob.size)
+        pinned.numpy()[:] = blob
+    image = torch.from_numpy(blob).to(DEV) if mode == "image" else None
+    old = synth.transformer("tiny-old", 4, 256, 1024, 256, 8192, seed=31, chunk=1 << 20)
+    po = ii.ii_plan(old)
+    blob_old = synth.blob(old)
+
+    def call():
+        if mode == "pageable":
+            ii.ii_load(plan, blob, base + off, s)
+        elif mode == "pinned":
+            ii.ii_load(plan, pinned, base + off, s)
+        elif mode == "image":
+            ii.ii_load_device(plan, image, base + off, s)
+        elif mode == "pertensor":
+            ii.ii_load_pertensor(plan, blob, base + off, s)
+        elif mode == "switch":
+            ii.ii_switch(po, plan, base, plan.arena_bytes, blob, s)
+
+    if mode == "switch":
+        ii.ii_load(po, blob_old, base + po.tensors()[1], s)
+        s.synchronize()
+        start = buf.cpu().numpy()
+        want = start.copy()
+        orc.switch(orc.nbytes(old), old.dst_align, orc.nbytes(t), t.src_offset, t.dst_align,
+                   blob, want[GUARD:GUARD + plan.arena_bytes])
+    else:
+        want = can.copy()
+        orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob,
+                  want[GUARD:GUARD + plan.arena_bytes])
+    monkeypatch.setenv("II_TEST_FAIL_AT", f"{site}:{nth}")
+    with pytest.raises(ii.IIError) as e:
+        call()
+    monkeypatch.delenv("II_TEST_FAIL_AT")
+    assert e.value.name == ("II_ENOMEM" if site.endswith("alloc") else "II_EHIP"), e.value
+    snap = buf.cpu().numpy()
+    time.sleep(0.05)
+    torch.cuda.synchronize()
+    assert np.array_equal(buf.cpu().numpy(), snap), "destination written after the error"
+    assert np.array_equal(snap[:GUARD], can[:GUARD])
+    assert np.array_equal(snap[GUARD + plan.arena_bytes:], can[GUARD + plan.arena_bytes:])
+    call()
+    s.synchronize()
+    got = buf.cpu().numpy()
+    if not np.array_equal(got, want):
+        bad = np.flatnonzero(got != want)
+        raise AssertionError(f"after the injected failure: {bad.size} bytes differ, first at "
+                             f"{int(bad[0]) - GUARD}")
+    _say(f"{mode}: {site} #{nth} failed with {e.value.name}; next call bit-exact")
+    if pinned is not None:
+        pinned.free()
+
+
+# -- reachability of destinations ----------------------------------------------
+
+def test_range_across_two_pinned_allocations_refused():
+    """A destination that starts in one pinned host allocation and ends in
+    another (whatever lies between them) is refused before anything is
+    enqueued; a destination inside one of them is accepted."""
+    bufs = [ii.ii_host_alloc(2 << 20) for _ in range(8)]
+    addrs = sorted((b.ptr, b) for b in bufs)
+    gaps = [(addrs[i + 1][0] - addrs[i][0], i) for i in range(len(addrs) - 1)]
+    dist, i = min(gaps)
+    a, b = addrs[i][1], addrs[i + 1][1]
+    if dist > (1 << 30):
+        pytest.skip(f"pinned allocations {dist} bytes apart")
+    span = b.ptr + b.nbytes - a.ptr
+    t = oracle_pins._u8_table([span], [0], [1])
+    plan = ii.ii_plan(t, 1 << 20)
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_check_dst(plan, [a.ptr])
+    assert e.value.name == "II_EINVAL"
+    _say(f"refused a {span}-byte range across two pinned allocations {dist} bytes apart")
+    inside = ii.ii_plan(oracle_pins._u8_table([a.nbytes], [0], [1]), 1 << 20)
+    ii.ii_check_dst(inside, [a.ptr])
+    # a range that runs one byte past the end of one allocation
+    past = ii.ii_plan(oracle_pins._u8_table([a.nbytes + 1], [0], [1]), 1 << 20)
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_check_dst(past, [a.ptr])
+    assert e.value.name == "II_EINVAL"
+    for x in bufs:
+        x.free()
+
+
+def test_freed_destination_refused_on_repeat(orc):
+    """A load that repeats the previous load's destination pointers still
+    checks that the memory is allocated: after the arena is freed, the same
+    addresses are refused (II_EINVAL) instead of being written, and the
+    plan stays usable."""
+    import ctypes
+    t = synth.tiny()
+    plan = ii.ii_plan(t)
+    _, off = plan.tensors()
+    blob = synth.blob(t)
+    # memory of our own from the process's HIP runtime (PyTorch's caching
+    # allocator would keep freed memory mapped)
+    hip = ctypes.CDLL("libamdhip64.so.7")
+    hip.hipMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t]
+    hip.hipFree.argtypes = [ctypes.c_void_p]
+    ptr = ctypes.c_void_p()
+    assert hip.hipMalloc(ctypes.byref(ptr), plan.arena_bytes) == 0
+    dst = ptr.value + off
+    ii.ii_load(plan, blob, dst)
+    torch.cuda.synchronize()
+    assert hip.hipFree(ptr) == 0
+    try:
+        ii.ii_check_dst(plan, dst)
+    except ii.IIError as e:
+        assert e.name == "II_EINVAL"
+    else:  # the runtime still reports the range as allocated: nothing to test
+        pytest.skip("the HIP runtime still reports freed memory as allocated")
+    with pytest.raises(ii.IIError) as e:
+        ii.ii_load(plan, blob, dst)              # same pointers as the last load
+    assert e.value.name == "II_EINVAL"
+    arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=DEV)
+    ii.ii_load(plan, blob, arena.data_ptr() + off)
+    torch.cuda.synchronize()
+    got = arena.cpu().numpy()
+    want = got.copy()
+    orc.arena(orc.nbytes(t), t.src_offset, t.dst_align, blob, want)
+    assert np.array_equal(got, want)

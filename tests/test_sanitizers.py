@@ -39,3 +39,14 @@ def test_copy_pool_tsan():
                        env=env)
     assert r.returncode == 0, r.stdout + r.stderr
     assert r.stdout.strip() == "OK"
+
+
+def test_reachability_decision():
+    """reach.h on a fake memory map: a range is reachable only inside one
+    device or pinned host allocation (not across two adjacent ones, not over
+    a pageable hole, not one byte past the end), ranges packed in one arena
+    cost one allocation query, and a later range that leaves the allocation
+    found last is still caught."""
+    r = subprocess.run([_bin(sanitize.REACH_BIN)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.strip() == "OK"
