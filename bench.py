@@ -1,27 +1,32 @@
 #!/usr/bin/env python3
 """Benchmark of merged tensor loading on one MI355X.
 
-Workload: the Llama-8B-shaped weight set (32 layers, hidden 4096, FFN 14336,
-8 KV heads x 128, vocab 128256; 291 bf16 tensors, 16,060,522,496 bytes of
-seeded random bits), planned into 64 MiB chunks, loaded into one device arena
-laid out by the plan.
+Workload (default): the Llama-70B-shaped weight set -- 80 layers, hidden
+8192, FFN 28672, 8 KV heads x 128, vocab 128256; 723 bf16 tensors,
+141,107,412,992 bytes of seeded random bits -- planned into 256 MiB chunks
+and loaded into one device arena laid out by the plan. The blob is pageable
+host memory (one process cannot pin 141 GB on the host).
 
-One step = one full materialisation of every tensor through the C-ABI, with
-the blob image already resident in HBM when the timed region starts:
-ii_load_device scatters all 240 chunks into the 291 destinations in one
-kernel launch. value = payload bytes / step time (GB = 1e9 B).
+One step = one full load of every tensor through the C-ABI (ii_load): host
+threads stage each chunk into a 3-slot pinned ring, one hipMemcpyAsync per
+chunk carries it to a device slot, and the scatter kernel writes it into its
+tensors while the next chunk is in flight. value = payload bytes x steps /
+wall time of the steps (GB = 1e9 B), the loads enqueued back to back and
+bracketed by device synchronisation; tensors/s beside it; both also as a
+fraction of the measured host-to-device copy peak.
 
-Reported beside it, never as value:
-  e2e           host blob -> tensors through ii_load (pinned staging ring, bulk
-                hipMemcpyAsync, per-chunk scatter), pageable and pinned blobs,
-                as a fraction of the measured host-to-device copy peak;
-  roofline      the scatter kernel's algorithmic HBM bytes per launch over its
-                mean launch time (HIP events on the launch stream), against
-                the 8 TB/s HBM peak; traffic from rocprofv3 counters when a
-                profile of the current kernel source is on record;
-  cpu_baseline  the CPU oracle (one core) on the same table.
-With --compare-per-tensor it also times the naive per-tensor pipeline
-(ii_load_pertensor) against the merged loader on the 8B and stress sets.
+Reported beside it:
+  roofline      the scatter kernel alone: the same table scattered from a
+                blob image already resident in HBM (ii_load_device, one
+                dispatch), its algorithmic HBM bytes per launch over its mean
+                launch time (HIP events on the launch stream) against the
+                8 TB/s HBM peak; traffic from rocprofv3 counters when a profile
+                of the current kernel source is on record; and the ring's own
+                per-chunk scatter (scatter_slot) from the timestamps of one
+                traced load;
+  cpu_baseline  the CPU oracle on one core, on a bounded sample of the table.
+--workload picks another set (tiny, stress, llama8b, mistral7b) for
+profiling; --configs measures every set in one process instead.
 """
 from __future__ import annotations
 
@@ -45,7 +50,6 @@ KERNEL = "scatter_image"
 KERNEL_SOURCES = ["paper_2607_18957_amd/csrc/scatter.hip",
                   "paper_2607_18957_amd/csrc/scatter_math.h",
                   "paper_2607_18957_amd/csrc/scatter_types.h"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "scatter_image_llama8b_counters.json")
 
 
 def log(msg: str) -> None:
@@ -100,14 +104,13 @@ def h2d_peak(torch, dev, chunk_bytes: int) -> dict:
     return {"GBps": results[best], "variant": best, "all": results}
 
 
-def d2d_ceiling(torch, dev, nbytes: int = 4 << 30, reps: int = 10) -> dict:
-    """Device-to-device hipMemcpyAsync of `nbytes` (read + write counted):
-    the measured ceiling for a plain copy on this GPU. Also the plain copy
-    kernel of known size that hardware-counter readings are scaled by."""
+def calibration_copy(torch, dev, nbytes: int = 4 << 30, reps: int = 3) -> dict:
+    """A device-to-device hipMemcpyAsync of `nbytes` (the runtime's own copy
+    kernel): a plain copy kernel of known size, against which the HBM
+    counters of the profile runs are scaled."""
     a = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     b = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     a.fill_(3)
-    b.copy_(a)
     s = torch.cuda.current_stream(dev)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(reps)]
@@ -119,7 +122,8 @@ def d2d_ceiling(torch, dev, nbytes: int = 4 << 30, reps: int = 10) -> dict:
     torch.cuda.synchronize(dev)
     ms = statistics.median(x.elapsed_time(y) for x, y in ev)
     del a, b
-    return {"GBps": 2 * nbytes / (ms * 1e-3) / 1e9, "bytes": nbytes, "median_ms": ms}
+    torch.cuda.empty_cache()
+    return {"bytes": nbytes, "median_ms": ms, "GBps_read_plus_write": 2 * nbytes / (ms * 1e-3) / 1e9}
 
 
 def raw_direct_read(path: str, nbytes: int, threads: int = 8, block: int = 64 << 20) -> float:
@@ -204,41 +208,6 @@ def from_file(torch, dev, ii, plan, table, blob, dst, stream) -> dict:
     return out
 
 
-def merged_vs_per_tensor(torch, dev, ii, synth, table, plan, blob, arena, dst, stream) -> dict:
-    """The same host-blob loads through ii_load and through the naive
-    per-tensor pipeline (ii_load_pertensor), on the 8B and stress sets: what
-    merging saves. Opt-in (--compare-per-tensor)."""
-    merge = {}
-    for name in ("llama8b", "stress"):
-        t2 = table if name == "llama8b" else synth.stress()
-        p2 = plan if name == "llama8b" else ii.ii_plan(t2)
-        b2 = blob if name == "llama8b" else synth.blob(t2)
-        nb2, off2 = p2.tensors()
-        a2 = arena if name == "llama8b" else torch.empty(p2.arena_bytes, dtype=torch.uint8,
-                                                           device=dev)
-        d2 = a2.data_ptr() + off2
-        row = {"tensors": t2.n, "payload_bytes": p2.payload_bytes}
-        for label, fn in (("merged", ii.ii_load), ("per_tensor", ii.ii_load_pertensor)):
-            fn(p2, b2, d2, stream)
-            torch.cuda.synchronize(dev)
-            times = []
-            for _ in range(3):
-                t1 = time.perf_counter()
-                fn(p2, b2, d2, stream)
-                torch.cuda.synchronize(dev)
-                times.append(time.perf_counter() - t1)
-            tm = statistics.median(times)
-            row[label] = {"GBps": p2.payload_bytes / tm / 1e9, "tensors_per_s": t2.n / tm}
-        row["speedup"] = row["merged"]["GBps"] / row["per_tensor"]["GBps"]
-        merge[name] = row
-        log(f"{name}: merged {row['merged']['GBps']:.1f} GB/s, per-tensor "
-            f"{row['per_tensor']['GBps']:.1f} GB/s ({row['speedup']:.2f}x)")
-        if name != "llama8b":
-            del a2
-            p2.free()
-    return merge
-
-
 def host_info() -> dict:
     """The host the CPU baseline ran on: processor model, logical CPUs,
     NUMA nodes."""
@@ -255,44 +224,52 @@ def host_info() -> dict:
     return {"cpu_model": model, "nproc": os.cpu_count(), "numa_nodes": nodes}
 
 
-def cpu_baseline(table, blob, budget_s: float = 12.0, max_passes: int = 4,
-                 copy_budget_s: float = 5.0) -> dict:
-    """The CPU oracle pinned to one core on the whole table: the sequential
+def plan_host_threads() -> int:
+    """Host threads a plan's ring uses by default (the planner's rule)."""
+    env = os.environ.get("II_HOST_THREADS")
+    return int(env) if env else max(1, min(8, os.cpu_count() or 1))
+
+
+def cpu_baseline(table, blob, max_bytes: int = 4 << 30, budget_s: float = 10.0,
+                 max_passes: int = 1000, copy_budget_s: float = 4.0) -> dict:
+    """The CPU oracle pinned to one core on the table's first tensors up to
+    max_bytes (the whole table when it is smaller): the sequential
     allocate-and-copy loader (a fresh aligned buffer per tensor, first touch
-    included; passes until the budget is used) and, beside it, the same
-    copies into one arena whose pages were touched beforehand (copy only)."""
+    included), passes until the budget is used; beside it, the same copies
+    into one arena whose pages were touched beforehand (copy only)."""
     import oracle
     orc = oracle.default()
     nb = orc.nbytes(table)
-    payload = int(nb.sum())
+    k = int(np.searchsorted(np.cumsum(nb.astype(np.int64)), max_bytes, side="right"))
+    k = max(1, min(table.n, k))
+    snb, ssrc, sal = nb[:k], table.src_offset[:k], table.dst_align[:k]
+    sample = int(snb.sum())
     cores = os.sched_getaffinity(0)
-    one = {min(cores)}
-    os.sched_setaffinity(0, one)
+    os.sched_setaffinity(0, {min(cores)})
     try:
         passes, t0 = 0, time.perf_counter()
-        while passes < max_passes and (passes == 0 or time.perf_counter() - t0 < budget_s):
-            orc.load_alloc_timed(nb, table.src_offset, table.dst_align, blob)
+        while passes == 0 or (passes < max_passes and time.perf_counter() - t0 < budget_s):
+            orc.load_alloc_timed(snb, ssrc, sal, blob)
             passes += 1
         dt = time.perf_counter() - t0
-        _, arena_bytes = orc.layout(nb, table.dst_align)
-        arena = np.empty(max(1, arena_bytes), dtype=np.uint8)
-        arena.fill(0)
+        _, arena_bytes = orc.layout(snb, sal)
+        arena = np.zeros(max(1, arena_bytes), dtype=np.uint8)
         cpasses, t1 = 0, time.perf_counter()
-        while cpasses < max_passes and (cpasses == 0 or time.perf_counter() - t1 < copy_budget_s):
-            orc.arena(nb, table.src_offset, table.dst_align, blob, arena)
+        while cpasses == 0 or (cpasses < max_passes and time.perf_counter() - t1 < copy_budget_s):
+            orc.arena(snb, ssrc, sal, blob, arena)
             cpasses += 1
         cdt = time.perf_counter() - t1
         del arena
     finally:
         os.sched_setaffinity(0, cores)
-    return {"value": payload * passes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "tensors_per_s": table.n * passes / dt,
-            "sample": f"whole {table.name} table ({table.n} tensors, {payload} B) x {passes} "
-                      f"passes, aligned_alloc + memcpy per tensor, {dt:.1f} s on 1 of "
-                      f"{len(cores)} host cores",
-            "copy_only": {"GBps": payload * cpasses / cdt / 1e9,
-                          "tensors_per_s": table.n * cpasses / cdt,
-                          "sample": f"same table x {cpasses} passes into one pre-touched "
+    what = "whole table" if k == table.n else f"first {k} of {table.n} tensors"
+    return {"value": sample * passes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "tensors_per_s": k * passes / dt,
+            "sample": f"{what} of {table.name} ({sample} B) x {passes} passes, aligned_alloc + "
+                      f"memcpy per tensor, {dt:.1f} s on 1 of {len(cores)} host cores",
+            "copy_only": {"GBps": sample * cpasses / cdt / 1e9,
+                          "tensors_per_s": k * cpasses / cdt,
+                          "sample": f"same tensors x {cpasses} passes into one pre-touched "
                                     f"{arena_bytes}-byte arena, {cdt:.1f} s"},
             **host_info()}
 
@@ -390,14 +367,50 @@ def all_configs(torch, dev, ii, synth) -> dict:
     # C1-H1000: the 8B set behind a 1000-byte header, so every source offset
     # is 8 mod 16 against 256-aligned destinations (the misaligned path on
     # large tensors); reported beside C1, oracle not repeated
+    def tp_shard():
+        # rank 1 of 4 of the 8B set read out of its unsharded blob: the gaps
+        # kernel from the resident image, and the ring from the pageable and
+        # the pinned blob (only the shard's bytes cross the link)
+        t = synth.llama8b_tp(1, 4)
+        plan = ii.ii_plan(t)
+        _, off = plan.tensors()
+        blob = synth.blob(t)
+        arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=dev)
+        dst = arena.data_ptr() + off
+        row = {"set": t.name, "tensors": t.n, "payload_bytes": plan.payload_bytes,
+               "segments": plan.num_segments, "span_bytes": plan.span[1] - plan.span[0]}
+        e2e(plan, blob, dst, 1)
+        row["pageable"] = rate(plan, statistics.median(e2e(plan, blob, dst, 5)))
+        pinned = ii.ii_host_alloc(blob.size)
+        synth.fill(pinned.ptr, 0, blob.size, t.seed)
+        e2e(plan, pinned, dst, 1)
+        row["pinned"] = rate(plan, statistics.median(e2e(plan, pinned, dst, 5)))
+        row["pinned_link_bytes"] = plan.copy_bytes
+        pinned.free()
+        image = torch.from_numpy(blob).to(dev)
+        ms = kernel_ms(plan, image, dst, 20)
+        alg = 2 * plan.payload_bytes + table_bytes(plan)
+        row["kernel"] = {"name": "scatter_image_gaps", "ms": ms, "GBps": alg / (ms * 1e-3) / 1e9,
+                         "frac_of_hbm_peak": alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
+        out["configs"]["C1-TP1of4"] = row
+        log(f"C1-TP1of4: pageable {row['pageable']['GBps']:.1f}, pinned "
+            f"{row['pinned']['GBps']:.1f} GB/s; kernel {row['kernel']['GBps']:.0f} GB/s")
+        del image, arena, blob
+        torch.cuda.empty_cache()
+        plan.free()
+
     for cid, make, reps, osample in (("C0", synth.tiny, 100, 1 << 40),
                                      ("C2", synth.stress, 20, 1 << 40),
                                      ("C1", synth.llama8b, 5, 4 << 30),
                                      ("C1-H1000", lambda: synth.llama8b(header=1000), 5, None),
+                                     ("C1-TP1of4", None, 0, 0),
                                      ("C4", None, 0, 0),
                                      ("C3", synth.llama70b, 2, 4 << 30)):
         if cid == "C4":
             switch_c4()
+            continue
+        if cid == "C1-TP1of4":
+            tp_shard()
             continue
         t = make()
         plan = ii.ii_plan(t)
@@ -429,6 +442,10 @@ def all_configs(torch, dev, ii, synth) -> dict:
             row["pinned_kernel_reads"] = rate(
                 plan, statistics.median(e2e(plan, img, dst, reps, ii.ii_load_device)))
             pinned.free()
+        if cid == "C1":
+            # storage stage: the same blob read from a tmpfs file and from
+            # the local disk with O_DIRECT
+            row["from_file"] = from_file(torch, dev, ii, plan, t, blob, dst, stream)
         if cid == "C2":
             # the naive per-tensor pipeline on the same table: what merging saves
             e2e(plan, blob, dst, 1, ii.ii_load_pertensor)
@@ -461,14 +478,20 @@ def all_configs(torch, dev, ii, synth) -> dict:
 # ---------------------------------------------------------------------------
 # profile summaries (rocprofv3 CSV output -> profiles/*.txt, *.json)
 
-PROFILE_CMDS = {
-    "trace": "cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv -d <out>/trace "
-             "-o run -- python3 <repo>/bench.py",
-    "fetch": "cd /tmp && rocprofv3 --pmc FETCH_SIZE --output-format csv -d <out>/pmc_fetch "
-             "-o run -- python3 <repo>/bench.py --e2e-reps 1",
-    "write": "cd /tmp && rocprofv3 --pmc WRITE_SIZE --output-format csv -d <out>/pmc_write "
-             "-o run -- python3 <repo>/bench.py --e2e-reps 1",
-}
+def profile_cmds(workload: str) -> dict:
+    """The three profiled runs of the benchmark command whose summaries are
+    committed (<out> = the output folder, <repo> = this repository)."""
+    bench = "python3 <repo>/bench.py --gpus 1 --steps 20 --warmup 5"
+    if workload != DEFAULT_WORKLOAD:
+        bench += f" --workload {workload}"
+    return {
+        "trace": f"cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
+                 f"-d <out>/trace_{workload} -o run -- {bench}",
+        "fetch": f"cd /tmp && timeout -s KILL 900 rocprofv3 --pmc FETCH_SIZE --output-format csv "
+                 f"-d <out>/fetch_{workload} -o run -- {bench}",
+        "write": f"cd /tmp && timeout -s KILL 900 rocprofv3 --pmc WRITE_SIZE --output-format csv "
+                 f"-d <out>/write_{workload} -o run -- {bench}",
+    }
 
 
 def _counter_means(path: str, counter: str) -> dict:
@@ -479,21 +502,40 @@ def _counter_means(path: str, counter: str) -> dict:
         for r in csv.DictReader(fh):
             if r["Counter_Name"] != counter:
                 continue
-            k = (r["Kernel_Name"], int(r["Grid_Size"]))
+            k = (r["Kernel_Name"].split("(")[0], int(r["Grid_Size"]))
             acc.setdefault(k, []).append(float(r["Counter_Value"]))
     return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
 
 
-def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -> None:
-    """Write the committed profile summaries for the scatter kernel from one
-    kernel-trace run and two counter runs of this benchmark."""
+def _trace_durations(path: str) -> dict:
+    """Kernel durations (ns) from a rocprofv3 kernel trace, keyed by (kernel
+    name, grid size in work-items)."""
+    import csv
+    acc: dict = {}
+    with open(path) as fh:
+        for r in csv.DictReader(fh):
+            gx, gy, gz = (int(r[f"Grid_Size_{a}"]) for a in "XYZ")
+            k = (r["Kernel_Name"].split("(")[0], gx * gy * gz)
+            acc.setdefault(k, []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    return acc
+
+
+def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
+              bench_json: str) -> None:
+    """Write the committed profile summaries of the image kernel and of the
+    ring's scatter for one workload, from one kernel-trace run and two counter
+    runs of the benchmark command, and the bench line of the traced run."""
     import csv
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
-    rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
+    cmds = profile_cmds(workload)
     run = json.loads(open(bench_json).read().strip().splitlines()[-1])
-    lines = ["# Kernel statistics, llama8b-shaped workload (291 tensors, 16,060,522,496 B,",
-             "# 240 chunks of 64 MiB), one GPU",
-             f"# command: {PROFILE_CMDS['trace']}",
+    cfg, roof = run["config"], run["roofline"]
+    ring = roof["ring_kernel"]
+    rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
+    lines = [f"# Kernel statistics, {workload}-shaped workload ({cfg['tensors']} tensors, "
+             f"{cfg['payload_bytes']} B, {cfg['chunks']} chunks of {cfg['chunk_bytes'] >> 20} MiB),",
+             "# one GPU, the benchmark command under the profiler:",
+             f"# {cmds['trace']}",
              "# (rocprofv3 --stats summary, durations in ns)", ""]
     lines.append(f"{'kernel':<34}{'calls':>7}{'avg_ns':>14}{'min_ns':>12}{'max_ns':>12}{'pct':>8}")
     for r in rows:
@@ -501,121 +543,165 @@ def summarize(trace_dir: str, fetch_dir: str, write_dir: str, bench_json: str) -
         lines.append(f"{name:<34}{r['Calls']:>7}{float(r['AverageNs']):>14.1f}"
                      f"{float(r['MinNs']):>12.0f}{float(r['MaxNs']):>12.0f}"
                      f"{float(r['Percentage']):>8.2f}")
-    def named(n):
-        return [r for r in rows if r["Name"].split("(")[0] == n]
-    img = named("ii::scatter_image")[0]
-    avg_ms = float(img["AverageNs"]) / 1e6
-    lines += ["", f"scatter_image average per launch: {avg_ms:.4f} ms (rocprofv3)",
-              f"bench.py HIP-event mean in the same run: {run['roofline']['kernel_ms']:.4f} ms",
-              f"bench.py value in the same run: {run['value']:.1f} GB/s, "
-              f"roofline frac {run['roofline']['frac']:.4f}"]
-    gaps = named("ii::scatter_image_gaps")
-    gap_lines = []
-    if gaps and "tp_shard" in run:
-        tp = run["tp_shard"]
-        gap_lines = [
-            f"# scatter_image_gaps, {tp['table']}: rank 1 of 4 of the llama8b-shaped set read",
-            f"# out of its unsharded file ({tp['payload_bytes']} B, {tp['segments']} segments),",
-            "# resident image, one GPU",
-            f"# command 1: {PROFILE_CMDS['trace']}",
-            f"# command 2: {PROFILE_CMDS['fetch']}",
-            f"# command 3: {PROFILE_CMDS['write']}", "",
-            f"average per launch: {float(gaps[0]['AverageNs']) / 1e6:.4f} ms (rocprofv3, "
-            f"{gaps[0]['Calls']} launches)",
-            f"bench.py HIP-event mean in the same run: {tp['kernel']['ms']:.4f} ms, "
-            f"{tp['kernel']['GBps']:.1f} GB/s algorithmic, frac "
-            f"{tp['kernel']['frac_of_hbm_peak']:.4f}"]
-    open(os.path.join(ROOT, "profiles", "scatter_image_llama8b_kernel_stats.txt"), "w").write(
+    durs = _trace_durations(os.path.join(trace_dir, "run_kernel_trace.csv"))
+    img = [v for k, v in durs.items() if k[0] == "ii::scatter_image"]
+    full_grid = -(-cfg["chunk_bytes"] // 4096) * 128
+    slot_full = durs.get(("ii::scatter_slot", full_grid), [])
+    lines.append("")
+    if img:
+        d = np.array(img[0]) / 1e6
+        lines += [f"scatter_image (resident image, one dispatch per load): {d.size} dispatches, "
+                  f"mean {d.mean():.4f} ms, median {np.median(d):.4f} ms (kernel trace)",
+                  f"  bench.py HIP-event mean of its timed launches in the same run: "
+                  f"{roof['kernel_ms']:.4f} ms",
+                  f"  algorithmic bytes per launch {roof['bytes_per_launch']} -> "
+                  f"{roof['bytes_per_launch'] / (d.mean() * 1e-3) / 1e9:.1f} GB/s over the traced "
+                  f"mean, {100 * roof['bytes_per_launch'] / (d.mean() * 1e-3) / 1e9 / HBM_PEAK_GBPS:.1f}% "
+                  "of 8 TB/s"]
+    if slot_full:
+        d = np.array(slot_full) / 1e3
+        lines += [f"scatter_slot (ring, one dispatch per chunk), full {cfg['chunk_bytes'] >> 20} MiB "
+                  f"chunks: {d.size} dispatches, mean {d.mean():.1f} us, median {np.median(d):.1f} us",
+                  f"  {ring['bytes_per_chunk']:.0f} algorithmic bytes per chunk -> "
+                  f"{ring['bytes_per_chunk'] / (d.mean() * 1e-6) / 1e9:.1f} GB/s, "
+                  f"{100 * ring['bytes_per_chunk'] / (d.mean() * 1e-6) / 1e9 / HBM_PEAK_GBPS:.1f}% of "
+                  "8 TB/s",
+                  f"  bench.py, one traced load in the same run: mean {ring['mean_us']:.1f} us per "
+                  "full chunk (timing events on the scatter stream)"]
+    lines += ["", f"bench line of the traced run: value {run['value']:.2f} GB/s "
+              f"({100 * run['frac_of_h2d_peak']:.1f}% of the H2D peak {run['h2d_peak']['GBps']:.2f}), "
+              f"roofline frac {roof['frac']:.4f}"]
+    open(os.path.join(ROOT, "profiles", f"scatter_image_{workload}_kernel_stats.txt"), "w").write(
         "\n".join(lines) + "\n")
 
     fetch = _counter_means(os.path.join(fetch_dir, "run_counter_collection.csv"), "FETCH_SIZE")
     write = _counter_means(os.path.join(write_dir, "run_counter_collection.csv"), "WRITE_SIZE")
-    # calibration: the 4 GiB device-to-device copy (the largest runtime copy kernel)
+    # calibration: the 4 GiB device-to-device copy of the benchmark (the
+    # largest runtime copy kernel)
     copies = [k for k in fetch if k[0].startswith("__amd_rocclr_copyBuffer")]
     cal = max(copies, key=lambda k: fetch[k][0])
-    cal_kib = (4 << 30) / 1024
+    cal_kib = run["calibration_copy"]["bytes"] / 1024
     f_scale = cal_kib / fetch[cal][0]
     w_scale = cal_kib / write[cal][0]
-    key = [k for k in fetch if k[0].split("(")[0] == "ii::scatter_image"][0]
-    fetch_b = fetch[key][0] * 1024 * f_scale
-    write_b = write[key][0] * 1024 * w_scale
-    payload = run["config"]["payload_bytes"]
-    out = {"kernel": "scatter_image", "workload": "llama8b", "kernel_source_hash":
-           kernel_source_hash(), "fetch_bytes": fetch_b, "write_bytes": write_b,
-           "bytes_per_launch": fetch_b + write_b, "algorithmic_bytes":
-           run["roofline"]["bytes_per_launch"], "dispatches": fetch[key][1],
-           "calibration": {"kernel": cal[0], "grid": cal[1], "bytes_copied": 4 << 30,
-                           "fetch_kib": fetch[cal][0], "write_kib": write[cal][0],
-                           "fetch_scale": f_scale, "write_scale": w_scale}}
-    json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
-    t = ["# HBM traffic of scatter_image, llama8b-shaped workload, from rocprofv3 counters",
-         f"# command 1: {PROFILE_CMDS['fetch']}",
-         f"# command 2: {PROFILE_CMDS['write']}",
+    out = {"kernel": "scatter_image", "workload": workload, "kernel_source_hash":
+           kernel_source_hash(), "calibration": {
+               "kernel": cal[0], "grid": cal[1], "bytes_copied": run["calibration_copy"]["bytes"],
+               "fetch_kib": fetch[cal][0], "write_kib": write[cal][0],
+               "fetch_scale": f_scale, "write_scale": w_scale}}
+    t = [f"# HBM traffic, {workload}-shaped workload, from rocprofv3 counters",
+         f"# command 1: {cmds['fetch']}",
+         f"# command 2: {cmds['write']}",
          "# Counters are KiB per dispatch. Scale factors come from the 4 GiB device-to-device",
          "# copy in the same runs (a plain copy kernel of known size: 4 GiB read, 4 GiB written).",
          "",
          f"calibration kernel        {cal[0]} (grid {cal[1]}), {fetch[cal][1]} dispatches",
          f"  FETCH_SIZE per dispatch {fetch[cal][0]:.1f} KiB  -> scale {f_scale:.4f}",
-         f"  WRITE_SIZE per dispatch {write[cal][0]:.1f} KiB  -> scale {w_scale:.4f}",
-         f"scatter_image             {fetch[key][1]} dispatches (grid {key[1]})",
-         f"  FETCH_SIZE per dispatch {fetch[key][0]:.1f} KiB  -> {fetch_b:.0f} B",
-         f"  WRITE_SIZE per dispatch {write[key][0]:.1f} KiB  -> {write_b:.0f} B",
-         f"  measured HBM bytes per launch  {fetch_b + write_b:.0f}",
-         f"  algorithmic bytes per launch   {run['roofline']['bytes_per_launch']} "
-         f"(2 x payload {payload} + segment and tile tables)",
-         f"  measured / algorithmic         {(fetch_b + write_b) / run['roofline']['bytes_per_launch']:.4f}",
-         f"kernel source hash        {kernel_source_hash()}"]
-    gk = [k for k in fetch if k[0].split("(")[0] == "ii::scatter_image_gaps"]
-    if gk and "tp_shard" in run:
-        k = gk[0]
-        tp = run["tp_shard"]
-        gf, gw = fetch[k][0] * 1024 * f_scale, write[k][0] * 1024 * w_scale
-        alg = tp["kernel"]["bytes_per_launch"]
-        out["tp_shard"] = {"kernel": "scatter_image_gaps", "workload": tp["table"],
-                           "fetch_bytes": gf, "write_bytes": gw, "bytes_per_launch": gf + gw,
-                           "algorithmic_bytes": alg, "dispatches": fetch[k][1]}
-        json.dump(out, open(TRAFFIC_FILE, "w"), indent=1)
-        gap_lines += ["", "counters (KiB per dispatch, scaled as for scatter_image):",
-                      f"  {fetch[k][1]} dispatches (grid {k[1]} work-items)",
-                      f"  FETCH_SIZE per dispatch {fetch[k][0]:.1f} KiB  -> {gf:.0f} B",
-                      f"  WRITE_SIZE per dispatch {write[k][0]:.1f} KiB  -> {gw:.0f} B",
-                      f"  measured HBM bytes per launch  {gf + gw:.0f}",
-                      f"  algorithmic bytes per launch   {alg} (2 x payload + segment and tile "
-                      "tables)",
-                      f"  measured / algorithmic         {(gf + gw) / alg:.4f}",
-                      f"kernel source hash        {kernel_source_hash()}"]
-    slot = [k for k in fetch if k[0].split("(")[0] == "ii::scatter_slot"]
-    if slot:
-        k = slot[0]
-        t += [f"scatter_slot (ring path)  {fetch[k][1]} dispatches, per 64 MiB chunk: "
-              f"fetch {fetch[k][0] * 1024 * f_scale:.0f} B, "
-              f"write {write[k][0] * 1024 * w_scale:.0f} B"]
-    open(os.path.join(ROOT, "profiles", "scatter_image_llama8b_counters.txt"), "w").write(
+         f"  WRITE_SIZE per dispatch {write[cal][0]:.1f} KiB  -> scale {w_scale:.4f}"]
+    key = [k for k in fetch if k[0] == "ii::scatter_image"]
+    if key:
+        k = key[0]
+        fb, wb = fetch[k][0] * 1024 * f_scale, write[k][0] * 1024 * w_scale
+        alg = roof["bytes_per_launch"]
+        out.update(fetch_bytes=fb, write_bytes=wb, bytes_per_launch=fb + wb,
+                   algorithmic_bytes=alg, dispatches=fetch[k][1])
+        t += [f"scatter_image             {fetch[k][1]} dispatches (grid {k[1]} work-items)",
+              f"  FETCH_SIZE per dispatch {fetch[k][0]:.1f} KiB  -> {fb:.0f} B",
+              f"  WRITE_SIZE per dispatch {write[k][0]:.1f} KiB  -> {wb:.0f} B",
+              f"  measured HBM bytes per launch  {fb + wb:.0f}",
+              f"  algorithmic bytes per launch   {alg} (2 x payload + segment and tile tables)",
+              f"  measured / algorithmic         {(fb + wb) / alg:.4f}"]
+    sk = ("ii::scatter_slot", full_grid)
+    if sk in fetch and sk in write:
+        fb, wb = fetch[sk][0] * 1024 * f_scale, write[sk][0] * 1024 * w_scale
+        out["ring_chunk"] = {"kernel": "scatter_slot", "fetch_bytes": fb, "write_bytes": wb,
+                             "bytes_per_chunk": fb + wb,
+                             "algorithmic_bytes": ring["bytes_per_chunk"],
+                             "dispatches": fetch[sk][1]}
+        t += [f"scatter_slot (ring)       {fetch[sk][1]} dispatches of a full "
+              f"{cfg['chunk_bytes'] >> 20} MiB chunk (grid {sk[1]} work-items)",
+              f"  FETCH_SIZE per dispatch {fetch[sk][0]:.1f} KiB  -> {fb:.0f} B",
+              f"  WRITE_SIZE per dispatch {write[sk][0]:.1f} KiB  -> {wb:.0f} B",
+              f"  measured / algorithmic         {(fb + wb) / ring['bytes_per_chunk']:.4f}"]
+    t.append(f"kernel source hash        {kernel_source_hash()}")
+    json.dump(out, open(traffic_file(workload), "w"), indent=1)
+    open(os.path.join(ROOT, "profiles", f"scatter_image_{workload}_counters.txt"), "w").write(
         "\n".join(t) + "\n")
-    if gap_lines:
-        open(os.path.join(ROOT, "profiles", "scatter_image_gaps_llama8b_tp1of4.txt"), "w").write(
-            "\n".join(gap_lines) + "\n")
-    print("\n".join(lines + [""] + t + [""] + gap_lines))
+    print("\n".join(lines + [""] + t))
+
+
+WORKLOADS = {
+    "tiny": lambda synth: synth.tiny(),
+    "stress": lambda synth: synth.stress(),
+    "llama8b": lambda synth: synth.llama8b(),
+    "mistral7b": lambda synth: synth.mistral7b(),
+    "llama70b": lambda synth: synth.llama70b(),
+}
+DEFAULT_WORKLOAD = "llama70b"
+# the shapes each set follows (synthetic bits in these tensor shapes)
+SHAPES = {"tiny": "a 4-layer hidden-256 transformer", "stress": "100,000 1-D tensors of 64 B-64 KiB",
+          "llama8b": "Llama-3.1-8B", "mistral7b": "Mistral-7B", "llama70b": "Llama-3.1-70B"}
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"scatter_image_{workload}_counters.json")
+
+
+def recorded_traffic(workload: str):
+    """HBM bytes per launch of the image kernel from the committed counter
+    runs, if they were taken on the current kernel source."""
+    path = traffic_file(workload)
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def ring_kernel(trace: dict, plan) -> dict:
+    """The ring's scatter (scatter_slot) from one traced load: per-chunk
+    duration between its start and end events on the scatter stream, full
+    chunks only, with the algorithmic bytes of a full chunk (read + write of
+    its bytes, its segment rows and 8-byte tile ranges)."""
+    ss, se = trace["scatter_start"], trace["scatter_end"]
+    cs, ce = trace["copy_start"], trace["copy_end"]
+    _, clen, sb = plan.chunks()
+    full = np.flatnonzero(clen == plan.chunk_bytes)
+    dur = (se - ss)[full]
+    dur = dur[~np.isnan(dur)]
+    segs = float(np.mean(np.diff(sb.astype(np.int64))[full]))
+    tiles = -(-plan.chunk_bytes // plan.tiles()["tile_bytes"])
+    alg = 2 * plan.chunk_bytes + 16 * segs + 8 * tiles
+    us = float(np.mean(dur)) * 1e3
+    cdur = (ce - cs)[full]
+    cdur = cdur[~np.isnan(cdur)]
+    return {"kernel": "scatter_slot", "chunk_bytes": plan.chunk_bytes, "chunks": int(dur.size),
+            "mean_us": us, "median_us": float(np.median(dur)) * 1e3,
+            "bytes_per_chunk": alg, "GBps": alg / (us * 1e-6) / 1e9,
+            "frac": alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
+            "copy_us_per_chunk": float(np.median(cdur)) * 1e3,
+            "copy_GBps": plan.chunk_bytes / (float(np.median(cdur)) * 1e-3) / 1e9}
 
 
 def main() -> int:
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
-        summarize(*sys.argv[2:6])
+        summarize(*sys.argv[2:7])
         return 0
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--e2e-reps", type=int, default=5)
-    ap.add_argument("--compare-per-tensor", action="store_true",
-                    help="also time the naive per-tensor pipeline on the 8B and stress sets")
+    ap.add_argument("--steps", type=int, default=10, help="timed loads")
+    ap.add_argument("--warmup", type=int, default=2, help="untimed loads before them")
+    ap.add_argument("--kernel-reps", type=int, default=10,
+                    help="timed launches of the image kernel (roofline leg)")
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default=DEFAULT_WORKLOAD)
     ap.add_argument("--configs", action="store_true",
                     help="instead of the benchmark line, measure every workload (tiny, stress, "
-                         "8B, 70B, switch) and print one JSON line of results")
+                         "8B, 70B, switch, tensor-parallel shard) and print one JSON line")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: the loader runs on one GPU; --gpus {args.gpus} is not supported "
-              "(loading across GPUs is designed but not implemented)", file=sys.stderr)
+        print(f"bench.py: one GPU only; --gpus {args.gpus} is not supported (loading across "
+              "GPUs is designed, not built: every rank would run this path on its own shard "
+              "table and link)", file=sys.stderr)
         return 2
 
     import torch
@@ -626,221 +712,113 @@ def main() -> int:
     if args.configs:
         print(json.dumps(all_configs(torch, dev, ii, synth)), flush=True)
         return 0
-    table = synth.llama8b()
+
+    table = WORKLOADS[args.workload](synth)
     plan = ii.ii_plan(table)
+    plan.prepare()  # ring and tables: allocated once, before any timing
     nb, off = plan.tensors()
     payload = plan.payload_bytes
-    lo, hi = plan.span
     log(f"workload {table.name}: N={table.n} payload={payload} K={plan.num_chunks} "
         f"S={plan.num_segments} C={plan.chunk_bytes}")
-
-    blob = synth.blob(table)
-    image = torch.from_numpy(blob).to(dev)
-    arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=dev)
-    dst = arena.data_ptr() + off
     stream = torch.cuda.current_stream(dev)
 
-    # ---- timed steps: resident image -> every tensor, one launch per step
-    for _ in range(args.warmup):
-        ii.ii_load_device(plan, image, dst, stream)
+    h2d = h2d_peak(torch, dev, plan.chunk_bytes)
+    torch.cuda.empty_cache()
+    log(f"H2D peak {h2d['GBps']:.2f} GB/s ({h2d['variant']})")
+
+    log(f"blob: {table.blob_bytes} bytes of pageable host memory")
+    blob = np.empty(table.blob_bytes, np.uint8)
+    synth.fill(blob.ctypes.data, 0, table.blob_bytes, table.seed, threads=16)
+    arena = torch.empty(plan.arena_bytes, dtype=torch.uint8, device=dev)
+    dst = arena.data_ptr() + off
+
+    # ---- timed steps: pageable blob -> every tensor through the ring
+    for i in range(args.warmup):
+        ii.ii_load(plan, blob, dst, stream)
+        torch.cuda.synchronize(dev)
+        log(f"warm-up load {i + 1}/{args.warmup}")
     torch.cuda.synchronize(dev)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
-    torch.cuda.synchronize(dev)
-    t0 = time.perf_counter()
-    for a, b in ev:
-        a.record(stream)
-        ii.ii_load_device(plan, image, dst, stream)
-        b.record(stream)
+    c0, t0 = time.process_time(), time.perf_counter()
+    for i in range(args.steps):
+        ii.ii_load(plan, blob, dst, stream)
+        if args.steps >= 4 and (i + 1) % max(1, args.steps // 4) == 0:
+            log(f"timed load {i + 1}/{args.steps} enqueued")
     torch.cuda.synchronize(dev)
     wall = time.perf_counter() - t0
+    host_cores = (time.process_time() - c0) / wall
     ms_step = wall * 1e3 / args.steps
-    kernel_ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
-    log(f"steps: {ms_step:.3f} ms/step wall, kernel {kernel_ms:.3f} ms")
+    value = payload * args.steps / wall / 1e9
+    log(f"steps: {ms_step:.1f} ms/load, {value:.2f} GB/s "
+        f"({100 * value / h2d['GBps']:.1f}% of the H2D peak), {host_cores:.1f} host cores")
 
-    # ---- tensor-parallel shard (rank 1 of 4) read out of the same unsharded image
-    tp = {"table": None}
-    tp_t = synth.llama8b_tp(1, 4)
-    assert tp_t.blob_bytes == table.blob_bytes and tp_t.seed == table.seed  # same file
-    tp_plan = ii.ii_plan(tp_t)
-    _, tp_off = tp_plan.tensors()
-    tp_arena = torch.empty(tp_plan.arena_bytes, dtype=torch.uint8, device=dev)
-    tp_dst = tp_arena.data_ptr() + tp_off
-    for _ in range(args.warmup):
-        ii.ii_load_device(tp_plan, image, tp_dst, stream)
-    tev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
-    for a, b in tev:
-        a.record(stream)
-        ii.ii_load_device(tp_plan, image, tp_dst, stream)
-        b.record(stream)
-    torch.cuda.synchronize(dev)
-    tp_kms = statistics.mean(a.elapsed_time(b) for a, b in tev)
-    tp_alg = 2 * tp_plan.payload_bytes + table_bytes(tp_plan)
-    tp_traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        rec = json.load(open(TRAFFIC_FILE))
-        if rec.get("kernel_source_hash") == kernel_source_hash() and "tp_shard" in rec:
-            tp_traffic = rec["tp_shard"]["bytes_per_launch"]
-    tp.update(table=tp_t.name, tensors=tp_t.n, payload_bytes=tp_plan.payload_bytes,
-              segments=tp_plan.num_segments, chunks=tp_plan.num_chunks,
-              span_bytes=tp_plan.span[1] - tp_plan.span[0],
-              pinned_copy_bytes=tp_plan.copy_bytes,
-              kernel={"name": "scatter_image_gaps", "ms": tp_kms,
-                      "GBps": tp_alg / (tp_kms * 1e-3) / 1e9, "traffic": tp_traffic,
-                      "frac_of_hbm_peak": tp_alg / (tp_kms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
-                      "bytes_per_launch": tp_alg})
-    log(f"tp shard {tp_t.name}: kernel {tp_kms:.3f} ms, "
-        f"{tp['kernel']['GBps']:.0f} GB/s algorithmic, S={tp_plan.num_segments}")
-
-    # spot check of the timed configuration against the blob (full parity is in the tests)
+    # spot check of the timed configuration (full parity is in the tests)
     rng = np.random.default_rng(0)
-    for i in rng.choice(table.n, size=8, replace=False):
+    for i in rng.choice(table.n, size=min(8, table.n), replace=False):
         n = int(nb[i])
+        if not n:
+            continue
         j = int(rng.integers(0, max(1, n - 4096)))
         m = min(4096, n - j)
         got = arena[int(off[i]) + j:int(off[i]) + j + m].cpu().numpy()
-        s = int(table.src_offset[i]) + j
-        if not np.array_equal(got, blob[s:s + m]):
+        s0 = int(table.src_offset[i]) + j
+        if not np.array_equal(got, blob[s0:s0 + m]):
             log(f"MISMATCH in tensor {i}")
             return 1
 
-    # ---- roofline of the scatter kernel
-    alg_bytes = 2 * payload + table_bytes(plan)
-    achieved = alg_bytes / (kernel_ms * 1e-3) / 1e9
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        rec = json.load(open(TRAFFIC_FILE))
-        if rec.get("kernel_source_hash") == kernel_source_hash():
-            traffic = rec.get("bytes_per_launch")
+    # ---- the ring's scatter, from one traced (untimed) load
+    plan.set_trace(True)
+    ii.ii_load(plan, blob, dst, stream)
+    torch.cuda.synchronize(dev)
+    ring = ring_kernel(plan.trace(), plan)
+    plan.set_trace(False)
+    log(f"ring scatter_slot: {ring['mean_us']:.1f} us per {plan.chunk_bytes >> 20} MiB chunk, "
+        f"{ring['GBps']:.0f} GB/s algorithmic; copy {ring['copy_us_per_chunk']:.0f} us per chunk")
+    plan.release()
 
-    d2d = d2d_ceiling(torch, dev)
-    log(f"D2D copy ceiling {d2d['GBps']:.0f} GB/s")
-
-    # ---- end to end through the host: pageable and pinned blobs
-    del image
+    # ---- roofline: the scatter kernel alone, from a resident image
     torch.cuda.empty_cache()
-    h2d = h2d_peak(torch, dev, plan.chunk_bytes)
-    log(f"H2D peak {h2d['GBps']:.2f} GB/s ({h2d['variant']})")
-    e2e = {"h2d_peak_GBps": h2d["GBps"], "h2d_peak_variant": h2d["variant"]}
-    # process CPU time (every thread: host copy pool, HIP runtime) over wall
-    # time of the timed loads: the host cores a load keeps busy
-    cpu_log = []
-
-    def cores(n):
-        c, w = (sum(x) for x in zip(*cpu_log[-n:])) if len(cpu_log) >= n else (0.0, 0.0)
-        cpu_log.clear()
-        return c / w if w else None
-
-    def timed(fn, p, src, d) -> float:
-        c1, t1 = time.process_time(), time.perf_counter()
-        fn(p, src, d, stream)
+    free, _ = torch.cuda.mem_get_info(dev)
+    roof = {"bound": "hbm", "peak": HBM_PEAK_GBPS, "unit": "GB/s", "kernel": KERNEL}
+    if free > table.blob_bytes + (1 << 30):
+        log("image: blob -> HBM")
+        image = torch.from_numpy(blob).to(dev)
+        for _ in range(2):
+            ii.ii_load_device(plan, image, dst, stream)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.kernel_reps)]
         torch.cuda.synchronize(dev)
-        w = time.perf_counter() - t1
-        cpu_log.append((time.process_time() - c1, w))
-        return w
-
-    def timed_load(src) -> float:
-        return timed(ii.ii_load, plan, src, dst)
-
-    def report(label, times):
-        t = statistics.median(times)
-        e2e[label] = {"GBps": payload / t / 1e9, "tensors_per_s": table.n / t,
-                      "frac_of_h2d_peak": payload / t / 1e9 / h2d["GBps"], "median_s": t,
-                      "runs": len(times), "host_cores": cores(len(times))}
-        log(f"e2e {label}: {payload / t / 1e9:.2f} GB/s "
-            f"({100 * payload / t / 1e9 / h2d['GBps']:.1f}% of H2D peak)")
-
-    def tp_load(src) -> float:
-        return timed(ii.ii_load, tp_plan, src, tp_dst)
-
-    def tp_report(label, times, link_bytes):
-        t = statistics.median(times)
-        tp[label] = {"GBps": tp_plan.payload_bytes / t / 1e9, "link_bytes": link_bytes,
-                     "link_GBps": link_bytes / t / 1e9,
-                     "frac_of_h2d_peak": tp_plan.payload_bytes / t / 1e9 / h2d["GBps"],
-                     "median_s": t, "runs": len(times), "host_cores": cores(len(times))}
-        log(f"tp shard {label}: {tp_plan.payload_bytes / t / 1e9:.2f} GB/s of shard bytes, "
-            f"link {link_bytes / t / 1e9:.2f} GB/s")
-
-    # pageable blob: staged through the pinned ring by the host threads. Cold:
-    # a fresh plan whose first load allocates its ring and tables; prepared:
-    # a fresh plan whose ring and tables were allocated beforehand
-    # (ii_plan_prepare, as a cold-starting process would during its other
-    # initialisation); then warm loads.
-    for label, prep in (("pageable_cold", False), ("pageable_cold_prepared", True)):
-        p2 = ii.ii_plan(table)
-        if prep:
-            p2.prepare()
-        t1 = time.perf_counter()
-        ii.ii_load(p2, blob, dst, stream)
+        for a, b in ev:
+            a.record(stream)
+            ii.ii_load_device(plan, image, dst, stream)
+            b.record(stream)
         torch.cuda.synchronize(dev)
-        report(label, [time.perf_counter() - t1])
-        p2.free()
-    timed_load(blob)  # warm: ring allocation, tables
-    report("pageable", [timed_load(blob) for _ in range(args.e2e_reps)])
-    # the shard: the host stage gathers only its bytes, so the link moves the payload
-    tp_load(blob)
-    tp_report("e2e_pageable_packed", [tp_load(blob) for _ in range(args.e2e_reps)],
-              tp_plan.payload_bytes)
-    # pinned blob: DMA straight from it; its first load also maps its pages for the device
-    pinned = ii.ii_host_alloc(blob.size)
-    synth.fill(pinned.ptr, 0, blob.size, table.seed)
-    report("pinned_first_load", [timed_load(pinned)])
-    report("pinned", [timed_load(pinned) for _ in range(args.e2e_reps)])
-    # the shard from the pinned blob: chunks that are mostly gaps are gathered
-    # through the staging slot, the others go by DMA in place
-    tp_load(pinned)
-    tp_report("e2e_pinned", [tp_load(pinned) for _ in range(args.e2e_reps)],
-              tp_plan.copy_bytes)
-    # the same pinned blob read by the gaps kernel itself (ii_load_device on
-    # host memory): only the shard's rows cross the link, no ring
-    pinned_img = (pinned.ptr, blob.size)
-    timed(ii.ii_load_device, tp_plan, pinned_img, tp_dst)
-    tp_report("e2e_pinned_kernel_reads",
-              [timed(ii.ii_load_device, tp_plan, pinned_img, tp_dst)
-               for _ in range(args.e2e_reps)], tp_plan.payload_bytes)
-    e2e["ring"] = {"depth": 3, "copy_streams": 2, "chunk_bytes": plan.chunk_bytes}
-    e2e["host_threads"] = int(os.environ.get("II_HOST_THREADS", min(8, os.cpu_count() or 1)))
-    pinned.free()
-
-    # ---- from a file: tmpfs (in-memory storage) and disk with O_DIRECT
-    e2e["from_file"] = from_file(torch, dev, ii, plan, table, blob, dst, stream)
-
-    # ---- model switch: the 8B arena reused for the Mistral-7B-shaped set
-    new_t = synth.mistral7b()
-    new_plan = ii.ii_plan(new_t)
-    new_blob = synth.blob(new_t)
-    sw_times = []
-    for rep in range(4):
-        ii.ii_load(plan, blob, dst, stream)  # the arena holds the old set again
-        torch.cuda.synchronize(dev)
-        t1 = time.perf_counter()
-        ii.ii_switch(plan, new_plan, arena, plan.arena_bytes, new_blob, stream)
-        torch.cuda.synchronize(dev)
-        if rep:
-            sw_times.append(time.perf_counter() - t1)
-    tsw = statistics.median(sw_times)
-    e2e["switch"] = {"from": table.name, "to": new_t.name,
-                     "new_payload_bytes": new_plan.payload_bytes,
-                     "scrubbed_bytes": plan.arena_bytes - new_plan.arena_bytes,
-                     "GBps": new_plan.payload_bytes / tsw / 1e9, "median_s": tsw,
-                     "frac_of_h2d_peak": new_plan.payload_bytes / tsw / 1e9 / h2d["GBps"]}
-    log(f"switch {table.name} -> {new_t.name}: {e2e['switch']['GBps']:.2f} GB/s "
-        f"({100 * e2e['switch']['frac_of_h2d_peak']:.1f}% of H2D peak)")
-    del new_blob
-    new_plan.free()
-
-    if args.compare_per_tensor:
-        e2e["merged_vs_per_tensor"] = merged_vs_per_tensor(torch, dev, ii, synth, table, plan,
-                                                           blob, arena, dst, stream)
+        kernel_ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
+        del image
+        torch.cuda.empty_cache()
+        alg = 2 * payload + table_bytes(plan)
+        achieved = alg / (kernel_ms * 1e-3) / 1e9
+        roof.update(achieved=achieved, frac=achieved / HBM_PEAK_GBPS,
+                    traffic=recorded_traffic(args.workload),
+                    workload=f"{table.name}, blob image resident in HBM, one dispatch per load",
+                    bytes_per_launch=alg, kernel_ms=kernel_ms, launches=args.kernel_reps)
+        log(f"{KERNEL}: {kernel_ms:.3f} ms per launch, {achieved:.0f} GB/s algorithmic "
+            f"({100 * achieved / HBM_PEAK_GBPS:.1f}% of HBM peak)")
+    else:
+        roof.update(achieved=None, frac=None, traffic=None,
+                    skipped="image and arena do not fit in HBM together")
+    roof["ring_kernel"] = ring
+    del arena
+    torch.cuda.empty_cache()
+    # a plain device-to-device copy of known size: the kernel the hardware
+    # counters of the profile runs are calibrated against
+    cal = calibration_copy(torch, dev)
 
     cpu = cpu_baseline(table, blob)
-    log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core")
+    log(f"cpu oracle: {cpu['value']:.2f} GB/s on 1 core ({cpu['sample']})")
 
     out = {
         "metric": METRIC,
-        "value": payload / (ms_step * 1e-3) / 1e9,
+        "value": value,
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -850,22 +828,27 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "u8",
-        "data": "synthetic (seeded random bits in Llama-3.1-8B tensor shapes)",
-        "config": {"workload": "llama8b-shaped weight set, blob image resident in HBM -> "
-                               "291 tensors in one device arena",
+        "data": f"synthetic (seeded random bits in {SHAPES[args.workload]} tensor shapes)",
+        "config": {"workload": f"{table.name}-shaped weight set ({table.n} tensors, {payload} B) "
+                               "loaded from a pageable host blob: host threads stage each "
+                               f"{plan.chunk_bytes >> 20} MiB chunk into a 3-slot pinned ring, one "
+                               "hipMemcpyAsync per chunk carries it over PCIe (exactly the "
+                               "payload crosses the link), the scatter kernel writes it into "
+                               "the tensors of one device arena",
                    "tensors": table.n, "payload_bytes": payload,
                    "chunk_bytes": plan.chunk_bytes, "chunks": plan.num_chunks,
-                   "segments": plan.num_segments, "dst_align": 256,
+                   "segments": plan.num_segments, "dst_align": int(table.dst_align[0]),
+                   "ring_depth": 3, "host_threads": plan_host_threads(),
                    "parallelism": "single GPU"},
-        "tensors_per_s": table.n / (ms_step * 1e-3),
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": traffic,
-                     "kernel": KERNEL, "bytes_per_launch": alg_bytes,
-                     "kernel_ms": kernel_ms, "d2d_copy_ceiling_GBps": d2d["GBps"],
-                     "frac_of_d2d_ceiling": achieved / d2d["GBps"]},
+        "tensors_per_s": table.n * args.steps / wall,
+        "frac_of_h2d_peak": value / h2d["GBps"],
+        "h2d_peak": {"GBps": h2d["GBps"], "variant": h2d["variant"],
+                     "what": "pinned host -> device hipMemcpyAsync, best of {chunk, 1 GiB} x "
+                             "{1, 2} streams"},
+        "host_cores": host_cores,
+        "roofline": roof,
         "cpu_baseline": cpu,
-        "e2e": e2e,
-        "tp_shard": tp,
+        "calibration_copy": cal,
     }
     print(json.dumps(out), flush=True)
     return 0

@@ -40,6 +40,40 @@ def test_counter_means(tmp_path):
         for name, grid, counter, value in rows:
             f.write(f"\"{name}\",{grid},{counter},{value}\n")
     got = bench._counter_means(str(path), "FETCH_SIZE")
-    assert got[("ii::scatter_image(x)", 1024)] == (20.0, 2)
+    assert got[("ii::scatter_image", 1024)] == (20.0, 2)
     assert got[("__amd_rocclr_copyBuffer", 64)] == (5.0, 1)
-    assert bench._counter_means(str(path), "WRITE_SIZE") == {("ii::scatter_image(x)", 1024): (7.0, 1)}
+    assert bench._counter_means(str(path), "WRITE_SIZE") == {("ii::scatter_image", 1024): (7.0, 1)}
+
+
+def test_trace_durations(tmp_path):
+    """Kernel durations from a kernel trace, keyed by name and total grid
+    size in work-items (a 2-D grid counts x * y)."""
+    path = tmp_path / "run_kernel_trace.csv"
+    with open(path, "w") as f:
+        f.write("Kernel_Name,Grid_Size_X,Grid_Size_Y,Grid_Size_Z,Start_Timestamp,End_Timestamp\n")
+        f.write("\"ii::scatter_slot(a, b)\",8192,1,1,100,350\n")
+        f.write("\"ii::scatter_slot(a, b)\",8192,1,1,400,600\n")
+        f.write("\"ii::scatter_image(c)\",1024,3,1,1000,9000\n")
+    got = bench._trace_durations(str(path))
+    assert got[("ii::scatter_slot", 8192)] == [250, 200]
+    assert got[("ii::scatter_image", 3072)] == [8000]
+
+
+def test_ring_kernel_from_trace():
+    """Per-chunk scatter figures from a load's timeline: full chunks only,
+    chunks without segments (NaN) skipped, and the algorithmic bytes of a
+    full chunk (its bytes read and written, its segment rows, its tiles)."""
+    import numpy as np
+    plan = ii.ii_plan(synth.tiny(chunk=1 << 20))
+    K = plan.num_chunks
+    ss = np.arange(K, dtype=np.float32) * 1.0
+    tr = {"scatter_start": ss, "scatter_end": ss + 0.01, "copy_start": ss - 0.5,
+          "copy_end": ss - 0.4}
+    r = bench.ring_kernel(tr, plan)
+    _, clen, sb = plan.chunks()
+    full = clen == plan.chunk_bytes
+    assert r["chunks"] == int(full.sum())
+    assert abs(r["mean_us"] - 10.0) < 1e-3
+    segs = np.diff(sb.astype(np.int64))[full].mean()
+    assert abs(r["bytes_per_chunk"] - (2 * (1 << 20) + 16 * segs + 8 * 256)) < 1e-6
+    assert abs(r["copy_us_per_chunk"] - 100.0) < 1e-2
