@@ -45,7 +45,9 @@ enum {
     II_EBUSY = 7,     /* the plan is in use by another call */
     II_EHIP = 8,      /* any other HIP runtime error (detail in ii_last_error) */
     II_ERANGE = 9,    /* the blob, image or file is shorter than the plan's span end */
-    II_EIO = 10       /* reading the model file failed (detail in ii_last_error) */
+    II_EIO = 10,      /* reading the model file failed (detail in ii_last_error) */
+    II_ESCRATCH = 11  /* the plan's tables exceed the static workspace of
+                         ii_load_device_noalloc */
 };
 
 /* ---- element types (storage width in brackets) ---------------------------- */
@@ -233,6 +235,27 @@ int ii_load_file(ii_plan_t* plan, int fd, uint64_t file_bytes, void* const* dst_
  */
 int ii_load_device(ii_plan_t* plan, const void* dev_image, uint64_t image_bytes,
                    void* const* dst_ptrs, hipStream_t stream);
+
+/*
+ * ii_load_device_noalloc -- ii_load_device for callers that cannot allocate
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same result, arguments, ordering and errors, but
+ * the call allocates nothing -- no device or pinned host memory, no events,
+ * streams or plan state. The kernel's tables (a 16-byte row per segment, an
+ * 8-byte segment range per tile, and for tables with gaps an 8-byte window
+ * and a 4-byte chunk index per tile) are uploaded on every call, on
+ * `stream`, into a static device workspace of 64 MiB that the library holds
+ * on each GPU it runs on until the process ends; a plan whose tables need
+ * more returns II_ESCRATCH before anything is checked or enqueued (the
+ * Llama-8B-shaped table needs 31 MB, the 100,000-tensor one 3.4 MB). Calls
+ * on one GPU share that workspace: two calls ordered on one stream are
+ * safe, calls that overlap on different streams of one GPU race (the later
+ * upload may overwrite tables an earlier kernel still reads) and must be
+ * ordered by the caller.
+ * Errors: as ii_load_device, plus II_ESCRATCH.
+ */
+int ii_load_device_noalloc(ii_plan_t* plan, const void* dev_image, uint64_t image_bytes,
+                           void* const* dst_ptrs, hipStream_t stream);
 
 /*
  * ii_load_pertensor -- the same result as ii_load by the naive per-tensor

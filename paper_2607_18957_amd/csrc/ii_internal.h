@@ -45,6 +45,9 @@ struct DstRange {
     size_t i;
 };
 
+// Static device workspace of ii_load_device_noalloc (runtime.hip).
+constexpr uint64_t kScratchBytes = 64ull << 20;
+
 struct Runtime;  // device-side state (runtime.hip)
 
 void set_error(const char* fmt, ...);
@@ -104,6 +107,11 @@ struct ii_plan_s {
     // segments (every full chunk then has that many tiles and tile g is
     // window g % it of chunk g / it), else 0
     uint32_t tiles_per_chunk = 0;
+    // host buffers of ii_load_device_noalloc, sized when the plan is made so
+    // that the call itself allocates nothing: the segment rows with resolved
+    // destinations, and the destination ranges its checks sort
+    std::vector<ii::SegDev> na_rows;
+    std::vector<ii::DstRange> na_ranges;
     // runtime configuration
     uint32_t ring_depth = 3;
     uint32_t host_threads = 8;

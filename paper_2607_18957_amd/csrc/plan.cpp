@@ -385,6 +385,8 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         // no chunk has a gap: tile m of every chunk is the window [m*T,
         // (m+1)*T) of it, and full chunks have ceil(C / T) tiles each
         p->tiles_per_chunk = p->packed_distinct ? 0 : (uint32_t)((C + T - 1) / T);
+        p->na_rows.resize(S);
+        p->na_ranges.reserve(n);
     } catch (const std::bad_alloc&) {
         return fail(II_ENOMEM, "ii_plan: host allocation failed");
     }
@@ -504,6 +506,7 @@ extern "C" const char* ii_strerror(int status) {
     case II_EHIP: return "HIP runtime error";
     case II_ERANGE: return "blob, image or file shorter than the plan's span";
     case II_EIO: return "reading the model file failed";
+    case II_ESCRATCH: return "plan tables exceed the static workspace";
     default: return "unknown status";
     }
 }

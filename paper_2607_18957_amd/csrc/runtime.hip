@@ -40,6 +40,7 @@
 #include <cmath>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <vector>
 
 #include "copy_pool.h"
@@ -751,6 +752,102 @@ static int run_device(ii_plan_t* p, const uint8_t* image, const uint64_t* dst, h
     return II_OK;
 }
 
+// ---------------------------------------------------------------------------
+// The resident-image load without allocation: the kernel's tables go into
+// `scratch`, a static device array each GPU holds for the life of the
+// process, uploaded on the call's stream every time (another plan's call may
+// have overwritten them in between).
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static uint8_t* g_scratch[kMaxDevices];  // device address of `scratch`, per device
+
+// The device address of the current device's copy of `scratch`, looked up
+// once per device. (In host code the array's name is only a host-side
+// stand-in for the symbol; kernels and copies must use this address.)
+static int scratch_ptr(uint8_t** out) {
+    int dev = -1;
+    II_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(II_EINVAL, "device %d is beyond the %d the library supports", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !ptr) {
+            (void)hipGetLastError();
+            return fail(II_EHIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        }
+        g_scratch[dev] = static_cast<uint8_t*>(ptr);
+    }
+    *out = g_scratch[dev];
+    return II_OK;
+}
+
+// Where each table of a plan sits in the workspace (offsets 256-aligned).
+struct ScratchLayout {
+    uint64_t rows, tiles, wins, tile_chunk, end;
+};
+
+static ScratchLayout scratch_layout(const ii_plan_t* p) {
+    auto up = [](uint64_t x) { return (x + 255) & ~255ull; };
+    ScratchLayout l;
+    l.rows = 0;
+    l.tiles = up(p->seg_len.size() * sizeof(SegDev));
+    l.wins = up(l.tiles + p->tiles.size() * sizeof(TileDev));
+    l.tile_chunk = up(l.wins + p->tile_win.size() * sizeof(TileWin));
+    l.end = l.tile_chunk + p->tile_chunk.size() * sizeof(uint32_t);
+    return l;
+}
+
+static int run_device_noalloc(ii_plan_t* p, const uint8_t* image, const uint64_t* dst,
+                              hipStream_t stream) {
+    // destination checks into the plan's own buffer (its capacity is the
+    // table's size, so nothing is allocated)
+    int rc = dst_ranges(p, dst, &p->na_ranges);
+    if (rc) return rc;
+    rc = check_reach(p->na_ranges);
+    if (rc) return rc;
+    if (p->tiles.empty()) return II_OK;  // nothing to move
+    const uint64_t ib = reinterpret_cast<uint64_t>(image);
+    if (!accessible(ib + p->lo, ib + p->hi))
+        return fail(II_EINVAL, "the image's span [%#llx, %#llx) is not memory the device can "
+                    "read: not inside one device allocation or one pinned host allocation",
+                    (unsigned long long)(ib + p->lo), (unsigned long long)(ib + p->hi));
+    rc = check_image(p, dst, ib + p->lo, ib + p->hi);
+    if (rc) return rc;
+    uint8_t* ws = nullptr;
+    rc = scratch_ptr(&ws);
+    if (rc) return rc;
+    const ScratchLayout l = scratch_layout(p);
+    const size_t S = p->seg_len.size();
+    for (size_t i = 0; i < S; ++i)
+        p->na_rows[i] = SegDev{p->seg_off[i], p->seg_len[i], dst[p->seg_tensor[i]] + p->seg_toff[i]};
+    // pageable sources: each copy returns once its bytes are staged, so the
+    // plan's buffers may be rewritten by the next call
+    if (S) II_HIP(h2d(ws + l.rows, p->na_rows.data(), S * sizeof(SegDev), stream));
+    II_HIP(h2d(ws + l.tiles, p->tiles.data(), p->tiles.size() * sizeof(TileDev), stream));
+    if (!p->tile_win.empty())
+        II_HIP(h2d(ws + l.wins, p->tile_win.data(), p->tile_win.size() * sizeof(TileWin), stream));
+    if (!p->tile_chunk.empty())
+        II_HIP(h2d(ws + l.tile_chunk, p->tile_chunk.data(),
+                   p->tile_chunk.size() * sizeof(uint32_t), stream));
+    const uint64_t last_len = p->chunk_len(p->num_chunks - 1);
+    II_HIP(launch_injected()
+               ? hipErrorLaunchFailure
+               : launch_scatter_image(
+                     image + p->lo, reinterpret_cast<const TileDev*>(ws + l.tiles),
+                     p->tile_win.empty() ? nullptr : reinterpret_cast<const TileWin*>(ws + l.wins),
+                     p->tile_chunk.empty() ? nullptr
+                                           : reinterpret_cast<const uint32_t*>(ws + l.tile_chunk),
+                     p->tiles.size(), (uint32_t)p->num_chunks, p->tiles_per_chunk,
+                     reinterpret_cast<const SegDev*>(ws + l.rows), p->chunk_bytes, last_len,
+                     p->tile_bytes, stream));
+    return II_OK;
+}
+
 // The naive per-tensor pipeline of Sec. 4.2 ("Naive CFA Model"), kept as the
 // comparison path for the merged loader: tensors in table order, one
 // host-to-device copy per tensor (pieces of at most one slot for tensors
@@ -908,6 +1005,29 @@ extern "C" int ii_load_device(ii_plan_t* p, const void* dev_image, uint64_t imag
     inject_arm();
     int rc = run_device(p, static_cast<const uint8_t*>(dev_image),
                         reinterpret_cast<const uint64_t*>(dst_ptrs), stream);
+    return rc ? drain(p, stream, rc) : II_OK;
+}
+
+extern "C" int ii_load_device_noalloc(ii_plan_t* p, const void* dev_image, uint64_t image_bytes,
+                                      void* const* dst_ptrs, hipStream_t stream) {
+    if (!p) return fail(II_EINVAL, "ii_load_device_noalloc: plan is NULL");
+    const ScratchLayout l = scratch_layout(p);
+    if (l.end > kScratchBytes)
+        return fail(II_ESCRATCH, "ii_load_device_noalloc: the plan's tables need %llu bytes, the "
+                    "static workspace holds %llu", (unsigned long long)l.end,
+                    (unsigned long long)kScratchBytes);
+    const size_t n = p->nbytes.size();
+    if (n && !dst_ptrs) return fail(II_EINVAL, "ii_load_device_noalloc: dst_ptrs is NULL");
+    if (p->num_chunks && !dev_image)
+        return fail(II_EINVAL, "ii_load_device_noalloc: dev_image is NULL");
+    if (image_bytes < p->hi)
+        return fail(II_ERANGE, "ii_load_device_noalloc: image has %llu bytes, plan needs %llu",
+                    (unsigned long long)image_bytes, (unsigned long long)p->hi);
+    BusyGuard g(p);
+    if (!g.ok) return fail(II_EBUSY, "ii_load_device_noalloc: plan in use");
+    inject_arm();
+    int rc = run_device_noalloc(p, static_cast<const uint8_t*>(dev_image),
+                                reinterpret_cast<const uint64_t*>(dst_ptrs), stream);
     return rc ? drain(p, stream, rc) : II_OK;
 }
 

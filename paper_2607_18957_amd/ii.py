@@ -42,10 +42,11 @@ except ImportError:
 
 _lib = ctypes.CDLL(LIB_PATH)
 
-OK, EINVAL, EOVERFLOW, EOVERLAP, EALIGN, ENOMEM, EARENA, EBUSY, EHIP, ERANGE, EIO = range(11)
+(OK, EINVAL, EOVERFLOW, EOVERLAP, EALIGN, ENOMEM, EARENA, EBUSY, EHIP, ERANGE, EIO,
+ ESCRATCH) = range(12)
 ERRNAMES = {0: "II_OK", 1: "II_EINVAL", 2: "II_EOVERFLOW", 3: "II_EOVERLAP", 4: "II_EALIGN",
             5: "II_ENOMEM", 6: "II_EARENA", 7: "II_EBUSY", 8: "II_EHIP", 9: "II_ERANGE",
-            10: "II_EIO"}
+            10: "II_EIO", 11: "II_ESCRATCH"}
 
 _c = ctypes
 _vp, _sz, _u32, _u64, _i32 = _c.c_void_p, _c.c_size_t, _c.c_uint32, _c.c_uint64, _c.c_int32
@@ -63,6 +64,7 @@ _sig("ii_plan", _c.c_int, _vp, _sz, _u64, _P(_vp))
 _sig("ii_plan_free", None, _vp)
 _sig("ii_load", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_load_device", _c.c_int, _vp, _vp, _u64, _vp, _vp)
+_sig("ii_load_device_noalloc", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_load_pertensor", _c.c_int, _vp, _vp, _u64, _vp, _vp)
 _sig("ii_load_file", _c.c_int, _vp, _c.c_int, _u64, _vp, _vp)
 _sig("ii_switch", _c.c_int, _vp, _vp, _vp, _u64, _vp, _u64, _vp)
@@ -398,6 +400,14 @@ def ii_load_device(plan: Plan, image, dst_ptrs, stream=None) -> None:
     _check(_lib.ii_load_device(plan.handle, ptr or None, nbytes,
                                d.ctypes.data if d.size else None, _stream(stream)),
            "ii_load_device")
+
+
+def ii_load_device_noalloc(plan: Plan, image, dst_ptrs, stream=None) -> None:
+    ptr, nbytes = _device(image)
+    d = _ptrs(dst_ptrs)
+    _check(_lib.ii_load_device_noalloc(plan.handle, ptr or None, nbytes,
+                                       d.ctypes.data if d.size else None, _stream(stream)),
+           "ii_load_device_noalloc")
 
 
 def ii_switch(plan_old: Plan, plan_new: Plan, arena, arena_bytes: int, blob, stream=None) -> None:

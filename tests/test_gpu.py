@@ -1075,6 +1075,7 @@ _INJECT_CASES = [
     ("launch", 1, "pageable"), ("launch", 9, "pageable"), ("launch", 5, "pinned"),
     ("h2d", 1, "image"), ("launch", 1, "image"),
     ("launch", 1, "switch"), ("launch", 4, "switch"), ("h2d", 6, "switch"),
+    ("h2d", 2, "noalloc"), ("launch", 1, "noalloc"),
     ("h2d", 3, "pertensor"),
 ]
 
@@ -1099,7 +1100,7 @@ def test_injected_failure(orc, monkeypatch, site, nth, mode):
     if mode == "pinned":
         pinned = ii.ii_host_alloc(blob.size)
         pinned.numpy()[:] = blob
-    image = torch.from_numpy(blob).to(DEV) if mode == "image" else None
+    image = torch.from_numpy(blob).to(DEV) if mode in ("image", "noalloc") else None
     old = synth.transformer("tiny-old", 4, 256, 1024, 256, 8192, seed=31, chunk=1 << 20)
     po = ii.ii_plan(old)
     blob_old = synth.blob(old)
@@ -1111,6 +1112,8 @@ def test_injected_failure(orc, monkeypatch, site, nth, mode):
             ii.ii_load(plan, pinned, base + off, s)
         elif mode == "image":
             ii.ii_load_device(plan, image, base + off, s)
+        elif mode == "noalloc":
+            ii.ii_load_device_noalloc(plan, image, base + off, s)
         elif mode == "pertensor":
             ii.ii_load_pertensor(plan, blob, base + off, s)
         elif mode == "switch":
