@@ -1,6 +1,7 @@
 """Host-only sanitizer builds of the planner (ASan + UBSan), the host copy
-pool (TSan) and the reachability decision of the loads (ASan + UBSan, against
-a fake memory map). Built with g++ from the library's own sources."""
+pool (TSan), the reachability decision of the loads (ASan + UBSan, against
+a fake memory map) and the per-tensor path's schedule (ASan + UBSan, carried
+out on host buffers). Built with g++ from the library's own sources."""
 from __future__ import annotations
 
 import os
@@ -13,6 +14,7 @@ INC = os.path.join(ROOT, "include")
 PLAN_BIN = os.path.join(HERE, "plan_fuzz")
 POOL_BIN = os.path.join(HERE, "pool_tsan")
 REACH_BIN = os.path.join(HERE, "reach_check")
+PERTENSOR_BIN = os.path.join(HERE, "pertensor_check")
 
 
 def build() -> None:
@@ -24,3 +26,5 @@ def build() -> None:
                                     os.path.join(HERE, "pool_tsan.cpp")])
     subprocess.check_call(common + ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
                                     "-o", REACH_BIN, os.path.join(HERE, "reach_check.cpp")])
+    subprocess.check_call(common + ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                                    "-o", PERTENSOR_BIN, os.path.join(HERE, "pertensor_check.cpp")])

@@ -50,3 +50,20 @@ def test_reachability_decision():
     r = subprocess.run([_bin(sanitize.REACH_BIN)], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert r.stdout.strip() == "OK"
+
+
+def test_pertensor_schedule():
+    """The per-tensor path's host schedule (pertensor.h), which names every
+    staging copy and host-to-device copy of ii_load_pertensor from a pageable
+    blob: on the 100,000-tensor stress table with 16 MiB slots at depth 3,
+    on slots smaller than the tensors and on 3,000 random tables (empty
+    tensors, rows at a stride), every staging copy stays inside its slot and
+    inside one row of its tensor, every device copy inside its slot and its
+    tensor and only over bytes staged in the current fill of the slot, slots
+    are handed over round robin, and carried out on host memory the
+    destinations equal the tensors read straight from the blob."""
+    r = subprocess.run([_bin(sanitize.PERTENSOR_BIN)], capture_output=True, text=True,
+                       timeout=600)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.startswith("OK"), r.stdout
+    assert int(r.stdout.split("copies=")[1]) >= 100_000
