@@ -46,7 +46,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "effective weight-load GB/s (and tensors/s) at 1 GPU; % of H2D and HBM peak"
 HBM_PEAK_GBPS = 8000.0
-KERNEL = "scatter_image"
+KERNEL = "scatter_layout"
 KERNEL_SOURCES = ["paper_2607_18957_amd/csrc/scatter.hip",
                   "paper_2607_18957_amd/csrc/scatter_math.h",
                   "paper_2607_18957_amd/csrc/scatter_types.h"]
@@ -65,16 +65,29 @@ def kernel_source_hash() -> str:
 
 
 def table_bytes(plan) -> int:
-    """Bytes of plan tables one image launch reads: a 16-byte segment row per
-    segment and an 8-byte segment range per tile; for a table with gaps
-    between its segments also an 8-byte window and a 4-byte chunk index per
-    tile."""
-    _, clen, _ = plan.chunks()
-    gaps = not np.array_equal(plan.packing()["chunk_len"], clen)
-    return plan.num_segments * 16 + len(plan.tiles()["first"]) * (8 + (12 if gaps else 0))
+    """Bytes of plan tables one image launch reads: a 32-byte layout row per
+    segment and an 8-byte segment range per layout tile, plus a 4-byte
+    window index per tile when some window of the layout holds only
+    padding."""
+    lt = plan.layout_tiles()
+    g = len(lt["first"])
+    sparse = not np.array_equal(lt["window"], np.arange(g, dtype=np.uint32))
+    return plan.num_segments * 32 + g * (8 + (4 if sparse else 0))
 
 
-def h2d_peak(torch, dev, chunk_bytes: int) -> dict:
+def h2d_peak(chunk_bytes: int) -> dict:
+    """The pinned host -> device copy peak, measured in a child process: the
+    streams it creates there do not take hardware queues from this process,
+    whose ring lanes then each get one (a process gets four by default)."""
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.abspath(__file__), "--h2d-peak", str(chunk_bytes)],
+                       capture_output=True, text=True, timeout=300)
+    if r.returncode != 0:
+        raise RuntimeError(f"H2D peak measurement failed:\n{r.stderr[-2000:]}")
+    return json.loads(r.stdout.strip().splitlines()[-1])
+
+
+def _h2d_peak_here(torch, dev, chunk_bytes: int) -> dict:
     """Pinned host -> device hipMemcpyAsync bandwidth: sizes {chunk, 1 GiB} x
     {1, 2} streams, 10 repetitions each; best median wins."""
     big = 1 << 30
@@ -305,7 +318,7 @@ def all_configs(torch, dev, ii, synth) -> dict:
     scatter kernel from a resident image (HIP events), end to end from a
     pageable and a pinned blob, and the CPU oracle on one core beside them."""
     stream = torch.cuda.current_stream(dev)
-    h2d = h2d_peak(torch, dev, 64 << 20)
+    h2d = h2d_peak(64 << 20)
     out = {"h2d_peak_GBps": h2d["GBps"], "hbm_peak_GBps": HBM_PEAK_GBPS, "configs": {}}
 
     def kernel_ms(plan, image, dst, reps):
@@ -345,6 +358,7 @@ def all_configs(torch, dev, ii, synth) -> dict:
         for rep in range(4):
             ii.ii_load(po, ob, arena.data_ptr() + ooff, stream)
             torch.cuda.synchronize(dev)
+            po.release()  # the old plan's ring (its lanes) is not needed by the switch
             t1 = time.perf_counter()
             ii.ii_switch(po, pn, arena, po.arena_bytes, nbl, stream)
             torch.cuda.synchronize(dev)
@@ -390,7 +404,7 @@ def all_configs(torch, dev, ii, synth) -> dict:
         image = torch.from_numpy(blob).to(dev)
         ms = kernel_ms(plan, image, dst, 20)
         alg = 2 * plan.payload_bytes + table_bytes(plan)
-        row["kernel"] = {"name": "scatter_image_gaps", "ms": ms, "GBps": alg / (ms * 1e-3) / 1e9,
+        row["kernel"] = {"name": KERNEL, "ms": ms, "GBps": alg / (ms * 1e-3) / 1e9,
                          "frac_of_hbm_peak": alg / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS}
         out["configs"]["C1-TP1of4"] = row
         log(f"C1-TP1of4: pageable {row['pageable']['GBps']:.1f}, pinned "
@@ -544,13 +558,13 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
                      f"{float(r['MinNs']):>12.0f}{float(r['MaxNs']):>12.0f}"
                      f"{float(r['Percentage']):>8.2f}")
     durs = _trace_durations(os.path.join(trace_dir, "run_kernel_trace.csv"))
-    img = [v for k, v in durs.items() if k[0] == "ii::scatter_image"]
+    img = [v for k, v in durs.items() if k[0] == "ii::" + KERNEL]
     full_grid = -(-cfg["chunk_bytes"] // 4096) * 128
     slot_full = durs.get(("ii::scatter_slot", full_grid), [])
     lines.append("")
     if img:
         d = np.array(img[0]) / 1e6
-        lines += [f"scatter_image (resident image, one dispatch per load): {d.size} dispatches, "
+        lines += [f"{KERNEL} (resident image, one dispatch per load): {d.size} dispatches, "
                   f"mean {d.mean():.4f} ms, median {np.median(d):.4f} ms (kernel trace)",
                   f"  bench.py HIP-event mean of its timed launches in the same run: "
                   f"{roof['kernel_ms']:.4f} ms",
@@ -571,7 +585,7 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
     lines += ["", f"bench line of the traced run: value {run['value']:.2f} GB/s "
               f"({100 * run['frac_of_h2d_peak']:.1f}% of the H2D peak {run['h2d_peak']['GBps']:.2f}), "
               f"roofline frac {roof['frac']:.4f}"]
-    open(os.path.join(ROOT, "profiles", f"scatter_image_{workload}_kernel_stats.txt"), "w").write(
+    open(os.path.join(ROOT, "profiles", f"{KERNEL}_{workload}_kernel_stats.txt"), "w").write(
         "\n".join(lines) + "\n")
 
     fetch = _counter_means(os.path.join(fetch_dir, "run_counter_collection.csv"), "FETCH_SIZE")
@@ -583,7 +597,7 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
     cal_kib = run["calibration_copy"]["bytes"] / 1024
     f_scale = cal_kib / fetch[cal][0]
     w_scale = cal_kib / write[cal][0]
-    out = {"kernel": "scatter_image", "workload": workload, "kernel_source_hash":
+    out = {"kernel": KERNEL, "workload": workload, "kernel_source_hash":
            kernel_source_hash(), "calibration": {
                "kernel": cal[0], "grid": cal[1], "bytes_copied": run["calibration_copy"]["bytes"],
                "fetch_kib": fetch[cal][0], "write_kib": write[cal][0],
@@ -597,14 +611,14 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
          f"calibration kernel        {cal[0]} (grid {cal[1]}), {fetch[cal][1]} dispatches",
          f"  FETCH_SIZE per dispatch {fetch[cal][0]:.1f} KiB  -> scale {f_scale:.4f}",
          f"  WRITE_SIZE per dispatch {write[cal][0]:.1f} KiB  -> scale {w_scale:.4f}"]
-    key = [k for k in fetch if k[0] == "ii::scatter_image"]
+    key = [k for k in fetch if k[0] == "ii::" + KERNEL]
     if key:
         k = key[0]
         fb, wb = fetch[k][0] * 1024 * f_scale, write[k][0] * 1024 * w_scale
         alg = roof["bytes_per_launch"]
         out.update(fetch_bytes=fb, write_bytes=wb, bytes_per_launch=fb + wb,
                    algorithmic_bytes=alg, dispatches=fetch[k][1])
-        t += [f"scatter_image             {fetch[k][1]} dispatches (grid {k[1]} work-items)",
+        t += [f"{KERNEL:<26}{fetch[k][1]} dispatches (grid {k[1]} work-items)",
               f"  FETCH_SIZE per dispatch {fetch[k][0]:.1f} KiB  -> {fb:.0f} B",
               f"  WRITE_SIZE per dispatch {write[k][0]:.1f} KiB  -> {wb:.0f} B",
               f"  measured HBM bytes per launch  {fb + wb:.0f}",
@@ -624,7 +638,7 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
               f"  measured / algorithmic         {(fb + wb) / ring['bytes_per_chunk']:.4f}"]
     t.append(f"kernel source hash        {kernel_source_hash()}")
     json.dump(out, open(traffic_file(workload), "w"), indent=1)
-    open(os.path.join(ROOT, "profiles", f"scatter_image_{workload}_counters.txt"), "w").write(
+    open(os.path.join(ROOT, "profiles", f"{KERNEL}_{workload}_counters.txt"), "w").write(
         "\n".join(t) + "\n")
     print("\n".join(lines + [""] + t))
 
@@ -643,7 +657,7 @@ SHAPES = {"tiny": "a 4-layer hidden-256 transformer", "stress": "100,000 1-D ten
 
 
 def traffic_file(workload: str) -> str:
-    return os.path.join(ROOT, "profiles", f"scatter_image_{workload}_counters.json")
+    return os.path.join(ROOT, "profiles", f"{KERNEL}_{workload}_counters.json")
 
 
 def recorded_traffic(workload: str):
@@ -687,6 +701,11 @@ def main() -> int:
     if len(sys.argv) > 1 and sys.argv[1] == "--summarize":
         summarize(*sys.argv[2:7])
         return 0
+    if len(sys.argv) > 1 and sys.argv[1] == "--h2d-peak":
+        import torch
+        dev = torch.device("cuda:0")
+        print(json.dumps(_h2d_peak_here(torch, dev, int(sys.argv[2]))), flush=True)
+        return 0
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10, help="timed loads")
@@ -722,8 +741,7 @@ def main() -> int:
         f"S={plan.num_segments} C={plan.chunk_bytes}")
     stream = torch.cuda.current_stream(dev)
 
-    h2d = h2d_peak(torch, dev, plan.chunk_bytes)
-    torch.cuda.empty_cache()
+    h2d = h2d_peak(plan.chunk_bytes)
     log(f"H2D peak {h2d['GBps']:.2f} GB/s ({h2d['variant']})")
 
     log(f"blob: {table.blob_bytes} bytes of pageable host memory")
@@ -834,11 +852,12 @@ def main() -> int:
                                f"{plan.chunk_bytes >> 20} MiB chunk into a 3-slot pinned ring, one "
                                "hipMemcpyAsync per chunk carries it over PCIe (exactly the "
                                "payload crosses the link), the scatter kernel writes it into "
-                               "the tensors of one device arena",
+                               "the tensors of one device arena; chunk k's copy and scatter run "
+                               "on lane k mod 3",
                    "tensors": table.n, "payload_bytes": payload,
                    "chunk_bytes": plan.chunk_bytes, "chunks": plan.num_chunks,
                    "segments": plan.num_segments, "dst_align": int(table.dst_align[0]),
-                   "ring_depth": 3, "host_threads": plan_host_threads(),
+                   "ring_depth": 3, "lanes": 3, "host_threads": plan_host_threads(),
                    "parallelism": "single GPU"},
         "tensors_per_s": table.n * args.steps / wall,
         "frac_of_h2d_peak": value / h2d["GBps"],

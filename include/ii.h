@@ -153,8 +153,9 @@ void ii_plan_free(ii_plan_t* plan);
  * has gaps, its run groups in one 1-D or 2-D copy each (see
  * ii_plan_copy_bytes; a chunk of many groups that is mostly gaps is still
  * gathered through the host slot).
- * Chunks holding no segment are not touched. Chunk k+1's copy overlaps
- * chunk k's scatter; a slot is
+ * Chunks holding no segment are not touched. Chunk k's copy and scatter
+ * run on lane k mod lanes (see ii_plan_set_ring), so with two or more lanes
+ * chunk k+1's copy overlaps chunk k's scatter. A slot is
  * reused only after the scatter that read it has finished (Sec. 4.2:
  * (C_i,InMem)->(C_i+1,InDisk), (C_i,InGPU)->(C_i+1,InMem),
  * (C_i,InGPU)->(T_j,Alloc), (T_j,Loaded)->(C_i,InGPU)).
@@ -217,8 +218,11 @@ int ii_load_file(ii_plan_t* plan, int fd, uint64_t file_bytes, void* const* dst_
 /*
  * ii_load_device -- the same materialisation from a blob image that is
  * already resident in device memory (for example a checkpoint image parked in
- * HBM): no staging and no host-to-device copy, every chunk is scattered
- * straight from the image by the same kernel, in one launch on `stream`.
+ * HBM): no staging and no host-to-device copy; every segment of every chunk
+ * is copied straight from the image into its tensor by one launch on
+ * `stream` (the device half of Sec. 4.2, with all chunks resident at once).
+ * The launch is cut by destination: each workgroup writes one window of
+ * tile_bytes of the plan's destination layout (see ii_plan_layout_tiles).
  *
  *   dev_image    device address of blob byte 0 (any alignment); the span
  *                [dev_image + lo, + hi) must lie inside one device allocation
@@ -241,13 +245,14 @@ int ii_load_device(ii_plan_t* plan, const void* dev_image, uint64_t image_bytes,
  * memory (code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc): the same result, arguments, ordering and errors, but
  * the call allocates nothing -- no device or pinned host memory, no events,
- * streams or plan state. The kernel's tables (a 16-byte row per segment, an
- * 8-byte segment range per tile, and for tables with gaps an 8-byte window
- * and a 4-byte chunk index per tile) are uploaded on every call, on
- * `stream`, into a static device workspace of 64 MiB that the library holds
- * on each GPU it runs on until the process ends; a plan whose tables need
- * more returns II_ESCRATCH before anything is checked or enqueued (the
- * Llama-8B-shaped table needs 31 MB, the 100,000-tensor one 3.4 MB). Calls
+ * streams or plan state. The kernel's tables (a 32-byte row per segment, an
+ * 8-byte segment range per layout tile, and when some window of the layout
+ * holds only padding a 4-byte window index per tile) are uploaded on every
+ * call, on `stream`, into a static device workspace of 64 MiB that the
+ * library holds on each GPU it runs on until the process ends; a plan whose
+ * tables need more returns II_ESCRATCH before anything is checked or
+ * enqueued (the Llama-8B-shaped table needs 31 MB, the 100,000-tensor one
+ * 5.1 MB). Calls
  * on one GPU share that workspace: two calls ordered on one stream are
  * safe, calls that overlap on different streams of one GPU race (the later
  * upload may overwrite tables an earlier kernel still reads) and must be
@@ -307,12 +312,14 @@ int ii_switch(const ii_plan_t* plan_old, ii_plan_t* plan_new, void* arena, uint6
  * or $II_RING_DEPTH); host_threads = threads that read, copy or gather
  * chunk bytes into the pinned slots (pageable blobs, files, gathered chunks;
  * 1..64; default min(8, cores) or $II_HOST_THREADS);
- * copy_streams = host-to-device copy streams the chunks alternate between
- * (1..min(2, depth); default 2 or $II_COPY_STREAMS). With 1, chunk copies run
- * strictly one after another in chunk order; with 2, the copies of chunks k
- * and k+1 may overlap, which keeps the link busy while the device maps
- * freshly pinned host pages. Errors: II_EINVAL (out of range), II_EBUSY
- * (ring already allocated).
+ * copy_streams = lanes, the streams the chunks alternate between (1..min(4,
+ * depth); default min(depth, 3) or $II_COPY_STREAMS): chunk k's host-to-device copy and
+ * then its scatter run on lane k mod copy_streams. With 1, copies and
+ * scatters alternate on one stream in chunk order; with more, the copy of
+ * one chunk overlaps the scatter of another, and a slot whose next chunk
+ * runs on another lane is handed over by an event. Each lane's first copy
+ * of a load may run before the work the caller enqueued ahead of it.
+ * Errors: II_EINVAL (out of range), II_EBUSY (ring already allocated).
  */
 int ii_plan_set_ring(ii_plan_t* plan, uint32_t depth, uint32_t host_threads,
                      uint32_t copy_streams);
@@ -332,7 +339,9 @@ int ii_check_dst(const ii_plan_t* plan, void* const* dst_ptrs);
  * ii_plan_prepare -- allocate, on the current device, what the plan's loads
  * would otherwise allocate on first use: the staging ring (pinned host slots,
  * touched page by page so the first load does not fault them in; device
- * slots; streams; host copy threads) and the plan's device tables. Optional:
+ * slots; streams; host copy threads) and the ring's device tables (the
+ * resident-image kernel's tables are allocated by the first ii_load_device
+ * that needs them). Optional:
  * a cold-starting process can call it while other initialisation runs, so
  * the first load starts moving bytes at once (Sec. 4.2 overlaps independent
  * steps of the cold start). Idempotent. Errors: II_EINVAL (NULL plan, or a
@@ -343,15 +352,17 @@ int ii_plan_prepare(ii_plan_t* plan);
 /*
  * Pipeline timeline. With tracing on (ii_plan_set_trace(plan, 1) or
  * $II_TRACE=1), every later ii_load / ii_switch on the plan records four
- * timing events per chunk k: before and after its host-to-device copy (on
- * the copy stream) and before and after its scatter (on the scatter stream).
- * ii_plan_trace waits for the last traced load to finish and writes, for
- * each chunk, the times in milliseconds since that load's first scatter-
- * stream event into arrays of num_chunks entries (NULL skips one); chunks
- * that hold no segment are not moved and get NaN. The dependency edges can be
- * read off them: copy_end[k] <= scatter_start[k], and scatter_end of the i-th
- * moved chunk <= copy_start of the (i + depth)-th. Errors: II_EINVAL (tracing
- * off or no traced load), II_EBUSY, II_EHIP.
+ * timing events per chunk k: before and after its host-to-device copy and
+ * before and after its scatter (on its lane). ii_plan_trace waits for the
+ * last traced load to finish and writes, for each chunk, the times in
+ * milliseconds since the point where that load's destination writes may
+ * begin (after the work the caller enqueued ahead of it; a copy that ran
+ * before that point has a negative time) into arrays of num_chunks entries
+ * (NULL skips one); chunks that hold no segment are not moved and get NaN.
+ * The dependency edges can be read off them: copy_end[k] <= scatter_start[k],
+ * and scatter_end of the i-th moved chunk <= copy_start of the (i +
+ * depth)-th. Errors: II_EINVAL (tracing off or no traced load), II_EBUSY,
+ * II_EHIP.
  */
 int ii_plan_set_trace(ii_plan_t* plan, int on);
 int ii_plan_trace(ii_plan_t* plan, float* copy_start, float* copy_end, float* scatter_start,
@@ -402,7 +413,8 @@ int ii_plan_chunks(const ii_plan_t* plan, uint64_t* src_begin, uint64_t* len,
  * num_segments) */
 int ii_plan_segments(const ii_plan_t* plan, uint32_t* chunk, uint32_t* chunk_off,
                      uint32_t* tensor, uint64_t* tensor_off, uint32_t* len);
-/* the kernel's work split, one workgroup per tile, tiles in chunk order:
+/* the ring's work split (the scatter of one chunk in its staging slot, or
+ * read in place), one workgroup per tile, tiles in chunk order:
  * tile g takes tile_bytes of its chunk's segment bytes (counted in segment
  * order, gaps between segments skipped; the chunk's last tile takes the
  * rest) and meets exactly the segments [first[g], last[g]). In a packed
@@ -412,6 +424,20 @@ int ii_plan_segments(const ii_plan_t* plan, uint32_t* chunk, uint32_t* chunk_off
  * *num_tiles entries; pass NULL arrays to read only the sizes. */
 int ii_plan_tiles(const ii_plan_t* plan, uint32_t* tile_bytes, uint64_t* num_tiles,
                   uint32_t* chunk, uint32_t* first, uint32_t* last, uint32_t* w0, uint32_t* w1);
+/* the resident-image kernel's work split (ii_load_device), one workgroup per
+ * tile, cut by destination: seg_order (num_segments entries) lists the
+ * segments by layout position -- dst_offset of its tensor plus its tensor
+ * offset -- and tile g takes the layout positions [window[g] * tile_bytes,
+ * (window[g] + 1) * tile_bytes) and meets exactly the segments
+ * seg_order[first[g]] .. seg_order[last[g] - 1]. Windows that hold only
+ * padding have no tile. A unit of work (one segment's piece of one 16-byte
+ * destination block) belongs to the tile whose window holds the layout
+ * position of its first byte, so each destination byte is written by
+ * exactly one workgroup whatever addresses the load passes. Arrays of
+ * *num_tiles entries (seg_order: num_segments); NULL skips a field.
+ * Errors: II_EINVAL (NULL plan). */
+int ii_plan_layout_tiles(const ii_plan_t* plan, uint64_t* num_tiles, uint32_t* seg_order,
+                         uint32_t* first, uint32_t* last, uint32_t* window);
 /* name of row i as given to ii_plan ("" if none); valid while the plan lives */
 const char* ii_plan_tensor_name(const ii_plan_t* plan, size_t i);
 

@@ -15,7 +15,7 @@
 namespace ii {
 
 constexpr uint32_t kDefaultTile = 4u << 10;  // segment bytes per workgroup (<= kMaxTile)
-constexpr uint32_t kMaxCopyStreams = 2;       // host-to-device copy streams of a ring
+constexpr uint32_t kMaxLanes = 4;             // streams a ring's chunks alternate between
 constexpr uint64_t kIoAlign = 4096;           // block alignment of direct-I/O file reads
 constexpr uint64_t kCopyAlign = 256;          // host-to-device copies start and end on these
 constexpr uint32_t kMaxDmaGroups = 2;         // most copies a pinned chunk is moved with
@@ -97,20 +97,26 @@ struct ii_plan_s {
     std::vector<uint64_t> chunk_plen;
     std::vector<uint64_t> chunk_run_begin;  // num_chunks + 1
     std::vector<uint32_t> run_off, run_poff, run_len;
-    // tiles (see TileDev), chunk by chunk
+    // ring tiles (see TileDev), chunk by chunk: what the scatter of one
+    // staged or in-place chunk runs over
     uint32_t tile_bytes = ii::kDefaultTile;
     std::vector<ii::TileDev> tiles;
     std::vector<ii::TileWin> tile_win;       // plans with gaps only
-    std::vector<uint32_t> tile_chunk;        // chunk of each tile (plans with gaps only)
     std::vector<uint64_t> chunk_tile_begin;  // num_chunks + 1
-    // ceil(chunk_bytes / tile_bytes) when no chunk has a gap between its
-    // segments (every full chunk then has that many tiles and tile g is
-    // window g % it of chunk g / it), else 0
-    uint32_t tiles_per_chunk = 0;
+    // layout tiles (the resident-image kernel): the segments in destination
+    // layout order -- lseg[j] is the j-th segment by layout position
+    // dst_offset[tensor] + tensor offset -- and tiles of tile_bytes of
+    // layout positions: tile g takes the window of layout positions
+    // [w * tile_bytes, (w + 1) * tile_bytes) with w = lwin[g] (w = g when
+    // lwin is empty: every window holds segment bytes) and the layout-order
+    // segments [ltiles[g].first, ltiles[g].last) that meet it
+    std::vector<uint32_t> lseg;
+    std::vector<ii::TileDev> ltiles;
+    std::vector<uint32_t> lwin;
     // host buffers of ii_load_device_noalloc, sized when the plan is made so
-    // that the call itself allocates nothing: the segment rows with resolved
-    // destinations, and the destination ranges its checks sort
-    std::vector<ii::SegDev> na_rows;
+    // that the call itself allocates nothing: the layout-order segment rows
+    // with resolved destinations, and the destination ranges its checks sort
+    std::vector<ii::LayoutSeg> na_rows;
     std::vector<ii::DstRange> na_ranges;
     // runtime configuration
     uint32_t ring_depth = 3;

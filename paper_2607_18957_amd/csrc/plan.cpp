@@ -337,7 +337,7 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
             p->copy_bytes += how == kPinnedInPlace ? e - b : p->chunk_plen[k];
         }
 
-        // 6. tiles: per chunk, tile_bytes of segment bytes each (packed
+        // 6. ring tiles: per chunk, tile_bytes of segment bytes each (packed
         // offsets), and -- for plans with gaps -- the same bytes as a window
         // of chunk offsets. Built segment by segment: the tiles that start
         // inside segment s begin their range at s, and every tile segment s
@@ -352,10 +352,7 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
         const uint64_t G = p->chunk_tile_begin[p->num_chunks];
         if (G > 0x7fffffffull) return fail(II_EINVAL, "ii_plan: more than 2^31 tiles");
         p->tiles.resize(G);
-        if (p->packed_distinct) {
-            p->tile_win.resize(G);
-            p->tile_chunk.resize(G);
-        }
+        if (p->packed_distinct) p->tile_win.resize(G);
         for (size_t k = 0; k < p->num_chunks; ++k) {
             const uint64_t s0 = p->chunk_seg_begin[k], s1 = p->chunk_seg_begin[k + 1];
             const uint64_t g0 = p->chunk_tile_begin[k];
@@ -377,14 +374,50 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
             for (uint64_t m = 0; m < M; ++m) {
                 const uint32_t f = td[m].first;
                 tw[m].w0 = (uint32_t)(p->seg_off[f] + (m * T - po[f]));
-                p->tile_chunk[g0 + m] = (uint32_t)k;
             }
             for (uint64_t m = 0; m + 1 < M; ++m) tw[m].w1 = tw[m + 1].w0;
             if (M) tw[M - 1].w1 = p->seg_off[s1 - 1] + p->seg_len[s1 - 1];
         }
-        // no chunk has a gap: tile m of every chunk is the window [m*T,
-        // (m+1)*T) of it, and full chunks have ceil(C / T) tiles each
-        p->tiles_per_chunk = p->packed_distinct ? 0 : (uint32_t)((C + T - 1) / T);
+
+        // 7. layout tiles: the segments in destination layout order, cut into
+        // windows of T layout positions. Layout positions grow with the table
+        // order and, inside a tensor, with the tensor offset, so a table read
+        // in table order is already sorted. The windows a segment meets are
+        // visited in increasing order; a window gets a tile the first time a
+        // segment meets it, and later segments meeting it extend the tile's
+        // range. Windows holding only padding get no tile.
+        {
+            std::vector<uint64_t> pos(S);
+            for (size_t x = 0; x < S; ++x)
+                pos[x] = p->dst_offset[p->seg_tensor[x]] + p->seg_toff[x];
+            p->lseg.resize(S);
+            for (size_t x = 0; x < S; ++x) p->lseg[x] = (uint32_t)x;
+            auto by_pos = [&pos](uint32_t a, uint32_t b) { return pos[a] < pos[b]; };
+            if (!std::is_sorted(pos.begin(), pos.end()))
+                std::sort(p->lseg.begin(), p->lseg.end(), by_pos);
+            uint64_t cur = ~0ull;  // window of the last tile made
+            for (size_t j = 0; j < S; ++j) {
+                const uint32_t x = p->lseg[j];
+                const uint64_t m0 = pos[x] / T, m1 = (pos[x] + p->seg_len[x] - 1) / T;
+                if (m1 >= (1ull << 32))
+                    return fail(II_EINVAL, "ii_plan: destination layout beyond 2^32 tiles");
+                for (uint64_t m = m0; m <= m1; ++m) {
+                    if (m != cur) {
+                        if (p->ltiles.size() >= 0x7fffffffull)
+                            return fail(II_EINVAL, "ii_plan: more than 2^31 tiles");
+                        p->ltiles.push_back(TileDev{(uint32_t)j, (uint32_t)(j + 1)});
+                        p->lwin.push_back((uint32_t)m);
+                        cur = m;
+                    } else {
+                        p->ltiles.back().last = (uint32_t)(j + 1);
+                    }
+                }
+            }
+            // windows strictly increase from window 0 or more: every window
+            // holds segment bytes exactly when the last tile is window G - 1
+            if (p->ltiles.empty() || p->lwin.back() == p->ltiles.size() - 1)
+                std::vector<uint32_t>().swap(p->lwin);
+        }
         p->na_rows.resize(S);
         p->na_ranges.reserve(n);
     } catch (const std::bad_alloc&) {
@@ -392,7 +425,9 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
     }
 
     p->ring_depth = env_u32("II_RING_DEPTH", 3, 1, 8);
-    p->copy_streams = std::min(p->ring_depth, env_u32("II_COPY_STREAMS", 2, 1, kMaxCopyStreams));
+    // lanes: as many as slots, up to 3 (with the caller's stream that is
+    // the four hardware queues a process gets by default)
+    p->copy_streams = std::min(p->ring_depth, env_u32("II_COPY_STREAMS", 3, 1, kMaxLanes));
     p->trace = env_u32("II_TRACE", 0, 0, 1) != 0;
     {
         long cores = sysconf(_SC_NPROCESSORS_ONLN);
@@ -476,6 +511,20 @@ extern "C" int ii_plan_tiles(const ii_plan_t* p, uint32_t* tile_bytes, uint64_t*
                                            : (uint32_t)std::min<uint64_t>(p->chunk_len(k),
                                                                            b + p->tile_bytes);
         }
+    return II_OK;
+}
+
+extern "C" int ii_plan_layout_tiles(const ii_plan_t* p, uint64_t* num_tiles, uint32_t* seg_order,
+                                    uint32_t* first, uint32_t* last, uint32_t* window) {
+    if (!p) return fail(II_EINVAL, "ii_plan_layout_tiles: plan is NULL");
+    const size_t G = p->ltiles.size(), S = p->lseg.size();
+    if (num_tiles) *num_tiles = G;
+    if (seg_order && S) memcpy(seg_order, p->lseg.data(), S * 4);
+    for (size_t g = 0; g < G; ++g) {
+        if (first) first[g] = p->ltiles[g].first;
+        if (last) last[g] = p->ltiles[g].last;
+        if (window) window[g] = p->lwin.empty() ? (uint32_t)g : p->lwin[g];
+    }
     return II_OK;
 }
 

@@ -45,6 +45,7 @@
 
 #include "copy_pool.h"
 #include "ii_internal.h"
+#include "pertensor.h"
 #include "reach.h"
 
 namespace ii {
@@ -52,10 +53,9 @@ namespace ii {
 hipError_t launch_scatter_slot(const uint8_t* slot, const TileDev* tiles, const TileWin* wins,
                                uint32_t ntiles, const SegDev* segs, bool implicit,
                                uint32_t tile_bytes, uint64_t plen, hipStream_t stream);
-hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const TileWin* wins,
-                                const uint32_t* tile_chunk, uint64_t ntiles, uint32_t num_chunks,
-                                uint32_t per_chunk, const SegDev* segs, uint64_t chunk_bytes,
-                                uint64_t last_len, uint32_t tile_bytes, hipStream_t stream);
+hipError_t launch_scatter_layout(const uint8_t* span, const TileDev* tiles, const uint32_t* win,
+                                 uint64_t ntiles, const LayoutSeg* segs, uint32_t tile_bytes,
+                                 hipStream_t stream);
 hipError_t launch_zero(const RangeDev* ranges, uint32_t n, hipStream_t stream);
 
 #define II_HIP(call)                                                                   \
@@ -126,22 +126,31 @@ static bool launch_injected() { return injected(kSiteLaunch); }
 
 struct Runtime {
     int device = -1;
-    // device tables
+    // device tables of the ring: segment rows with chunk offsets, tiles and
+    // (plans with gaps) their windows
     SegDev* d_segs = nullptr;
     SegDev* h_segs = nullptr;  // pinned staging for d_segs uploads
     TileDev* d_tiles = nullptr;
     TileWin* d_wins = nullptr;
-    uint32_t* d_tile_chunk = nullptr;
     // segment rows with packed staging offsets (plans with packed_distinct)
     SegDev* d_psegs = nullptr;
     SegDev* h_psegs = nullptr;
-    bool tiles_ready = false, wins_ready = false, tile_chunk_ready = false;  // uploaded
-    hipEvent_t tables_idle = nullptr;   // after the last kernel that read d_segs
-    hipEvent_t upload_done = nullptr;   // after the last read of h_segs
+    bool tiles_ready = false, wins_ready = false;  // uploaded
+    // device tables of the resident-image kernel: layout-order rows, layout
+    // tiles and (layouts with padding-only windows) their windows
+    LayoutSeg* d_lsegs = nullptr;
+    LayoutSeg* h_lsegs = nullptr;  // pinned staging for d_lsegs uploads
+    TileDev* d_ltiles = nullptr;
+    uint32_t* d_lwin = nullptr;
+    bool ltiles_ready = false, lwin_ready = false;  // uploaded
+    hipEvent_t tables_idle = nullptr;   // after the last kernel that read a row table
+    hipEvent_t upload_done = nullptr;   // after the last read of h_segs / h_psegs / h_lsegs
     bool tables_used = false, uploaded = false;
-    std::vector<uint64_t> cached_dst;   // destination addresses d_segs was built for
+    std::vector<uint64_t> cached_dst;   // destination addresses of the last load
     std::vector<DstRange> cached_ranges;  // ... their ranges, sorted by address
     bool cached_valid = false;
+    // whether d_segs (and d_psegs) / d_lsegs hold rows for cached_dst
+    bool ring_rows_ok = false, layout_rows_ok = false;
     uint64_t image_b = 0, image_e = 0;  // source image range last checked against them
     // scrub ranges
     RangeDev* d_ranges = nullptr;
@@ -154,9 +163,12 @@ struct Runtime {
     std::vector<uint8_t*> hslot, dslot;
     std::vector<hipEvent_t> copy_done, scatter_done;
     std::vector<char> copy_rec, scatter_rec;
-    hipStream_t copy_s[kMaxCopyStreams] = {}, scatter_s = nullptr;
-    uint32_t ncopy = 1;
-    hipEvent_t entry = nullptr, done = nullptr;
+    std::vector<int> slot_lane;  // lane of the last scatter that read each device slot (-1: none)
+    // lanes: chunk j's copy and then its scatter run on lane j mod nlanes
+    hipStream_t lane_s[kMaxLanes] = {};
+    hipEvent_t lane_done[kMaxLanes] = {};
+    uint32_t nlanes = 1;
+    hipEvent_t entry = nullptr, go = nullptr, done = nullptr;
     CopyPool* pool = nullptr;
     // optional per-chunk timeline of the last ring load (timing events)
     std::vector<hipEvent_t> tr_cs, tr_ce, tr_ss, tr_se;
@@ -193,14 +205,19 @@ static void free_ring(Runtime* r) {
     r->scatter_done.clear();
     r->copy_rec.clear();
     r->scatter_rec.clear();
-    for (auto& c : r->copy_s)
+    r->slot_lane.clear();
+    for (auto& c : r->lane_s) {
         if (c) (void)hipStreamDestroy(c);
-    if (r->scatter_s) (void)hipStreamDestroy(r->scatter_s);
-    if (r->entry) (void)hipEventDestroy(r->entry);
-    if (r->done) (void)hipEventDestroy(r->done);
-    for (auto& c : r->copy_s) c = nullptr;
-    r->scatter_s = nullptr;
-    r->entry = r->done = nullptr;
+        c = nullptr;
+    }
+    for (auto& e : r->lane_done) {
+        if (e) (void)hipEventDestroy(e);
+        e = nullptr;
+    }
+    for (hipEvent_t* e : {&r->entry, &r->go, &r->done}) {
+        if (*e) (void)hipEventDestroy(*e);
+        *e = nullptr;
+    }
     delete r->pool;
     r->pool = nullptr;
     r->depth = 0;
@@ -212,9 +229,8 @@ static void destroy(Runtime* r) {
     (void)hipGetDevice(&cur);
     if (r->device >= 0 && cur != r->device) (void)hipSetDevice(r->device);
     // drain everything the plan may still have in flight
-    for (auto c : r->copy_s)
+    for (auto c : r->lane_s)
         if (c) (void)hipStreamSynchronize(c);
-    if (r->scatter_s) (void)hipStreamSynchronize(r->scatter_s);
     if (r->tables_idle && r->tables_used) (void)hipEventSynchronize(r->tables_idle);
     if (r->upload_done && r->uploaded) (void)hipEventSynchronize(r->upload_done);
     if (r->ranges_idle && r->ranges_used) (void)hipEventSynchronize(r->ranges_idle);
@@ -224,7 +240,10 @@ static void destroy(Runtime* r) {
     if (r->h_segs) (void)hipHostFree(r->h_segs);
     if (r->d_tiles) (void)hipFree(r->d_tiles);
     if (r->d_wins) (void)hipFree(r->d_wins);
-    if (r->d_tile_chunk) (void)hipFree(r->d_tile_chunk);
+    if (r->d_lsegs) (void)hipFree(r->d_lsegs);
+    if (r->h_lsegs) (void)hipHostFree(r->h_lsegs);
+    if (r->d_ltiles) (void)hipFree(r->d_ltiles);
+    if (r->d_lwin) (void)hipFree(r->d_lwin);
     if (r->d_psegs) (void)hipFree(r->d_psegs);
     if (r->h_psegs) (void)hipHostFree(r->h_psegs);
     if (r->d_ranges) (void)hipFree(r->d_ranges);
@@ -242,7 +261,10 @@ void runtime_destroy(ii_plan_t* p) {
     p->rt = nullptr;
 }
 
-static int ensure_tables(ii_plan_t* p) {
+// The plan's device state, its events and its list of chunks that hold
+// segments (the tables of either path come from ensure_ring_tables and
+// ensure_layout_tables).
+static int ensure_state(ii_plan_t* p) {
     int dev = -1;
     II_HIP(hipGetDevice(&dev));
     if (!p->rt) {
@@ -262,10 +284,16 @@ static int ensure_tables(ii_plan_t* p) {
             if (p->chunk_seg_begin[k] < p->chunk_seg_begin[k + 1]) r->live.push_back((uint32_t)k);
         r->live_ready = true;
     }
-    // Each table is allocated and uploaded separately, and counted as ready
-    // only once its upload returned: a call that failed half-way (one
-    // allocation made, the next refused) leaves nothing a later load would
-    // take for initialised.
+    return II_OK;
+}
+
+// Each table is allocated and uploaded separately, and counted as ready only
+// once its upload returned: a call that failed half-way (one allocation
+// made, the next refused) leaves nothing a later load would take for
+// initialised. The tile tables never change after they are uploaded
+// (synchronously, once per plan).
+static int ensure_ring_tables(ii_plan_t* p) {
+    Runtime* r = p->rt;
     const size_t S = p->seg_len.size();
     if (S && !r->d_segs) II_HIP(dev_alloc(&r->d_segs, S * sizeof(SegDev)));
     if (S && !r->h_segs) II_HIP(host_alloc(&r->h_segs, S * sizeof(SegDev)));
@@ -273,23 +301,33 @@ static int ensure_tables(ii_plan_t* p) {
         if (!r->d_psegs) II_HIP(dev_alloc(&r->d_psegs, S * sizeof(SegDev)));
         if (!r->h_psegs) II_HIP(host_alloc(&r->h_psegs, S * sizeof(SegDev)));
     }
-    // synchronous, once per plan: the tile tables never change afterwards
     if (!p->tile_win.empty() && !r->wins_ready) {
         if (!r->d_wins) II_HIP(dev_alloc(&r->d_wins, p->tile_win.size() * sizeof(TileWin)));
         II_HIP(h2d_sync(r->d_wins, p->tile_win.data(), p->tile_win.size() * sizeof(TileWin)));
         r->wins_ready = true;
     }
-    if (!p->tile_chunk.empty() && !r->tile_chunk_ready) {
-        if (!r->d_tile_chunk)
-            II_HIP(dev_alloc(&r->d_tile_chunk, p->tile_chunk.size() * sizeof(uint32_t)));
-        II_HIP(h2d_sync(r->d_tile_chunk, p->tile_chunk.data(),
-                        p->tile_chunk.size() * sizeof(uint32_t)));
-        r->tile_chunk_ready = true;
-    }
     if (!p->tiles.empty() && !r->tiles_ready) {
         if (!r->d_tiles) II_HIP(dev_alloc(&r->d_tiles, p->tiles.size() * sizeof(TileDev)));
         II_HIP(h2d_sync(r->d_tiles, p->tiles.data(), p->tiles.size() * sizeof(TileDev)));
         r->tiles_ready = true;
+    }
+    return II_OK;
+}
+
+static int ensure_layout_tables(ii_plan_t* p) {
+    Runtime* r = p->rt;
+    const size_t S = p->seg_len.size();
+    if (S && !r->d_lsegs) II_HIP(dev_alloc(&r->d_lsegs, S * sizeof(LayoutSeg)));
+    if (S && !r->h_lsegs) II_HIP(host_alloc(&r->h_lsegs, S * sizeof(LayoutSeg)));
+    if (!p->lwin.empty() && !r->lwin_ready) {
+        if (!r->d_lwin) II_HIP(dev_alloc(&r->d_lwin, p->lwin.size() * sizeof(uint32_t)));
+        II_HIP(h2d_sync(r->d_lwin, p->lwin.data(), p->lwin.size() * sizeof(uint32_t)));
+        r->lwin_ready = true;
+    }
+    if (!p->ltiles.empty() && !r->ltiles_ready) {
+        if (!r->d_ltiles) II_HIP(dev_alloc(&r->d_ltiles, p->ltiles.size() * sizeof(TileDev)));
+        II_HIP(h2d_sync(r->d_ltiles, p->ltiles.data(), p->ltiles.size() * sizeof(TileDev)));
+        r->ltiles_ready = true;
     }
     return II_OK;
 }
@@ -304,6 +342,7 @@ static int ensure_ring(ii_plan_t* p) {
     r->scatter_done.assign(D, nullptr);
     r->copy_rec.assign(D, 0);
     r->scatter_rec.assign(D, 0);
+    r->slot_lane.assign(D, -1);
     r->depth = D;  // free_ring() cleans up partial state on failure below
     int rc = II_OK;
     auto bail = [&](int code) {
@@ -322,11 +361,13 @@ static int ensure_ring(ii_plan_t* p) {
         II_RING(hipEventCreateWithFlags(&r->copy_done[i], hipEventDisableTiming));
         II_RING(hipEventCreateWithFlags(&r->scatter_done[i], hipEventDisableTiming));
     }
-    r->ncopy = p->copy_streams;
-    for (uint32_t i = 0; i < r->ncopy; ++i)
-        II_RING(hipStreamCreateWithFlags(&r->copy_s[i], hipStreamNonBlocking));
-    II_RING(hipStreamCreateWithFlags(&r->scatter_s, hipStreamNonBlocking));
+    r->nlanes = p->copy_streams;
+    for (uint32_t i = 0; i < r->nlanes; ++i) {
+        II_RING(hipStreamCreateWithFlags(&r->lane_s[i], hipStreamNonBlocking));
+        II_RING(hipEventCreateWithFlags(&r->lane_done[i], hipEventDisableTiming));
+    }
     II_RING(hipEventCreateWithFlags(&r->entry, hipEventDisableTiming));
+    II_RING(hipEventCreateWithFlags(&r->go, hipEventDisableTiming));
     II_RING(hipEventCreateWithFlags(&r->done, hipEventDisableTiming));
 #undef II_RING
     r->pool = new (std::nothrow) CopyPool(p->host_threads);
@@ -434,14 +475,17 @@ static int check_image(const ii_plan_t* p, const uint64_t* dst, uint64_t b, uint
     return II_OK;
 }
 
-// Make d_segs hold this load's resolved destination addresses. The upload is
-// ordered on `s`, after every kernel that read the previous table. The
+// Make the row tables a load reads (`which`: the ring's, the resident-image
+// kernel's) hold its resolved destination addresses. The upload is ordered
+// on `s`, after every kernel that read the previous tables. The
 // checks that depend only on the addresses (present, aligned, disjoint) run
 // for destinations not seen before; reachability -- whether the memory is
 // still allocated -- is checked on every call, one query per allocation,
 // since a freed arena may be passed again at the same addresses.
+enum RowTables { kRingRows = 1, kLayoutRows = 2 };
+
 static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, uint64_t image_b,
-                            uint64_t image_e) {
+                            uint64_t image_e, int which) {
     Runtime* r = p->rt;
     const size_t n = p->nbytes.size(), S = p->seg_len.size();
     const bool same = r->cached_valid && r->cached_dst.size() == n &&
@@ -467,29 +511,49 @@ static int prepare_segments(ii_plan_t* p, const uint64_t* dst, hipStream_t s, ui
             if (rc) return rc;
         }
     }
-    if (same) {
-        r->image_b = image_b;
-        r->image_e = image_e;
-        return II_OK;
+    if (!same) {
+        // new destinations: every row table is stale until rebuilt for them
+        r->ring_rows_ok = r->layout_rows_ok = false;
+        try {
+            r->cached_dst.assign(dst, dst + n);
+        } catch (const std::bad_alloc&) {
+            return fail(II_ENOMEM, "destination check: host allocation failed");
+        }
+        r->cached_valid = true;
     }
-    if (S) {
-        if (r->uploaded) II_HIP(hipEventSynchronize(r->upload_done));  // h_segs free again
+    r->image_b = image_b;
+    r->image_e = image_e;
+    const bool ring = S && (which & kRingRows) && !r->ring_rows_ok;
+    const bool layout = S && (which & kLayoutRows) && !r->layout_rows_ok;
+    if (!ring && !layout) return II_OK;
+    if (r->uploaded) II_HIP(hipEventSynchronize(r->upload_done));  // staging buffers free again
+    if (ring) {
         for (size_t i = 0; i < S; ++i)
             r->h_segs[i] = SegDev{p->seg_off[i], p->seg_len[i],
                                   dst[p->seg_tensor[i]] + p->seg_toff[i]};
         if (p->packed_distinct)
             for (size_t i = 0; i < S; ++i)
                 r->h_psegs[i] = SegDev{p->seg_poff[i], p->seg_len[i], r->h_segs[i].dst};
-        if (r->tables_used) II_HIP(hipStreamWaitEvent(s, r->tables_idle, 0));
+    }
+    if (layout) {
+        const uint64_t C = p->chunk_bytes;
+        for (size_t j = 0; j < S; ++j) {
+            const uint32_t x = p->lseg[j], t = p->seg_tensor[x];
+            r->h_lsegs[j] = LayoutSeg{(uint64_t)p->seg_chunk[x] * C + p->seg_off[x],
+                                      dst[t] + p->seg_toff[x], p->dst_offset[t] + p->seg_toff[x],
+                                      p->seg_len[x], 0};
+        }
+    }
+    if (r->tables_used) II_HIP(hipStreamWaitEvent(s, r->tables_idle, 0));
+    if (ring) {
         II_HIP(h2d(r->d_segs, r->h_segs, S * sizeof(SegDev), s));
         if (p->packed_distinct) II_HIP(h2d(r->d_psegs, r->h_psegs, S * sizeof(SegDev), s));
-        II_HIP(hipEventRecord(r->upload_done, s));
-        r->uploaded = true;
     }
-    r->cached_dst.assign(dst, dst + n);
-    r->cached_valid = true;
-    r->image_b = image_b;
-    r->image_e = image_e;
+    if (layout) II_HIP(h2d(r->d_lsegs, r->h_lsegs, S * sizeof(LayoutSeg), s));
+    II_HIP(hipEventRecord(r->upload_done, s));
+    r->uploaded = true;
+    if (ring) r->ring_rows_ok = true;
+    if (layout) r->layout_rows_ok = true;
     return II_OK;
 }
 
@@ -544,11 +608,9 @@ static bool is_device_ptr(const void* ptr) {
 // Drain the plan's streams after an error so that nothing enqueued by the
 // failed call still touches caller memory.
 static int drain(ii_plan_t* p, hipStream_t caller, int rc) {
-    if (p->rt) {
-        for (auto c : p->rt->copy_s)
+    if (p->rt)
+        for (auto c : p->rt->lane_s)
             if (c) (void)hipStreamSynchronize(c);
-        if (p->rt->scatter_s) (void)hipStreamSynchronize(p->rt->scatter_s);
-    }
     (void)hipStreamSynchronize(caller);
     (void)hipGetLastError();
     return rc;
@@ -582,7 +644,9 @@ struct Source {
 
 static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStream_t stream,
                     const std::vector<RangeDev>* scrub) {
-    int rc = ensure_tables(p);
+    int rc = ensure_state(p);
+    if (rc) return rc;
+    rc = ensure_ring_tables(p);
     if (rc) return rc;
     rc = ensure_ring(p);
     if (rc) return rc;
@@ -598,16 +662,35 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         if (rc) return rc;
         r->tr_chunks = 0;
     }
-    // entry edge: destination writes start after the caller's prior work
-    II_HIP(hipEventRecord(r->entry, stream));
-    II_HIP(hipStreamWaitEvent(r->scatter_s, r->entry, 0));
-    if (trace) II_HIP(hipEventRecord(r->tr_t0, r->scatter_s));
-    rc = prepare_segments(p, dst, r->scatter_s, 0, 0);
+    // Destination checks; new destinations' rows are uploaded on lane 0,
+    // ahead of every scatter of this load.
+    hipStream_t lane0 = r->lane_s[0];
+    rc = prepare_segments(p, dst, lane0, 0, 0, kRingRows);
     if (rc) return rc;
-    if (scrub) {
-        rc = launch_scrub(p, *scrub, r->scatter_s);
-        if (rc) return rc;
-    }
+    // Entry edge: destination writes start after the caller's prior work.
+    // Copies into the ring need no such wait (they write only the plan's own
+    // slots), so each lane's first copy may run while that work is still
+    // pending; the lane waits before its first scatter. Lane 0 opens first
+    // (chunk 0 is its): it waits for the entry event, runs the scrub of a
+    // switch, and records `go`; every other lane waits for `go`.
+    II_HIP(hipEventRecord(r->entry, stream));
+    uint32_t opened = 0;  // bit l: lane l's scatters are ordered after `go`
+    auto open_lane = [&](uint32_t l) -> int {
+        if (opened & (1u << l)) return II_OK;
+        if (!(opened & 1u)) {
+            II_HIP(hipStreamWaitEvent(lane0, r->entry, 0));
+            if (trace) II_HIP(hipEventRecord(r->tr_t0, lane0));
+            if (scrub) {
+                const int e = launch_scrub(p, *scrub, lane0);
+                if (e) return e;
+            }
+            II_HIP(hipEventRecord(r->go, lane0));
+            opened |= 1u;
+        }
+        if (l) II_HIP(hipStreamWaitEvent(r->lane_s[l], r->go, 0));
+        opened |= 1u << l;
+        return II_OK;
+    };
 
     const uint32_t D = r->depth;
     const uint64_t C = p->chunk_bytes;
@@ -653,6 +736,10 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         const uint64_t len = packed ? p->chunk_plen[k] : u1 - u0;
         const uint64_t doff = packed ? 0 : u0;
         const uint8_t* from = blob ? blob + at : nullptr;
+        // InMem -> InGPU on lane l, once the device slot's previous scatter
+        // is done (implied when that scatter ran on this lane)
+        const uint32_t l = j % r->nlanes;
+        hipStream_t cs = r->lane_s[l];
         if (staged) {
             // InDisk -> InMem: the pinned slot is free once its last copy finished
             if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
@@ -686,9 +773,8 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
             }
             from = stage;
         }
-        // InMem -> InGPU, once the device slot's previous scatter is done
-        hipStream_t cs = r->copy_s[j % r->ncopy];
-        if (r->scatter_rec[slot]) II_HIP(hipStreamWaitEvent(cs, r->scatter_done[slot], 0));
+        if (r->scatter_rec[slot] && r->slot_lane[slot] != (int)l)
+            II_HIP(hipStreamWaitEvent(cs, r->scatter_done[slot], 0));
         if (trace) II_HIP(hipEventRecord(r->tr_cs[j], cs));
         if (pinned && how == kPinnedGroups) {
             // one copy per run group straight from the pinned blob into the
@@ -708,9 +794,11 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
         II_HIP(hipEventRecord(r->copy_done[slot], cs));
         if (trace) II_HIP(hipEventRecord(r->tr_ce[j], cs));
         r->copy_rec[slot] = 1;
-        // InGPU -> tensors Loaded, then the slot is released
-        II_HIP(hipStreamWaitEvent(r->scatter_s, r->copy_done[slot], 0));
-        if (trace) II_HIP(hipEventRecord(r->tr_ss[j], r->scatter_s));
+        // InGPU -> tensors Loaded on the same lane, after the copy; then the
+        // slot is released
+        rc = open_lane(l);
+        if (rc) return rc;
+        if (trace) II_HIP(hipEventRecord(r->tr_ss[j], cs));
         const uint64_t t0 = p->chunk_tile_begin[k], nt = p->chunk_tile_begin[k + 1] - t0;
         // windows are implicit in a packed slot and in a plan without gaps
         // (which keeps no window table)
@@ -719,34 +807,45 @@ static int run_ring(ii_plan_t* p, const Source& src, const uint64_t* dst, hipStr
                                  : launch_scatter_slot(r->dslot[slot], r->d_tiles + t0,
                                    implicit ? nullptr : r->d_wins + t0, (uint32_t)nt,
                                    packed ? r->d_psegs : r->d_segs, implicit, p->tile_bytes,
-                                   p->chunk_plen[k], r->scatter_s));
-        II_HIP(hipEventRecord(r->scatter_done[slot], r->scatter_s));
-        if (trace) II_HIP(hipEventRecord(r->tr_se[j], r->scatter_s));
+                                   p->chunk_plen[k], cs));
+        II_HIP(hipEventRecord(r->scatter_done[slot], cs));
+        if (trace) II_HIP(hipEventRecord(r->tr_se[j], cs));
         r->scatter_rec[slot] = 1;
+        r->slot_lane[slot] = (int)l;
     }
     if (trace) {
         r->tr_id = live;
         r->tr_chunks = L;
     }
-    II_HIP(hipEventRecord(r->tables_idle, r->scatter_s));
+    // a load without chunks still waits for the entry edge and runs the scrub
+    rc = open_lane(0);
+    if (rc) return rc;
+    // completion: lane 0 joins the other lanes, the caller's stream waits
+    for (uint32_t x = 1; x < r->nlanes; ++x)
+        if (opened & (1u << x)) {
+            II_HIP(hipEventRecord(r->lane_done[x], r->lane_s[x]));
+            II_HIP(hipStreamWaitEvent(lane0, r->lane_done[x], 0));
+        }
+    II_HIP(hipEventRecord(r->tables_idle, lane0));
     r->tables_used = true;
-    II_HIP(hipEventRecord(r->done, r->scatter_s));
+    II_HIP(hipEventRecord(r->done, lane0));
     II_HIP(hipStreamWaitEvent(stream, r->done, 0));
     return II_OK;
 }
 
 static int run_device(ii_plan_t* p, const uint8_t* image, const uint64_t* dst, hipStream_t stream) {
-    int rc = ensure_tables(p);
+    int rc = ensure_state(p);
+    if (rc) return rc;
+    rc = ensure_layout_tables(p);
     if (rc) return rc;
     Runtime* r = p->rt;
     const uint64_t ib = reinterpret_cast<uint64_t>(image);
-    rc = prepare_segments(p, dst, stream, ib + p->lo, ib + p->hi);
+    rc = prepare_segments(p, dst, stream, ib + p->lo, ib + p->hi, kLayoutRows);
     if (rc) return rc;
-    const uint64_t last_len = p->num_chunks ? p->chunk_len(p->num_chunks - 1) : 0;
     II_HIP(launch_injected() ? hipErrorLaunchFailure
-                             : launch_scatter_image(image + p->lo, r->d_tiles, r->d_wins, r->d_tile_chunk,
-                                p->tiles.size(), (uint32_t)p->num_chunks, p->tiles_per_chunk,
-                                r->d_segs, p->chunk_bytes, last_len, p->tile_bytes, stream));
+                             : launch_scatter_layout(image + p->lo, r->d_ltiles, r->d_lwin,
+                                                     p->ltiles.size(), r->d_lsegs, p->tile_bytes,
+                                                     stream));
     II_HIP(hipEventRecord(r->tables_idle, stream));
     r->tables_used = true;
     return II_OK;
@@ -788,17 +887,16 @@ static int scratch_ptr(uint8_t** out) {
 
 // Where each table of a plan sits in the workspace (offsets 256-aligned).
 struct ScratchLayout {
-    uint64_t rows, tiles, wins, tile_chunk, end;
+    uint64_t rows, tiles, win, end;
 };
 
 static ScratchLayout scratch_layout(const ii_plan_t* p) {
     auto up = [](uint64_t x) { return (x + 255) & ~255ull; };
     ScratchLayout l;
     l.rows = 0;
-    l.tiles = up(p->seg_len.size() * sizeof(SegDev));
-    l.wins = up(l.tiles + p->tiles.size() * sizeof(TileDev));
-    l.tile_chunk = up(l.wins + p->tile_win.size() * sizeof(TileWin));
-    l.end = l.tile_chunk + p->tile_chunk.size() * sizeof(uint32_t);
+    l.tiles = up(p->lseg.size() * sizeof(LayoutSeg));
+    l.win = up(l.tiles + p->ltiles.size() * sizeof(TileDev));
+    l.end = l.win + p->lwin.size() * sizeof(uint32_t);
     return l;
 }
 
@@ -810,7 +908,7 @@ static int run_device_noalloc(ii_plan_t* p, const uint8_t* image, const uint64_t
     if (rc) return rc;
     rc = check_reach(p->na_ranges);
     if (rc) return rc;
-    if (p->tiles.empty()) return II_OK;  // nothing to move
+    if (p->ltiles.empty()) return II_OK;  // nothing to move
     const uint64_t ib = reinterpret_cast<uint64_t>(image);
     if (!accessible(ib + p->lo, ib + p->hi))
         return fail(II_EINVAL, "the image's span [%#llx, %#llx) is not memory the device can "
@@ -822,28 +920,26 @@ static int run_device_noalloc(ii_plan_t* p, const uint8_t* image, const uint64_t
     rc = scratch_ptr(&ws);
     if (rc) return rc;
     const ScratchLayout l = scratch_layout(p);
-    const size_t S = p->seg_len.size();
-    for (size_t i = 0; i < S; ++i)
-        p->na_rows[i] = SegDev{p->seg_off[i], p->seg_len[i], dst[p->seg_tensor[i]] + p->seg_toff[i]};
+    const size_t S = p->lseg.size();
+    const uint64_t C = p->chunk_bytes;
+    for (size_t j = 0; j < S; ++j) {
+        const uint32_t x = p->lseg[j], t = p->seg_tensor[x];
+        p->na_rows[j] = LayoutSeg{(uint64_t)p->seg_chunk[x] * C + p->seg_off[x],
+                                  dst[t] + p->seg_toff[x], p->dst_offset[t] + p->seg_toff[x],
+                                  p->seg_len[x], 0};
+    }
     // pageable sources: each copy returns once its bytes are staged, so the
     // plan's buffers may be rewritten by the next call
-    if (S) II_HIP(h2d(ws + l.rows, p->na_rows.data(), S * sizeof(SegDev), stream));
-    II_HIP(h2d(ws + l.tiles, p->tiles.data(), p->tiles.size() * sizeof(TileDev), stream));
-    if (!p->tile_win.empty())
-        II_HIP(h2d(ws + l.wins, p->tile_win.data(), p->tile_win.size() * sizeof(TileWin), stream));
-    if (!p->tile_chunk.empty())
-        II_HIP(h2d(ws + l.tile_chunk, p->tile_chunk.data(),
-                   p->tile_chunk.size() * sizeof(uint32_t), stream));
-    const uint64_t last_len = p->chunk_len(p->num_chunks - 1);
+    if (S) II_HIP(h2d(ws + l.rows, p->na_rows.data(), S * sizeof(LayoutSeg), stream));
+    II_HIP(h2d(ws + l.tiles, p->ltiles.data(), p->ltiles.size() * sizeof(TileDev), stream));
+    if (!p->lwin.empty())
+        II_HIP(h2d(ws + l.win, p->lwin.data(), p->lwin.size() * sizeof(uint32_t), stream));
     II_HIP(launch_injected()
                ? hipErrorLaunchFailure
-               : launch_scatter_image(
+               : launch_scatter_layout(
                      image + p->lo, reinterpret_cast<const TileDev*>(ws + l.tiles),
-                     p->tile_win.empty() ? nullptr : reinterpret_cast<const TileWin*>(ws + l.wins),
-                     p->tile_chunk.empty() ? nullptr
-                                           : reinterpret_cast<const uint32_t*>(ws + l.tile_chunk),
-                     p->tiles.size(), (uint32_t)p->num_chunks, p->tiles_per_chunk,
-                     reinterpret_cast<const SegDev*>(ws + l.rows), p->chunk_bytes, last_len,
+                     p->lwin.empty() ? nullptr : reinterpret_cast<const uint32_t*>(ws + l.win),
+                     p->ltiles.size(), reinterpret_cast<const LayoutSeg*>(ws + l.rows),
                      p->tile_bytes, stream));
     return II_OK;
 }
@@ -859,7 +955,7 @@ static int run_device_noalloc(ii_plan_t* p, const uint8_t* image, const uint64_t
 // tensor without staging.
 static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
                          hipStream_t stream) {
-    int rc = ensure_tables(p);
+    int rc = ensure_state(p);
     if (rc) return rc;
     rc = ensure_ring(p);
     if (rc) return rc;
@@ -867,58 +963,45 @@ static int run_pertensor(ii_plan_t* p, const uint8_t* blob, const uint64_t* dst,
     rc = check_dst(p, dst);
     if (rc) return rc;
     const bool pinned = pinned_span(p, blob);
-    hipStream_t cs = r->copy_s[0];
+    hipStream_t cs = r->lane_s[0];
     II_HIP(hipEventRecord(r->entry, stream));
     II_HIP(hipStreamWaitEvent(cs, r->entry, 0));
-    const uint64_t C = p->chunk_bytes;
-    const uint32_t D = r->depth;
-    uint32_t slot = 0;
-    uint64_t used = 0;  // bytes of the current slot already packed
-    auto close_slot = [&]() -> int {
-        II_HIP(hipEventRecord(r->copy_done[slot], cs));
-        r->copy_rec[slot] = 1;
-        slot = (slot + 1) % D;
-        used = 0;
-        if (r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
-        return II_OK;
-    };
-    if (!pinned && r->copy_rec[slot]) II_HIP(hipEventSynchronize(r->copy_done[slot]));
-    for (size_t i = 0; i < p->nbytes.size(); ++i) {
-        const uint64_t n = p->nbytes[i];
-        if (!n) continue;
-        const uint8_t* src = blob + p->src_offset[i];
-        // a tensor given as rows is gathered row by row (rb bytes every
-        // `stride` source bytes) into one contiguous destination
-        const uint64_t rb = n / p->rows[i], stride = p->row_stride[i];
-        if (pinned) {
+    if (pinned) {
+        // straight from the pinned blob, tensor by tensor (rows by one 2-D copy)
+        for (size_t i = 0; i < p->nbytes.size(); ++i) {
+            const uint64_t n = p->nbytes[i];
+            if (!n) continue;
+            const uint8_t* src = blob + p->src_offset[i];
+            const uint64_t rb = n / p->rows[i];
             if (p->rows[i] > 1)
-                II_HIP(h2d_2d(reinterpret_cast<void*>(dst[i]), rb, src, stride, rb, p->rows[i],
-                              cs));
+                II_HIP(h2d_2d(reinterpret_cast<void*>(dst[i]), rb, src, p->row_stride[i], rb,
+                              p->rows[i], cs));
             else
                 II_HIP(h2d(reinterpret_cast<void*>(dst[i]), src, n, cs));
-            continue;
         }
-        for (uint64_t x = 0; x < n;) {
-            if (used == C) {
-                rc = close_slot();
-                if (rc) return rc;
-            }
-            // stage tensor bytes [x, x + len) and copy them with one DMA
-            const uint64_t len = std::min(n - x, C - used);
-            uint8_t* stage = r->hslot[slot] + used;
-            for (uint64_t y = x; y < x + len;) {
-                const uint64_t q = y / rb, c = y % rb, m = std::min(x + len - y, rb - c);
-                r->pool->copy(stage + (y - x), src + q * stride + c, m);
-                y += m;
-            }
-            II_HIP(h2d(reinterpret_cast<void*>(dst[i] + x), stage, len, cs));
-            used += len;
-            x += len;
-        }
-    }
-    if (!pinned && used) {
-        II_HIP(hipEventRecord(r->copy_done[slot], cs));
-        r->copy_rec[slot] = 1;
+    } else {
+        // through the pinned slots (pertensor.h): slot 0 may still be read by
+        // the previous load's copies
+        if (r->copy_rec[0]) II_HIP(hipEventSynchronize(r->copy_done[0]));
+        auto stage = [&](uint32_t slot, uint64_t at, size_t i, uint64_t src_rel,
+                         uint64_t len) -> int {
+            r->pool->copy(r->hslot[slot] + at, blob + p->src_offset[i] + src_rel, len);
+            return II_OK;
+        };
+        auto copy = [&](uint32_t slot, uint64_t at, size_t i, uint64_t toff, uint64_t len) -> int {
+            II_HIP(h2d(reinterpret_cast<void*>(dst[i] + toff), r->hslot[slot] + at, len, cs));
+            return II_OK;
+        };
+        auto close = [&](uint32_t slot, uint32_t next) -> int {
+            II_HIP(hipEventRecord(r->copy_done[slot], cs));
+            r->copy_rec[slot] = 1;
+            if (next < r->depth && r->copy_rec[next])
+                II_HIP(hipEventSynchronize(r->copy_done[next]));
+            return II_OK;
+        };
+        rc = pertensor_schedule(p->nbytes.data(), p->rows.data(), p->row_stride.data(),
+                                p->nbytes.size(), p->chunk_bytes, r->depth, stage, copy, close);
+        if (rc) return rc;
     }
     II_HIP(hipEventRecord(r->done, cs));
     II_HIP(hipStreamWaitEvent(stream, r->done, 0));
@@ -1107,9 +1190,9 @@ extern "C" int ii_plan_set_ring(ii_plan_t* p, uint32_t depth, uint32_t host_thre
                                 uint32_t copy_streams) {
     if (!p) return fail(II_EINVAL, "ii_plan_set_ring: plan is NULL");
     if (depth < 1 || depth > 8 || host_threads < 1 || host_threads > 64 || copy_streams < 1 ||
-        copy_streams > kMaxCopyStreams || copy_streams > depth)
+        copy_streams > kMaxLanes || copy_streams > depth)
         return fail(II_EINVAL, "ii_plan_set_ring: depth must be 1..8, host_threads 1..64, "
-                               "copy_streams 1..min(2, depth)");
+                               "copy_streams 1..min(4, depth)");
     if (p->rt && p->rt->depth) return fail(II_EBUSY, "ii_plan_set_ring: ring already allocated");
     p->ring_depth = depth;
     p->host_threads = host_threads;
@@ -1163,7 +1246,9 @@ extern "C" int ii_plan_prepare(ii_plan_t* p) {
     BusyGuard g(p);
     if (!g.ok) return fail(II_EBUSY, "ii_plan_prepare: plan in use");
     inject_arm();
-    int rc = ensure_tables(p);
+    int rc = ensure_state(p);
+    if (rc) return rc;
+    rc = ensure_ring_tables(p);
     if (rc) return rc;
     return ensure_ring(p);
 }

@@ -8,25 +8,39 @@
 // movement, bound by HBM bandwidth: per payload byte one read of the chunk
 // and one write of the tensor.
 //
-// Work split. A chunk's segment bytes are cut into tiles of tile_bytes (4 KiB
-// by default), in segment order with gaps between segments skipped; one
-// 128-thread workgroup (two wavefronts) owns one tile, two 16-byte units
-// per lane. Measured on a Llama-8B-shaped set against 256 threads x 8 KiB,
-// 64 x 2 KiB and other shapes: two units per lane in small workgroups is
-// fastest. The planner stores, per tile, the segment rows whose bytes meet
-// it (and, for tables with gaps, the tile's window of chunk offsets), so a
-// workgroup reads only its own rows, and no workgroup is launched for bytes
-// no tensor needs (the gaps a sharded table leaves in the file). In a
-// packed staging slot, and in a chunk without gaps, the window is simply
-// the tile's share of the slot or chunk.
+// Work split. One 128-thread workgroup (two wavefronts) owns one tile of
+// tile_bytes (4 KiB by default), two 16-byte units per lane. Measured on a
+// Llama-8B-shaped set against 256 threads x 8 KiB, 64 x 2 KiB, 8 and 16 KiB
+// tiles, four or eight units per lane and persistent grids of 8 or 16
+// workgroups per CU: two units per lane in small workgroups, one tile each,
+// is fastest. The planner stores, per tile, the segment rows whose bytes
+// meet it, so a workgroup reads only its own rows.
+//   Ring (scatter_slot): a staged chunk's segment bytes are cut in segment
+// order, gaps between segments skipped, so no workgroup exists for bytes no
+// tensor needs (the gaps a sharded table leaves in the file). In a packed
+// staging slot, and in a chunk without gaps, a tile's window is simply its
+// share of the slot or chunk.
+//   Resident image (scatter_layout): the tiles are windows of the plan's
+// destination layout instead, the segments of all chunks in layout order.
+// Each workgroup then writes one aligned 4 KiB block of destination memory
+// (less any padding) and reads wherever its bytes lie. Writes that start or
+// end inside a 128-byte line cost HBM bandwidth (a plain copy into a
+// destination 48 bytes off a line runs 7% slower than an aligned one) while
+// misaligned reads cost nothing measurable, so cutting by destination wins
+// wherever source and destination offsets are not congruent modulo the
+// tile (the 100,000-tensor set: 5.43 against 5.09 TB/s) and ties where
+// they are (the Llama sets).
 //
 // Units. Destination memory is written in 16-byte blocks aligned to 16
 // bytes, so every store of a block that a segment covers completely is one
 // dwordx4 store. A unit is one (segment, destination block) pair. A unit
-// belongs to the tile holding the source byte of the first destination byte
-// it covers (its anchor), so every unit has exactly one owner even when the
-// source and destination phases (address mod 16) differ, and the units a
-// tile owns are contiguous within each segment.
+// belongs to the tile whose window holds its anchor: the coordinate of the
+// first destination byte it covers -- its source offset in the chunk for
+// the ring, its layout position for the resident image. Within a segment
+// both coordinates grow with the destination address, so every unit has
+// exactly one owner even when the source and destination phases (address
+// mod 16) differ, and the units a tile owns are contiguous within each
+// segment.
 //
 // Lanes to units. The workgroup stages its segment rows in LDS, counts each
 // segment's units in the tile, and forms an exclusive prefix sum. Lane u of
@@ -104,14 +118,14 @@ __device__ __forceinline__ uint32_t wave_scan(uint32_t v) {
 
 }  // namespace
 
-// One workgroup's share of the scatter: the units anchored in the window
-// [w0, w1) of offsets from device address cbase, among segments [s_first,
-// s_last). Every tile holds segment bytes, so s_first < s_last (the planner
+// One workgroup's share of the scatter: the units anchored in its window,
+// among segment rows [s_first, s_last). row(s, &cnt) returns the row of
+// segment s seen from the window and its count of units anchored there.
+// Every tile holds segment bytes, so s_first < s_last (the planner
 // guarantees it); the batch loop runs at least once with no guard, which
 // lets the argument loads issue together with the tile's own.
-__device__ __forceinline__ void scatter_tile(uint64_t cbase, uint64_t w0, uint64_t w1,
-                                             uint32_t s_first, uint32_t s_last,
-                                             const SegDev* __restrict__ segs) {
+template <class RowOf>
+__device__ __forceinline__ void scatter_tile(uint32_t s_first, uint32_t s_last, RowOf row) {
     __shared__ SegRow rows[kMaxSegBatch];
     __shared__ uint32_t pre[kMaxSegBatch];
     __shared__ uint32_t wsum[kBlock / 64];
@@ -123,10 +137,7 @@ __device__ __forceinline__ void scatter_tile(uint64_t cbase, uint64_t w0, uint64
     do {
         const uint32_t ns = min((uint32_t)kMaxSegBatch, s_last - s0);
         uint32_t cnt = 0;
-        if (tid < ns) {
-            const SegDev sd = segs[s0 + tid];
-            rows[tid] = make_row(sd.dst, sd.off, sd.len, cbase, w0, w1, &cnt);
-        }
+        if (tid < ns) rows[tid] = row(s0 + tid, &cnt);
         const uint32_t inc = wave_scan(cnt);
         if ((tid & 63u) == 63u) wsum[tid >> 6] = inc;
         __syncthreads();
@@ -189,45 +200,33 @@ __global__ __launch_bounds__(kBlock) void scatter_slot(
         w0 = tw.w0;
         w1 = tw.w1;
     }
-    scatter_tile(reinterpret_cast<uint64_t>(slot), w0, w1, td.first, td.last, segs);
+    const uint64_t cbase = reinterpret_cast<uint64_t>(slot);
+    scatter_tile(td.first, td.last, [&](uint32_t s, uint32_t* cnt) {
+        const SegDev sd = segs[s];
+        return make_row(sd.dst, sd.off, sd.len, cbase, w0, w1, cnt);
+    });
 }
 
-// Resident-image path: every tile of every chunk in one dispatch (a grid of
-// gy rows of gx workgroups, see grid_shape; tile g = y * gx + x, none past
-// ntiles); `span` is the device address of the blob's span byte lo, so chunk
-// k starts at span + k * chunk_bytes. This kernel serves tables whose segments fill every chunk
-// with no gap: every chunk but the last has per_chunk = ceil(chunk_bytes /
-// tile_bytes) tiles, tile g is tile g % per_chunk of chunk g / per_chunk,
-// and its window is that share of the chunk, so a workgroup reads only its
-// 8-byte segment range.
-__global__ __launch_bounds__(kBlock) void scatter_image(
+// Resident-image path: the whole table in one dispatch (a grid of gy rows of
+// gx workgroups, see grid_shape; tile g = y * gx + x, none past ntiles).
+// `span` is the device address of the blob's span byte lo; segment rows are
+// in layout order. Tile g takes the layout window w = win[g] (w = g when win
+// is null: no window of the layout is all padding).
+__global__ __launch_bounds__(kBlock) void scatter_layout(
     const uint8_t* __restrict__ span, const TileDev* __restrict__ tiles,
-    const SegDev* __restrict__ segs, uint64_t chunk_bytes, uint64_t last_len,
-    uint32_t num_chunks, uint32_t per_chunk, uint32_t tile_bytes, uint32_t ntiles) {
+    const uint32_t* __restrict__ win, const LayoutSeg* __restrict__ segs, uint32_t tile_bytes,
+    uint32_t ntiles) {
     const uint32_t g = blockIdx.y * gridDim.x + blockIdx.x;
     if (g >= ntiles) return;
     const TileDev td = tiles[g];
-    const uint32_t k = g / per_chunk;
-    const uint64_t clen = (k + 1 == num_chunks) ? last_len : chunk_bytes;
-    const uint64_t w0 = (uint64_t)(g - k * per_chunk) * tile_bytes;
-    const uint64_t w1 = min(clen, w0 + tile_bytes);
-    scatter_tile(reinterpret_cast<uint64_t>(span) + (uint64_t)k * chunk_bytes, w0, w1, td.first,
-                 td.last, segs);
-}
-
-// The resident-image path for tables with gaps between segments (tensor-
-// parallel shards read out of an unsharded file): tiles cover only segment
-// bytes, so each workgroup also reads its chunk index and its window.
-__global__ __launch_bounds__(kBlock) void scatter_image_gaps(
-    const uint8_t* __restrict__ span, const TileDev* __restrict__ tiles,
-    const TileWin* __restrict__ wins, const uint32_t* __restrict__ tile_chunk,
-    const SegDev* __restrict__ segs, uint64_t chunk_bytes, uint32_t ntiles) {
-    const uint32_t g = blockIdx.y * gridDim.x + blockIdx.x;
-    if (g >= ntiles) return;
-    const TileDev td = tiles[g];
-    const TileWin tw = wins[g];
-    const uint64_t cbase = reinterpret_cast<uint64_t>(span) + (uint64_t)tile_chunk[g] * chunk_bytes;
-    scatter_tile(cbase, tw.w0, tw.w1, td.first, td.last, segs);
+    const uint64_t w0 = (uint64_t)(win ? win[g] : g) * tile_bytes;
+    const uint64_t w1 = w0 + tile_bytes;
+    const uint64_t sb = reinterpret_cast<uint64_t>(span);
+    scatter_tile(td.first, td.last, [&](uint32_t s, uint32_t* cnt) {
+        const LayoutSeg ls = segs[s];
+        // source address of layout position x is sb + ls.src + (x - ls.pos)
+        return make_row(ls.dst, ls.pos, ls.len, sb + ls.src - ls.pos, w0, w1, cnt);
+    });
 }
 
 // Zero the byte ranges [r.begin, r.end) (device addresses). One workgroup per
@@ -259,22 +258,15 @@ hipError_t launch_scatter_slot(const uint8_t* slot, const TileDev* tiles, const 
     return hipGetLastError();
 }
 
-hipError_t launch_scatter_image(const uint8_t* span, const TileDev* tiles, const TileWin* wins,
-                                const uint32_t* tile_chunk, uint64_t ntiles, uint32_t num_chunks,
-                                uint32_t per_chunk, const SegDev* segs, uint64_t chunk_bytes,
-                                uint64_t last_len, uint32_t tile_bytes, hipStream_t stream) {
+hipError_t launch_scatter_layout(const uint8_t* span, const TileDev* tiles, const uint32_t* win,
+                                 uint64_t ntiles, const LayoutSeg* segs, uint32_t tile_bytes,
+                                 hipStream_t stream) {
     if (ntiles == 0) return hipSuccess;
     if (ntiles > 0x7fffffffull) return hipErrorInvalidConfiguration;
-    if (!per_chunk && (!wins || !tile_chunk)) return hipErrorInvalidValue;
     uint32_t gx, gy;
     grid_shape(ntiles, &gx, &gy);
-    if (per_chunk)
-        hipLaunchKernelGGL(scatter_image, dim3(gx, gy), dim3(kBlock), 0, stream, span, tiles, segs,
-                           chunk_bytes, last_len, num_chunks, per_chunk, tile_bytes,
-                           (uint32_t)ntiles);
-    else
-        hipLaunchKernelGGL(scatter_image_gaps, dim3(gx, gy), dim3(kBlock), 0, stream, span, tiles,
-                           wins, tile_chunk, segs, chunk_bytes, (uint32_t)ntiles);
+    hipLaunchKernelGGL(scatter_layout, dim3(gx, gy), dim3(kBlock), 0, stream, span, tiles, win,
+                       segs, tile_bytes, (uint32_t)ntiles);
     return hipGetLastError();
 }
 

@@ -38,6 +38,21 @@ struct TileWin {
 };
 static_assert(sizeof(TileWin) == 8, "TileWin must stay 8 bytes");
 
+// One segment as the resident-image kernel reads it, in destination layout
+// order: its bytes sit at span offset src (chunk * chunk_bytes + chunk
+// offset) of the image and go to device address dst; pos is its layout
+// position (the plan's destination offset of its first byte), the
+// coordinate the image kernel's tiles are cut in. 32 bytes: two dwordx4
+// loads per row.
+struct LayoutSeg {
+    uint64_t src;
+    uint64_t dst;
+    uint64_t pos;
+    uint32_t len;
+    uint32_t pad;
+};
+static_assert(sizeof(LayoutSeg) == 32, "LayoutSeg must stay 32 bytes");
+
 // Zero-fill range for the switch scrub: [begin, end) as device addresses.
 struct RangeDev {
     uint64_t begin;

@@ -85,6 +85,7 @@ _sig("ii_plan_packing", _c.c_int, _vp, _vp, _vp)
 _sig("ii_plan_chunks", _c.c_int, _vp, _vp, _vp, _vp)
 _sig("ii_plan_segments", _c.c_int, _vp, _vp, _vp, _vp, _vp, _vp)
 _sig("ii_plan_tiles", _c.c_int, _vp, _P(_u32), _P(_u64), _vp, _vp, _vp, _vp, _vp)
+_sig("ii_plan_layout_tiles", _c.c_int, _vp, _P(_u64), _vp, _vp, _vp, _vp)
 _sig("ii_plan_tensor_name", _c.c_char_p, _vp, _sz)
 _sig("ii_host_alloc", _c.c_int, _u64, _P(_vp))
 _sig("ii_host_free", _c.c_int, _vp)
@@ -260,7 +261,7 @@ class Plan:
         return out
 
     def tiles(self) -> dict:
-        """The kernel's tiles: tile_bytes and, per tile, chunk, first, last,
+        """The ring's tiles: tile_bytes and, per tile, chunk, first, last,
         w0, w1 (see ii_plan_tiles)."""
         tb, nt = _u32(), _u64()
         _check(_lib.ii_plan_tiles(self.handle, _c.byref(tb), _c.byref(nt), None, None, None,
@@ -272,6 +273,21 @@ class Plan:
                                   p(out["first"]), p(out["last"]), p(out["w0"]), p(out["w1"])),
                "ii_plan_tiles")
         out["tile_bytes"] = tb.value
+        return out
+
+    def layout_tiles(self) -> dict:
+        """The resident-image kernel's tiles (see ii_plan_layout_tiles):
+        seg_order (segments by layout position) and, per tile, first, last
+        and window."""
+        nt = _u64()
+        _check(_lib.ii_plan_layout_tiles(self.handle, _c.byref(nt), None, None, None, None),
+               "ii_plan_layout_tiles")
+        out = {f: np.zeros(nt.value, np.uint32) for f in ("first", "last", "window")}
+        out["seg_order"] = np.zeros(self.num_segments, np.uint32)
+        p = lambda a: a.ctypes.data if a.size else None  # noqa: E731
+        _check(_lib.ii_plan_layout_tiles(self.handle, _c.byref(nt), p(out["seg_order"]),
+                                         p(out["first"]), p(out["last"]), p(out["window"])),
+               "ii_plan_layout_tiles")
         return out
 
     def packing(self) -> dict:

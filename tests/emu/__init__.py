@@ -35,6 +35,10 @@ def _load():
                                     vp, ctypes.c_int, u32, u32, vp, vp, vp, u64, u64, u64, u64,
                                     vp, u32, ctypes.c_char_p, ctypes.c_int, vp]
         lib.emu_scatter.restype = ctypes.c_int
+        lib.emu_scatter_layout.argtypes = [u64, u64, u64, vp, vp, vp, vp, vp, vp, vp, u64, vp,
+                                           vp, vp, u32, vp, vp, vp, u64, u64, u64, u64, vp, u32,
+                                           ctypes.c_char_p, ctypes.c_int, vp]
+        lib.emu_scatter_layout.restype = ctypes.c_int
         _lib = lib
     return _lib
 
@@ -96,3 +100,26 @@ def scatter_packed(plan, blob: np.ndarray, tensor_dst: np.ndarray, arena_base: i
         image[k * C + po:k * C + po + ln] = blob[a:a + ln]
     return _emulate(plan, image, 0, K * C, pk["seg_off"], True, tensor_dst, arena_base, arena,
                     src_base, batch)
+
+
+def scatter_layout(plan, blob: np.ndarray, tensor_dst: np.ndarray, arena_base: int,
+                   arena: np.ndarray, src_base: int, batch: int = 256):
+    """Run the emulated resident-image kernel over the plan's layout tiles
+    (windows of the destination layout, segments in layout order), reading
+    chunks from the blob in place. Returns (ok, message, stats)."""
+    lo, hi = plan.span
+    seg = plan.segments()
+    lt = plan.layout_tiles()
+    nb, doff = plan.tensors()
+    tb = plan.tiles()["tile_bytes"]
+    err = ctypes.create_string_buffer(512)
+    stats = np.zeros(4, np.uint64)
+    p = lambda a: a.ctypes.data if a.size else None  # noqa: E731
+    dst = np.ascontiguousarray(tensor_dst, dtype=np.uint64)
+    rc = _load().emu_scatter_layout(plan.chunk_bytes, lo, hi, blob.ctypes.data, p(seg["chunk"]),
+                                    p(seg["chunk_off"]), p(seg["len"]), p(seg["tensor"]),
+                                    p(seg["tensor_off"]), p(lt["seg_order"]), len(lt["first"]),
+                                    p(lt["first"]), p(lt["last"]), p(lt["window"]), tb, p(dst),
+                                    p(doff), p(nb), len(nb), src_base, arena_base, arena.size,
+                                    arena.ctypes.data, batch, err, 512, stats.ctypes.data)
+    return rc == 0, err.value.decode(), stats

@@ -238,6 +238,122 @@ int emu_scatter(uint64_t num_chunks, uint64_t chunk_bytes, uint64_t lo, uint64_t
     return 0;
 }
 
+// Emulate the resident-image kernel (scatter_layout) over the plan's layout
+// tiles: tile g takes the layout positions [window[g] * tile_bytes, +
+// tile_bytes) and the layout-order segments seg_order[first[g] ..
+// last[g]); segment x's bytes sit at emulated address src_base + chunk[x] *
+// chunk_bytes + chunk_off[x] and go to tensor_dst[tensor[x]] + tensor_off[x],
+// its layout position being dst_offset[tensor[x]] + tensor_off[x]. Checks
+// as emu_scatter, and that every unit's anchor (the layout position of its
+// first destination byte) lies in its tile's window.
+int emu_scatter_layout(uint64_t chunk_bytes, uint64_t lo, uint64_t hi, const uint8_t* blob,
+                       const uint32_t* seg_chunk, const uint32_t* seg_off,
+                       const uint32_t* seg_len, const uint32_t* seg_tensor,
+                       const uint64_t* seg_toff, const uint32_t* seg_order, uint64_t ntiles,
+                       const uint32_t* tile_first, const uint32_t* tile_last,
+                       const uint32_t* tile_window, uint32_t tile_bytes,
+                       const uint64_t* tensor_dst, const uint64_t* tensor_dst_offset,
+                       const uint64_t* tensor_nbytes, uint64_t ntensors, uint64_t src_base,
+                       uint64_t arena_base, uint64_t arena_len, uint8_t* arena, uint32_t batch,
+                       char* err, int errlen, uint64_t* stats) {
+    EmuMem m;
+    m.blob = blob;
+    m.lo = lo;
+    m.hi = hi;
+    m.src_base = src_base;
+    m.arena = arena;
+    m.arena_base = arena_base;
+    m.arena_len = arena_len;
+    std::vector<uint8_t> writes(arena_len, 0);
+    m.writes = &writes;
+    uint64_t units = 0, max_rows = 0;
+    if (batch > kMaxSegBatch) batch = kMaxSegBatch;
+    std::vector<SegRow> rows(batch);
+    std::vector<uint32_t> pre(batch), cnt(batch), srow(batch);
+    std::vector<uint64_t> rpos(batch), rdst(batch);
+    uint64_t prev_window = 0;
+    for (uint64_t g = 0; g < ntiles && m.err.empty(); ++g) {
+        const uint64_t w0 = (uint64_t)tile_window[g] * tile_bytes, w1 = w0 + tile_bytes;
+        if (g && tile_window[g] <= prev_window) m.bad("tile windows not increasing", g);
+        prev_window = tile_window[g];
+        const uint32_t first = tile_first[g], last = tile_last[g];
+        if (first >= last) m.bad("tile without segments", g);
+        max_rows = std::max<uint64_t>(max_rows, last - first);
+        for (uint32_t s0 = first; s0 < last && m.err.empty(); s0 += batch) {
+            const uint32_t ns = std::min(batch, last - s0);
+            uint32_t total = 0;
+            for (uint32_t i = 0; i < ns; ++i) {
+                const uint32_t s = seg_order[s0 + i];
+                const uint64_t src = (uint64_t)seg_chunk[s] * chunk_bytes + seg_off[s];
+                rdst[i] = tensor_dst[seg_tensor[s]] + seg_toff[s];
+                rpos[i] = tensor_dst_offset[seg_tensor[s]] + seg_toff[s];
+                rows[i] = make_row(rdst[i], rpos[i], seg_len[s], src_base + src - rpos[i], w0,
+                                   w1, &cnt[i]);
+                pre[i] = total;
+                total += cnt[i];
+                rows[i].ubase -= pre[i];
+                srow[i] = s;
+            }
+            for (uint32_t base = 0; base < total && m.err.empty(); base += kBlockE * kUnrollE) {
+                for (uint32_t tid = 0; tid < kBlockE && m.err.empty(); ++tid) {
+                    for (int j = 0; j < kUnrollE; ++j) {
+                        const uint32_t u = base + (uint32_t)j * kBlockE + tid;
+                        if (u >= total || !m.err.empty()) continue;
+                        const uint32_t r = find_row(pre.data(), ns, u);
+                        if (r >= ns) m.bad("row index out of range", r);
+                        if (!(pre[r] <= u && u < pre[r] + cnt[r])) {
+                            m.bad("lane mapped to a row that does not own its unit", u);
+                            break;
+                        }
+                        const uint32_t s = srow[r];
+                        m.row_src_b = src_base + (uint64_t)seg_chunk[s] * chunk_bytes + seg_off[s];
+                        m.row_src_e = m.row_src_b + seg_len[s];
+                        m.row_dst_b = rows[r].dbeg;
+                        m.row_dst_e = rows[r].dend;
+                        const UnitIO io = unit_io(rows[r], u);
+                        const uint64_t anchor = rpos[r] + (io.d + io.c0 - rdst[r]);
+                        if (anchor < w0 || anchor >= w1) m.bad("unit anchored outside its tile", io.d);
+                        U4 x0{0, 0, 0, 0}, x1{0, 0, 0, 0};
+                        if (io.need0) x0 = m.ld16(io.A);
+                        if (io.need1) x1 = m.ld16(io.A + 16);
+                        const U4 v = funnel16(x0, x1, io.p);
+                        if (io.c1 > io.c0) store_unit(m, io.d, v, io.c0, io.c1);
+                        else m.bad("unit with no bytes", io.d);
+                        ++units;
+                    }
+                }
+            }
+        }
+    }
+    if (m.err.empty()) {
+        std::vector<uint8_t> want(arena_len, 0);
+        for (uint64_t i = 0; i < ntensors; ++i) {
+            if (!tensor_nbytes[i]) continue;
+            uint64_t b = tensor_dst[i] - arena_base;
+            for (uint64_t j = 0; j < tensor_nbytes[i]; ++j) want[b + j] = 1;
+        }
+        for (uint64_t x = 0; x < arena_len; ++x)
+            if (writes[x] != want[x]) {
+                char b[160];
+                snprintf(b, sizeof b, "arena byte %llu written %u times, expected %u",
+                         (unsigned long long)x, writes[x], want[x]);
+                m.err = b;
+                break;
+            }
+    }
+    if (stats) {
+        stats[0] = units;
+        stats[1] = m.loads;
+        stats[2] = m.stores;
+        stats[3] = max_rows;
+    }
+    if (!m.err.empty()) {
+        snprintf(err, errlen, "%s", m.err.c_str());
+        return 1;
+    }
+    return 0;
+}
+
 // The image launch's grid for n workgroups (grid_shape): no dimension may
 // count more than 2^32 - 1 work-items, the indices y * gx + x must cover
 // [0, n), and fewer than gy of them may lie past it. Returns 0 if so.

@@ -5,6 +5,7 @@ destination alignments, chunk sizes and ring shapes."""
 import numpy as np
 
 import oracle_pins
+from paper_2607_18957_amd import synth
 
 
 def random_table(rng):
@@ -47,3 +48,13 @@ def cases(seed, count):
         depth = int(rng.integers(1, 4))
         cs = int(rng.integers(1, min(depth, 2) + 1))
         yield case, t, depth, cs
+
+
+def sparse_layout_table(n=400, seed=7):
+    """Small tensors of the stress distribution with destination alignments
+    up to 1 MiB: most 4 KiB windows of the destination layout hold only
+    padding."""
+    t = synth.stress(n=n, chunk=1 << 20)
+    rng = np.random.default_rng(seed)
+    t.dst_align = rng.choice(np.array([1, 256, 4096, 1 << 16, 1 << 20], dtype=np.uint64), size=t.n)
+    return t

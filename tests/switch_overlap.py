@@ -3,14 +3,15 @@ process of its own: run by test_gpu.py as a child process and prints one
 JSON line.
 
 With the old model's work still pending on the caller's stream, ii_switch
-copies the new model's first ring-depth chunks into the ring at once and
-writes the arena only after that work. Whether those copies really run
-during the old model's work depends on the HIP runtime giving the ring's
-copy streams hardware queues of their own (a process gets a few queues,
-four by default; streams beyond them share one, and a copy stream that
-shares the caller's queue waits behind the caller's work). A fresh process
-holds only the caller's stream and the plan's, so the measurement is
-repeatable there.
+copies the new model's first chunks into the ring at once -- one per lane,
+the ring's streams, here as many lanes as slots -- and writes the arena
+only after that work. Whether those copies really run during the old
+model's work depends on the HIP runtime giving the lanes hardware queues of
+their own (a process gets a few queues, four by default; streams beyond
+them share one, and a lane that shares the caller's queue waits behind the
+caller's work). A fresh process holds only the caller's stream and the new
+plan's three lanes (the old model is loaded from a device image, on the
+caller's stream), so the measurement is repeatable there.
 """
 import json
 import os
@@ -41,15 +42,16 @@ def main():
     old = synth.tiny(chunk=1 << 20)
     new = synth.transformer("tiny-b", 4, 256, 1024, 256, 4096, seed=21, chunk=1 << 20)
     po, pn = ii.ii_plan(old), ii.ii_plan(new)
-    pn.set_ring(depth, 4, 2)
+    pn.set_ring(depth, 4, depth)
     pn.prepare()
     blob_o, blob_n = synth.blob(old), synth.blob(new)
+    image_o = torch.from_numpy(blob_o).to(DEV)
     arena = torch.empty(po.arena_bytes, dtype=torch.uint8, device=DEV)
     base = arena.data_ptr()
     s = torch.cuda.current_stream(DEV)
 
     def reload():
-        ii.ii_load(po, blob_o, base + po.tensors()[1], s)
+        ii.ii_load_device(po, image_o, base + po.tensors()[1], s)
         s.synchronize()
 
     reload()

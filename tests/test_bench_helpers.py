@@ -19,30 +19,37 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_table_bytes_per_launch():
-    """16 B per segment row and 8 B per tile range; tables with gaps add an
-    8-byte window and a 4-byte chunk index per tile."""
+    """32 B per layout row and 8 B per layout tile; a layout with windows of
+    padding only adds a 4-byte window index per tile."""
+    import oracle_pins
     dense = ii.ii_plan(synth.tiny())
-    tiles = len(dense.tiles()["first"])
-    assert bench.table_bytes(dense) == dense.num_segments * 16 + tiles * 8
+    tiles = len(dense.layout_tiles()["first"])
+    assert bench.table_bytes(dense) == dense.num_segments * 32 + tiles * 8
     shard = ii.ii_plan(synth.tiny_tp(1, 4))
-    tiles = len(shard.tiles()["first"])
-    assert bench.table_bytes(shard) == shard.num_segments * 16 + tiles * 20
+    tiles = len(shard.layout_tiles()["first"])
+    assert bench.table_bytes(shard) == shard.num_segments * 32 + tiles * 8
+    # 100-byte tensors 64 KiB apart in the layout: most windows are padding
+    sparse = ii.ii_plan(oracle_pins._u8_table([100] * 5, [0, 100, 200, 300, 400], [65536] * 5),
+                        1 << 20)
+    tiles = len(sparse.layout_tiles()["first"])
+    assert tiles == 5
+    assert bench.table_bytes(sparse) == sparse.num_segments * 32 + tiles * 12
 
 
 def test_counter_means(tmp_path):
     path = tmp_path / "run_counter_collection.csv"
-    rows = [("ii::scatter_image(x)", 1024, "FETCH_SIZE", 10.0),
-            ("ii::scatter_image(x)", 1024, "FETCH_SIZE", 30.0),
-            ("ii::scatter_image(x)", 1024, "WRITE_SIZE", 7.0),
+    rows = [("ii::scatter_layout(x)", 1024, "FETCH_SIZE", 10.0),
+            ("ii::scatter_layout(x)", 1024, "FETCH_SIZE", 30.0),
+            ("ii::scatter_layout(x)", 1024, "WRITE_SIZE", 7.0),
             ("__amd_rocclr_copyBuffer", 64, "FETCH_SIZE", 5.0)]
     with open(path, "w") as f:
         f.write("Kernel_Name,Grid_Size,Counter_Name,Counter_Value\n")
         for name, grid, counter, value in rows:
             f.write(f"\"{name}\",{grid},{counter},{value}\n")
     got = bench._counter_means(str(path), "FETCH_SIZE")
-    assert got[("ii::scatter_image", 1024)] == (20.0, 2)
+    assert got[("ii::scatter_layout", 1024)] == (20.0, 2)
     assert got[("__amd_rocclr_copyBuffer", 64)] == (5.0, 1)
-    assert bench._counter_means(str(path), "WRITE_SIZE") == {("ii::scatter_image", 1024): (7.0, 1)}
+    assert bench._counter_means(str(path), "WRITE_SIZE") == {("ii::scatter_layout", 1024): (7.0, 1)}
 
 
 def test_trace_durations(tmp_path):
@@ -53,10 +60,10 @@ def test_trace_durations(tmp_path):
         f.write("Kernel_Name,Grid_Size_X,Grid_Size_Y,Grid_Size_Z,Start_Timestamp,End_Timestamp\n")
         f.write("\"ii::scatter_slot(a, b)\",8192,1,1,100,350\n")
         f.write("\"ii::scatter_slot(a, b)\",8192,1,1,400,600\n")
-        f.write("\"ii::scatter_image(c)\",1024,3,1,1000,9000\n")
+        f.write("\"ii::scatter_layout(c)\",1024,3,1,1000,9000\n")
     got = bench._trace_durations(str(path))
     assert got[("ii::scatter_slot", 8192)] == [250, 200]
-    assert got[("ii::scatter_image", 3072)] == [8000]
+    assert got[("ii::scatter_layout", 3072)] == [8000]
 
 
 def test_ring_kernel_from_trace():

@@ -21,6 +21,20 @@ from paper_2607_18957_amd import ii, synth
 
 def _run(orc, table, *, chunk=None, arena_phase=0, src_phase=0, batch=256, dst_of=None,
          tile=None, monkeypatch=None, packed=False):
+    """The ring's kernel over the chunks in place (or, packed=True, over the
+    packed staging layout) and, unless packed, the resident-image kernel over
+    the layout tiles; each result compared with the oracle's."""
+    stats = _run_one(orc, table, chunk=chunk, arena_phase=arena_phase, src_phase=src_phase,
+                     batch=batch, dst_of=dst_of, tile=tile, monkeypatch=monkeypatch,
+                     kind="packed" if packed else "chunk")
+    if not packed:
+        _run_one(orc, table, chunk=chunk, arena_phase=arena_phase, src_phase=src_phase,
+                 batch=batch, dst_of=dst_of, tile=tile, monkeypatch=monkeypatch, kind="layout")
+    return stats
+
+
+def _run_one(orc, table, *, chunk, arena_phase, src_phase, batch, dst_of, tile, monkeypatch,
+             kind):
     if tile:
         monkeypatch.setenv("II_TILE_BYTES", str(tile))
     plan = ii.ii_plan(table, chunk or table.chunk_bytes)
@@ -32,9 +46,9 @@ def _run(orc, table, *, chunk=None, arena_phase=0, src_phase=0, batch=256, dst_o
     dst = base + rel
     can = synth.canary(arena_len)
     got = can.copy()
-    run = emu.scatter_packed if packed else emu.scatter
+    run = {"packed": emu.scatter_packed, "chunk": emu.scatter, "layout": emu.scatter_layout}[kind]
     ok, msg, stats = run(plan, blob, dst, base, got, (1 << 40) + src_phase, batch)
-    assert ok, msg
+    assert ok, f"{kind}: {msg}"
     want = can.copy()
     # the oracle arena, at the same (possibly shifted) offsets
     nbo = orc.nbytes(table)
@@ -53,7 +67,7 @@ def _run(orc, table, *, chunk=None, arena_phase=0, src_phase=0, batch=256, dst_o
         outs = orc.load(nbo, table.src_offset, blob)
         for o, d in zip(outs, dst - base):
             want[int(d):int(d) + o.size] = o
-    assert np.array_equal(got, want), int(np.flatnonzero(got != want)[0])
+    assert np.array_equal(got, want), (kind, int(np.flatnonzero(got != want)[0]))
     return stats
 
 
@@ -226,3 +240,14 @@ def test_image_grid_shape():
         assert lib.emu_grid_check(n, ctypes.byref(gx), ctypes.byref(gy)) == 0, n
         assert gy.value == max(1, -(-n // m)), n
         assert gx.value * 128 <= 0xffffffff and gx.value * gy.value >= n, n
+
+
+def test_layout_windows_of_padding_only(orc):
+    """Destination alignments up to 1 MiB on small tensors (the GPU suite's
+    table): most layout windows hold only padding and have no tile."""
+    t = random_tables.sparse_layout_table()
+    plan = ii.ii_plan(t)
+    lt = plan.layout_tiles()
+    assert not np.array_equal(lt["window"], np.arange(len(lt["first"])))
+    _run(orc, t, arena_phase=0, src_phase=5)
+    _run(orc, t, packed=True)

@@ -45,6 +45,7 @@ def _compare(orc, table, chunk=None):
     assert np.array_equal(np.diff(sb.astype(np.int64)),
                           np.bincount(op["seg_chunk"], minlength=plan.num_chunks))
     _check_tiles(plan, s, l)
+    _check_layout_tiles(plan, s)
     pk = _check_packing(plan, s)
     if np.array_equal(pk["chunk_len"], l):   # dense chunks: packing changes nothing
         assert np.array_equal(pk["seg_off"], s["chunk_off"])
@@ -106,6 +107,40 @@ def _check_tiles(plan, s, chunk_len):
             jj = np.maximum(j, 0)
             return np.where(j < 0, 0, cum[jj] + np.clip(x - off[a:b][jj], 0, ln[a:b][jj]))
         assert np.array_equal(below(w1) - below(w0), P1 - P0), k
+
+
+def _check_layout_tiles(plan, s):
+    """The resident-image kernel's tiles, derived here from the segments and
+    the layout alone: a segment's layout position is its tensor's
+    destination offset plus its tensor offset; seg_order lists the segments
+    by that position; the tiles are exactly the windows [w*T, (w+1)*T) of
+    layout positions that some segment meets, in increasing order, and tile
+    g meets exactly the segments whose layout ranges meet its window."""
+    T = plan.tiles()["tile_bytes"]
+    lt = plan.layout_tiles()
+    _, doff = plan.tensors()
+    S = plan.num_segments
+    pos = doff[s["tensor"]].astype(np.int64) + s["tensor_off"].astype(np.int64)
+    ln = s["len"].astype(np.int64)
+    order = lt["seg_order"].astype(np.int64)
+    assert np.array_equal(np.sort(order), np.arange(S))
+    ps, ls = pos[order], ln[order]
+    assert (np.diff(ps) > 0).all() if S > 1 else True
+    assert (ps[1:] >= ps[:-1] + ls[:-1]).all()   # disjoint, in layout order
+    m0, m1 = ps // T, (ps + ls - 1) // T
+    win = lt["window"].astype(np.int64)
+    union = int((m1 - m0 + 1).sum()) - int((m0[1:] == m1[:-1]).sum())
+    assert win.size == union
+    if not win.size:
+        return
+    assert (np.diff(win) > 0).all()
+    assert np.isin(m0, win).all() and np.isin(m1, win).all()
+    w0 = win * T
+    first = np.searchsorted(ps + ls, w0, side="right")
+    last = np.searchsorted(ps, w0 + T, side="left")
+    assert (first < last).all()                  # every tile meets a segment
+    assert np.array_equal(lt["first"].astype(np.int64), first)
+    assert np.array_equal(lt["last"].astype(np.int64), last)
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama8b", "mistral7b", "llama70b"])
@@ -303,6 +338,7 @@ def _compare_rows(orc, table, chunk=None):
     assert sb[0] == 0 and sb[-1] == plan.num_segments
     assert plan.copy_bytes == _expected_copy_bytes(op)
     _check_tiles(plan, s, l)
+    _check_layout_tiles(plan, s)
     _check_packing(plan, s)
     return plan
 
