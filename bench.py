@@ -10,7 +10,8 @@ host memory (one process cannot pin 141 GB on the host).
 One step = one full load of every tensor through the C-ABI (ii_load): host
 threads stage each chunk into a 3-slot pinned ring, one hipMemcpyAsync per
 chunk carries it to a device slot, and the scatter kernel writes it into its
-tensors while the next chunk is in flight. value = payload bytes x steps /
+tensors (chunk k's copy and scatter on lane k mod 3) while the next chunks
+are in flight. value = payload bytes x steps /
 wall time of the steps (GB = 1e9 B), the loads enqueued back to back and
 bracketed by device synchronisation; tensors/s beside it; both also as a
 fraction of the measured host-to-device copy peak.
@@ -494,17 +495,19 @@ def all_configs(torch, dev, ii, synth) -> dict:
 
 def profile_cmds(workload: str) -> dict:
     """The three profiled runs of the benchmark command whose summaries are
-    committed (<out> = the output folder, <repo> = this repository)."""
-    bench = "python3 <repo>/bench.py --gpus 1 --steps 20 --warmup 5"
+    committed (<out> = the output folder, <repo> = this repository): the
+    default command itself for the default workload, so that the profiled
+    kernel average and the benchmark line describe the same launches."""
+    bench = "python3 <repo>/bench.py"
     if workload != DEFAULT_WORKLOAD:
         bench += f" --workload {workload}"
     return {
         "trace": f"cd /tmp && rocprofv3 --kernel-trace --stats --output-format csv "
-                 f"-d <out>/trace_{workload} -o run -- {bench}",
+                 f"-d <out>/trace_{workload} -o run_%pid% -- {bench}",
         "fetch": f"cd /tmp && timeout -s KILL 900 rocprofv3 --pmc FETCH_SIZE --output-format csv "
-                 f"-d <out>/fetch_{workload} -o run -- {bench}",
+                 f"-d <out>/fetch_{workload} -o run_%pid% -- {bench}",
         "write": f"cd /tmp && timeout -s KILL 900 rocprofv3 --pmc WRITE_SIZE --output-format csv "
-                 f"-d <out>/write_{workload} -o run -- {bench}",
+                 f"-d <out>/write_{workload} -o run_%pid% -- {bench}",
     }
 
 
@@ -534,6 +537,17 @@ def _trace_durations(path: str) -> dict:
     return acc
 
 
+def _profile_csv(folder: str, suffix: str) -> str:
+    """The benchmark process's CSV among those a profiled run wrote (the
+    child process that measures the H2D peak writes files of its own): the
+    one that names this library's kernels."""
+    for path in sorted(glob.glob(os.path.join(folder, "**", f"*{suffix}"), recursive=True)):
+        with open(path) as fh:
+            if "ii::" in fh.read():
+                return path
+    raise FileNotFoundError(f"no {suffix} naming ii:: kernels under {folder}")
+
+
 def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
               bench_json: str) -> None:
     """Write the committed profile summaries of the image kernel and of the
@@ -545,7 +559,7 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
     run = json.loads(open(bench_json).read().strip().splitlines()[-1])
     cfg, roof = run["config"], run["roofline"]
     ring = roof["ring_kernel"]
-    rows = list(csv.DictReader(open(os.path.join(trace_dir, "run_kernel_stats.csv"))))
+    rows = list(csv.DictReader(open(_profile_csv(trace_dir, "kernel_stats.csv"))))
     lines = [f"# Kernel statistics, {workload}-shaped workload ({cfg['tensors']} tensors, "
              f"{cfg['payload_bytes']} B, {cfg['chunks']} chunks of {cfg['chunk_bytes'] >> 20} MiB),",
              "# one GPU, the benchmark command under the profiler:",
@@ -557,7 +571,7 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
         lines.append(f"{name:<34}{r['Calls']:>7}{float(r['AverageNs']):>14.1f}"
                      f"{float(r['MinNs']):>12.0f}{float(r['MaxNs']):>12.0f}"
                      f"{float(r['Percentage']):>8.2f}")
-    durs = _trace_durations(os.path.join(trace_dir, "run_kernel_trace.csv"))
+    durs = _trace_durations(_profile_csv(trace_dir, "kernel_trace.csv"))
     img = [v for k, v in durs.items() if k[0] == "ii::" + KERNEL]
     full_grid = -(-cfg["chunk_bytes"] // 4096) * 128
     slot_full = durs.get(("ii::scatter_slot", full_grid), [])
@@ -581,15 +595,15 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
                   f"{100 * ring['bytes_per_chunk'] / (d.mean() * 1e-6) / 1e9 / HBM_PEAK_GBPS:.1f}% of "
                   "8 TB/s",
                   f"  bench.py, one traced load in the same run: mean {ring['mean_us']:.1f} us per "
-                  "full chunk (timing events on the scatter stream)"]
+                  "full chunk (timing events on its lane)"]
     lines += ["", f"bench line of the traced run: value {run['value']:.2f} GB/s "
               f"({100 * run['frac_of_h2d_peak']:.1f}% of the H2D peak {run['h2d_peak']['GBps']:.2f}), "
               f"roofline frac {roof['frac']:.4f}"]
     open(os.path.join(ROOT, "profiles", f"{KERNEL}_{workload}_kernel_stats.txt"), "w").write(
         "\n".join(lines) + "\n")
 
-    fetch = _counter_means(os.path.join(fetch_dir, "run_counter_collection.csv"), "FETCH_SIZE")
-    write = _counter_means(os.path.join(write_dir, "run_counter_collection.csv"), "WRITE_SIZE")
+    fetch = _counter_means(_profile_csv(fetch_dir, "counter_collection.csv"), "FETCH_SIZE")
+    write = _counter_means(_profile_csv(write_dir, "counter_collection.csv"), "WRITE_SIZE")
     # calibration: the 4 GiB device-to-device copy of the benchmark (the
     # largest runtime copy kernel)
     copies = [k for k in fetch if k[0].startswith("__amd_rocclr_copyBuffer")]

@@ -58,3 +58,20 @@ def sparse_layout_table(n=400, seed=7):
     rng = np.random.default_rng(seed)
     t.dst_align = rng.choice(np.array([1, 256, 4096, 1 << 16, 1 << 20], dtype=np.uint64), size=t.n)
     return t
+
+
+def handover_table(pairs=6, chunk=1 << 16):
+    """Chunks that alternate between heavy and light scatters: even chunks
+    hold `chunk` one-byte tensors (thousands of segments per tile), odd
+    chunks one tensor of `chunk` bytes. With more ring slots than lanes,
+    the lane that refills a slot is not the lane whose scatter last read
+    it, and that scatter (a heavy one) runs far longer than the light
+    scatter ahead of the refill on the refilling lane."""
+    sizes = []
+    for _ in range(pairs):
+        sizes += [1] * chunk + [chunk]
+    src = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.uint64)
+    t = oracle_pins._u8_table(sizes, src, [1] * len(sizes))
+    t.chunk_bytes = chunk
+    t.blob = np.random.default_rng(9).integers(0, 256, size=int(src[-1]) + chunk, dtype=np.uint8)
+    return t

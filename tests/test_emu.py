@@ -251,3 +251,11 @@ def test_layout_windows_of_padding_only(orc):
     assert not np.array_equal(lt["window"], np.arange(len(lt["first"])))
     _run(orc, t, arena_phase=0, src_phase=5)
     _run(orc, t, packed=True)
+
+
+def test_handover_table(orc):
+    """The GPU suite's lane hand-over table (alternating chunks of 65,536
+    one-byte tensors and of one 64 KiB tensor), ring and image splits."""
+    t = random_tables.handover_table(pairs=2)
+    _run(orc, t)
+    _run(orc, t, packed=True)

@@ -431,6 +431,23 @@ def test_ring_race_stress(orc, depth, copy_streams):
             raise AssertionError(f"arena {i}: {bad.size} bytes differ, first at {int(bad[0])}")
 
 
+@pytest.mark.parametrize("depth,lanes", [(3, 2), (4, 3)])
+def test_ring_handover_between_lanes(orc, depth, lanes):
+    """With more slots than lanes, a slot is refilled by another lane than
+    the one whose scatter last read it, and the refill must wait for that
+    scatter (the hand-over event). Chunks alternate between a heavy scatter
+    (65,536 one-byte tensors) and a light one (one tensor), so the
+    refilling lane reaches the refill long before the other lane's heavy
+    scatter has ended; a refill that did not wait would overwrite the slot
+    under it. Pinned and pageable blobs, two loads each."""
+    t = random_tables.handover_table()
+    plan = ii.ii_plan(t)
+    plan.set_ring(depth, 2, lanes)
+    assert plan.num_chunks == 12
+    for mode in ("pinned", "pageable", "pinned", "pageable"):
+        _load_arena(orc, t, mode=mode, blob=t.blob, plan=plan)
+
+
 def test_back_to_back_loads_no_sync(orc):
     """Two loads on one plan into different arenas with no host sync between
     them: slot reuse carries across calls."""
