@@ -72,6 +72,7 @@ def handover_table(pairs=6, chunk=1 << 16):
         sizes += [1] * chunk + [chunk]
     src = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.uint64)
     t = oracle_pins._u8_table(sizes, src, [1] * len(sizes))
+    t.name = "handover"
     t.chunk_bytes = chunk
     t.blob = np.random.default_rng(9).integers(0, 256, size=int(src[-1]) + chunk, dtype=np.uint8)
     return t
