@@ -438,6 +438,14 @@ int ii_plan_tiles(const ii_plan_t* plan, uint32_t* tile_bytes, uint64_t* num_til
  * Errors: II_EINVAL (NULL plan). */
 int ii_plan_layout_tiles(const ii_plan_t* plan, uint64_t* num_tiles, uint32_t* seg_order,
                          uint32_t* first, uint32_t* last, uint32_t* window);
+/* which of its two variants the resident-image kernel runs for this plan: 1
+ * for the variant for tables of many small tensors (tiles that one segment
+ * meets take a path without LDS staging, and every tile issues all its
+ * loads before using any), chosen when at least II_LAYOUT_MIXED_PCT percent
+ * (default 5; 0 = always, 101 = never) of the tiles meet three or more
+ * segments; 0 for the other (fewer loads in flight, faster on tables of
+ * large tensors). Both write the same bytes. 0 for a NULL plan. */
+int ii_plan_layout_mixed(const ii_plan_t* plan);
 /* name of row i as given to ii_plan ("" if none); valid while the plan lives */
 const char* ii_plan_tensor_name(const ii_plan_t* plan, size_t i);
 

@@ -113,6 +113,9 @@ struct ii_plan_s {
     std::vector<uint32_t> lseg;
     std::vector<ii::TileDev> ltiles;
     std::vector<uint32_t> lwin;
+    // whether the image kernel runs its variant for tables of many small
+    // tensors (more loads in flight; see the planner's rule)
+    bool layout_mixed = false;
     // host buffers of ii_load_device_noalloc, sized when the plan is made so
     // that the call itself allocates nothing: the layout-order segment rows
     // with resolved destinations, and the destination ranges its checks sort

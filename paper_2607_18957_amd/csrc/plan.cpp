@@ -417,6 +417,16 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
             // holds segment bytes exactly when the last tile is window G - 1
             if (p->ltiles.empty() || p->lwin.back() == p->ltiles.size() - 1)
                 std::vector<uint32_t>().swap(p->lwin);
+            // the image kernel's variant for tables of many small tensors
+            // (ii_plan_layout_mixed): when at least II_LAYOUT_MIXED_PCT
+            // percent (default 5) of the tiles meet three or more segments
+            // (0 = always, 101 = never).
+            // The 100,000-tensor set has 10.4% such tiles; a tensor-parallel
+            // shard of rows of 15 KB, none; tables of large tensors, none.
+            uint64_t many = 0;
+            for (const TileDev& td : p->ltiles) many += td.last - td.first >= 3;
+            const uint32_t pct = env_u32("II_LAYOUT_MIXED_PCT", 5, 0, 101);
+            p->layout_mixed = pct <= 100 && many * 100 >= (uint64_t)pct * p->ltiles.size();
         }
         p->na_rows.resize(S);
         p->na_ranges.reserve(n);
@@ -527,6 +537,8 @@ extern "C" int ii_plan_layout_tiles(const ii_plan_t* p, uint64_t* num_tiles, uin
     }
     return II_OK;
 }
+
+extern "C" int ii_plan_layout_mixed(const ii_plan_t* p) { return p && p->layout_mixed ? 1 : 0; }
 
 extern "C" int ii_plan_packing(const ii_plan_t* p, uint32_t* seg_off, uint64_t* chunk_len) {
     if (!p) return fail(II_EINVAL, "ii_plan_packing: plan is NULL");

@@ -55,7 +55,7 @@ hipError_t launch_scatter_slot(const uint8_t* slot, const TileDev* tiles, const 
                                uint32_t tile_bytes, uint64_t plen, hipStream_t stream);
 hipError_t launch_scatter_layout(const uint8_t* span, const TileDev* tiles, const uint32_t* win,
                                  uint64_t ntiles, const LayoutSeg* segs, uint32_t tile_bytes,
-                                 hipStream_t stream);
+                                 bool mixed, hipStream_t stream);
 hipError_t launch_zero(const RangeDev* ranges, uint32_t n, hipStream_t stream);
 
 #define II_HIP(call)                                                                   \
@@ -845,7 +845,7 @@ static int run_device(ii_plan_t* p, const uint8_t* image, const uint64_t* dst, h
     II_HIP(launch_injected() ? hipErrorLaunchFailure
                              : launch_scatter_layout(image + p->lo, r->d_ltiles, r->d_lwin,
                                                      p->ltiles.size(), r->d_lsegs, p->tile_bytes,
-                                                     stream));
+                                                     p->layout_mixed, stream));
     II_HIP(hipEventRecord(r->tables_idle, stream));
     r->tables_used = true;
     return II_OK;
@@ -940,7 +940,7 @@ static int run_device_noalloc(ii_plan_t* p, const uint8_t* image, const uint64_t
                      image + p->lo, reinterpret_cast<const TileDev*>(ws + l.tiles),
                      p->lwin.empty() ? nullptr : reinterpret_cast<const uint32_t*>(ws + l.win),
                      p->ltiles.size(), reinterpret_cast<const LayoutSeg*>(ws + l.rows),
-                     p->tile_bytes, stream));
+                     p->tile_bytes, p->layout_mixed, stream));
     return II_OK;
 }
 

@@ -86,6 +86,7 @@ _sig("ii_plan_chunks", _c.c_int, _vp, _vp, _vp, _vp)
 _sig("ii_plan_segments", _c.c_int, _vp, _vp, _vp, _vp, _vp, _vp)
 _sig("ii_plan_tiles", _c.c_int, _vp, _P(_u32), _P(_u64), _vp, _vp, _vp, _vp, _vp)
 _sig("ii_plan_layout_tiles", _c.c_int, _vp, _P(_u64), _vp, _vp, _vp, _vp)
+_sig("ii_plan_layout_mixed", _c.c_int, _vp)
 _sig("ii_plan_tensor_name", _c.c_char_p, _vp, _sz)
 _sig("ii_host_alloc", _c.c_int, _u64, _P(_vp))
 _sig("ii_host_free", _c.c_int, _vp)
@@ -289,6 +290,12 @@ class Plan:
                                          p(out["first"]), p(out["last"]), p(out["window"])),
                "ii_plan_layout_tiles")
         return out
+
+    @property
+    def layout_mixed(self) -> bool:
+        """Whether the image kernel runs its variant for many small tensors
+        (see ii_plan_layout_mixed)."""
+        return bool(_lib.ii_plan_layout_mixed(self.handle))
 
     def packing(self) -> dict:
         """Packed staging layout: seg_off (per segment), chunk_len (per chunk)."""

@@ -239,7 +239,9 @@ int emu_scatter(uint64_t num_chunks, uint64_t chunk_bytes, uint64_t lo, uint64_t
 }
 
 // Emulate the resident-image kernel (scatter_layout) over the plan's layout
-// tiles: tile g takes the layout positions [window[g] * tile_bytes, +
+// tiles. (Its single-segment path forms the one row in every lane and maps
+// lane unit u to unit u of that row: the arithmetic below with one row,
+// whose prefix is 0, so this emulation covers both paths.) Tile g takes the layout positions [window[g] * tile_bytes, +
 // tile_bytes) and the layout-order segments seg_order[first[g] ..
 // last[g]); segment x's bytes sit at emulated address src_base + chunk[x] *
 // chunk_bytes + chunk_off[x] and go to tensor_dst[tensor[x]] + tensor_off[x],

@@ -846,6 +846,29 @@ def test_many_segments_per_tile(orc):
         _load_arena(orc, t, mode=mode, plan=plan)
 
 
+@pytest.mark.parametrize("pct", ["0", "101"], ids=["mixed", "dense"])
+def test_image_kernel_both_variants(orc, monkeypatch, pct):
+    """Each variant of the image kernel, forced for every table (the one for
+    many small tensors: tiles of one segment without LDS staging, all loads
+    issued first; the other: one unit's loads in flight per lane), writes
+    every byte as the oracle does: headers, byte-aligned and padded
+    layouts, windows of padding only, tiles of hundreds of 1-32 byte
+    segments, shard rows at a stride, and 40 seeded random tables."""
+    monkeypatch.setenv("II_LAYOUT_MIXED_PCT", pct)
+    tables = [synth.tiny(header=1000), synth.tiny(dst_align=1),
+              synth.stress(n=20_000, header=5, dst_align=16),
+              random_tables.sparse_layout_table(),
+              synth.stress(n=50_000, lo_bytes=1, hi_bytes=32, chunk=1 << 20, dst_align=1),
+              synth.tiny_tp(1, 4)]
+    tables += [t for _, t, _, _ in random_tables.cases(7, 40)]
+    for t in tables:
+        plan = ii.ii_plan(t)
+        assert plan.layout_mixed == (pct == "0")
+        for mode in ("image", "image-pinned"):
+            _load_arena(orc, t, mode=mode, plan=plan, blob=getattr(t, "blob", None))
+        plan.free()
+
+
 @pytest.mark.slow
 def test_largest_chunk(orc):
     """chunk_bytes at its maximum, 2^32 - 16: chunk offsets and tile windows

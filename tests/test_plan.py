@@ -7,6 +7,7 @@ per-tile segment windows (an implementation detail of the kernel's work
 split) are checked against a brute-force intersection.
 """
 import itertools
+import os
 import random
 
 import numpy as np
@@ -141,6 +142,11 @@ def _check_layout_tiles(plan, s):
     assert (first < last).all()                  # every tile meets a segment
     assert np.array_equal(lt["first"].astype(np.int64), first)
     assert np.array_equal(lt["last"].astype(np.int64), last)
+    # the kernel variant: the one for many small tensors when at least
+    # II_LAYOUT_MIXED_PCT percent (default 5) of the tiles meet 3+ segments
+    pct = min(101, max(0, int(os.environ.get("II_LAYOUT_MIXED_PCT", "5"))))
+    many = int(((last - first) >= 3).sum())
+    assert plan.layout_mixed == (pct <= 100 and many * 100 >= pct * win.size)
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama8b", "mistral7b", "llama70b"])
@@ -157,6 +163,26 @@ def test_stress_set(orc):
     plan = _compare(orc, t)
     assert plan.num_chunks == 57
     assert plan.payload_bytes == t.blob_bytes  # packed from offset 0, no gaps
+
+
+def test_image_kernel_variant_by_table(monkeypatch):
+    """The image kernel's variant for many small tensors is chosen for the
+    100,000-tensor set (10% of its tiles meet three or more segments) and
+    not for tables of large tensors or a tensor-parallel shard (whose tiles
+    meet at most two); II_LAYOUT_MIXED_PCT forces either."""
+    want = {"stress": True, "tiny": False, "llama8b": False, "llama8b_tp": False}
+    make = {"stress": synth.stress, "tiny": synth.tiny, "llama8b": synth.llama8b,
+            "llama8b_tp": lambda: synth.llama8b_tp(1, 4)}
+    for name, m in make.items():
+        plan = ii.ii_plan(m())
+        assert plan.layout_mixed == want[name], name
+        plan.free()
+    for pct, mixed in (("0", True), ("101", False)):
+        monkeypatch.setenv("II_LAYOUT_MIXED_PCT", pct)
+        for m in (synth.tiny, synth.stress):
+            plan = ii.ii_plan(m())
+            assert plan.layout_mixed == mixed, pct
+            plan.free()
 
 
 def test_header_offset_and_alignment_variants(orc):
