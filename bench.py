@@ -20,8 +20,9 @@ Reported beside it:
   roofline      the scatter kernel alone: the same table scattered from a
                 blob image already resident in HBM (ii_load_device, one
                 dispatch), its algorithmic HBM bytes per launch over its mean
-                launch time (HIP events on the launch stream) against the
-                8 TB/s HBM peak; traffic from rocprofv3 counters when a profile
+                launch time (HIP events on the launch stream, the launches
+                queued behind a spin kernel so that host time between calls
+                is not counted) against the 8 TB/s HBM peak; traffic from rocprofv3 counters when a profile
                 of the current kernel source is on record; and the ring's own
                 per-chunk scatter (scatter_slot) from the timestamps of one
                 traced load;
@@ -116,6 +117,31 @@ def _h2d_peak_here(torch, dev, chunk_bytes: int) -> dict:
     best = max(results, key=results.get)
     del host, devbuf
     return {"GBps": results[best], "variant": best, "all": results}
+
+
+def timed_launches(torch, dev, stream, launch, reps: int) -> float:
+    """Mean device time (ms) of `launch()`, called `reps` times, each call
+    bracketed by timing events on `stream`. The stream is first held by a
+    spin kernel (about 5 ms) so that every call is enqueued behind it: the
+    events then time the device work alone, not the host's enqueue of the
+    next call (tens of microseconds for a table of 100,000 tensors, as much
+    as the kernel of a small table takes)."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    x, y = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    x.record(stream)
+    torch.cuda._sleep(1 << 20)
+    y.record(stream)
+    torch.cuda.synchronize(dev)
+    per_cycle = max(x.elapsed_time(y), 1e-3) / (1 << 20)  # ms
+    torch.cuda._sleep(int(min(5.0 / per_cycle, 1 << 40)))
+    for a, b in ev:
+        a.record(stream)
+        launch()
+        b.record(stream)
+    torch.cuda.synchronize(dev)
+    return statistics.mean(a.elapsed_time(b) for a, b in ev)
 
 
 def calibration_copy(torch, dev, nbytes: int = 4 << 30, reps: int = 3) -> dict:
@@ -325,14 +351,8 @@ def all_configs(torch, dev, ii, synth) -> dict:
     def kernel_ms(plan, image, dst, reps):
         for _ in range(3):
             ii.ii_load_device(plan, image, dst, stream)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(reps)]
-        for a, b in ev:
-            a.record(stream)
-            ii.ii_load_device(plan, image, dst, stream)
-            b.record(stream)
-        torch.cuda.synchronize(dev)
-        return statistics.mean(a.elapsed_time(b) for a, b in ev)
+        return timed_launches(torch, dev, stream,
+                              lambda: ii.ii_load_device(plan, image, dst, stream), reps)
 
     def e2e(plan, src, dst, reps, fn=None):
         fn = fn or ii.ii_load
@@ -537,11 +557,20 @@ def _trace_durations(path: str) -> dict:
     return acc
 
 
+def _is_image_kernel(name: str) -> bool:
+    """Whether a profiler's kernel name (before its argument list) is the
+    image kernel, in either variant: "void ii::scatter_layout<true>"."""
+    base = name[5:] if name.startswith("void ") else name
+    return base.split("<")[0] == "ii::" + KERNEL
+
+
 def _profile_csv(folder: str, suffix: str) -> str:
     """The benchmark process's CSV among those a profiled run wrote (the
     child process that measures the H2D peak writes files of its own): the
-    one that names this library's kernels."""
-    for path in sorted(glob.glob(os.path.join(folder, "**", f"*{suffix}"), recursive=True)):
+    newest one that names this library's kernels (a folder reused by a
+    later run keeps the earlier run's files)."""
+    paths = glob.glob(os.path.join(folder, "**", f"*{suffix}"), recursive=True)
+    for path in sorted(paths, key=os.path.getmtime, reverse=True):
         with open(path) as fh:
             if "ii::" in fh.read():
                 return path
@@ -572,7 +601,7 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
                      f"{float(r['MinNs']):>12.0f}{float(r['MaxNs']):>12.0f}"
                      f"{float(r['Percentage']):>8.2f}")
     durs = _trace_durations(_profile_csv(trace_dir, "kernel_trace.csv"))
-    img = [v for k, v in durs.items() if k[0] == "ii::" + KERNEL]
+    img = [v for k, v in durs.items() if _is_image_kernel(k[0])]
     full_grid = -(-cfg["chunk_bytes"] // 4096) * 128
     slot_full = durs.get(("ii::scatter_slot", full_grid), [])
     lines.append("")
@@ -625,7 +654,7 @@ def summarize(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
          f"calibration kernel        {cal[0]} (grid {cal[1]}), {fetch[cal][1]} dispatches",
          f"  FETCH_SIZE per dispatch {fetch[cal][0]:.1f} KiB  -> scale {f_scale:.4f}",
          f"  WRITE_SIZE per dispatch {write[cal][0]:.1f} KiB  -> scale {w_scale:.4f}"]
-    key = [k for k in fetch if k[0] == "ii::" + KERNEL]
+    key = [k for k in fetch if _is_image_kernel(k[0])]
     if key:
         k = key[0]
         fb, wb = fetch[k][0] * 1024 * f_scale, write[k][0] * 1024 * w_scale
@@ -816,15 +845,9 @@ def main() -> int:
         image = torch.from_numpy(blob).to(dev)
         for _ in range(2):
             ii.ii_load_device(plan, image, dst, stream)
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.kernel_reps)]
-        torch.cuda.synchronize(dev)
-        for a, b in ev:
-            a.record(stream)
-            ii.ii_load_device(plan, image, dst, stream)
-            b.record(stream)
-        torch.cuda.synchronize(dev)
-        kernel_ms = statistics.mean(a.elapsed_time(b) for a, b in ev)
+        kernel_ms = timed_launches(torch, dev, stream,
+                                   lambda: ii.ii_load_device(plan, image, dst, stream),
+                                   args.kernel_reps)
         del image
         torch.cuda.empty_cache()
         alg = 2 * payload + table_bytes(plan)
