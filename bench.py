@@ -59,10 +59,17 @@ def log(msg: str) -> None:
 
 
 def kernel_source_hash() -> str:
+    """Hash of the kernel sources' code: comments removed and whitespace
+    runs collapsed, so an edit of comments alone keeps recorded profiles
+    current (no string literal in them holds a comment marker)."""
+    import re
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, f)) as fh:
+            code = fh.read()
+        code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
+        code = re.sub(r"//[^\n]*", " ", code)
+        h.update(" ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 
@@ -717,7 +724,7 @@ def recorded_traffic(workload: str):
 
 def ring_kernel(trace: dict, plan) -> dict:
     """The ring's scatter (scatter_slot) from one traced load: per-chunk
-    duration between its start and end events on the scatter stream, full
+    duration between its start and end events on its lane, full
     chunks only, with the algorithmic bytes of a full chunk (read + write of
     its bytes, its segment rows and 8-byte tile ranges)."""
     ss, se = trace["scatter_start"], trace["scatter_end"]

@@ -1,10 +1,11 @@
-// Load pipeline: pinned staging ring, bulk host-to-device copies on
-// dedicated copy streams, per-chunk scatter on a dedicated scatter stream,
-// hipEvent edges between them, and the C-ABI entry points that drive it.
+// Load pipeline: pinned staging ring, bulk host-to-device copies and
+// per-chunk scatters on the ring's lanes (its own streams), hipEvent edges
+// between them, and the C-ABI entry points that drive it.
 //
 // The chunk lifecycle of InstantInfer's refined tensor materialisation
 // (arXiv 2607.18957, Sec. 4.2) maps onto the ring as follows; j counts the
-// chunks that hold at least one segment (the others are never touched).
+// chunks that hold at least one segment (the others are never touched), and
+// chunk j's copy and scatter both run on lane j mod L.
 //   InDisk -> InMem   host threads bring chunk j's bytes into pinned slot
 //                     j mod D: a copy of its used range, or a gather of only
 //                     its segments when it has gaps (pageable blob or file;
@@ -16,21 +17,24 @@
 //                     copy_done[slot].
 //   InMem  -> InGPU   one hipMemcpyAsync per chunk (or one per row group,
 //                     2-D for rows at a fixed stride) into device slot
-//                     j mod D on copy stream j mod 2 (1 with a single copy
-//                     stream:
-//                     copies back to back in chunk order, the paper's
-//                     (C_i,InGPU)->(C_i+1,InMem) edge), after
-//                     scatter_done[slot] (the device slot is free); records
-//                     copy_done[slot].
-//   InGPU  -> tensors the scatter stream waits for copy_done[slot] and runs
-//                     the scatter kernel over the chunk's tiles, moving its
-//                     tensor pieces from Alloc to Loaded; records
-//                     scatter_done[slot].
+//                     j mod D on the chunk's lane; with one lane the copies
+//                     run back to back in chunk order (the paper's
+//                     (C_i,InGPU)->(C_i+1,InMem) edge). The device slot is
+//                     free once the scatter that last read it is done: the
+//                     lane's own stream order, or scatter_done[slot] when
+//                     another lane ran that scatter. Records copy_done[slot].
+//   InGPU  -> tensors the scatter kernel over the chunk's tiles, next on the
+//                     same lane, moving its tensor pieces from Alloc to
+//                     Loaded; records scatter_done[slot].
 //   Destroyed         scatter_done[slot] releases the slot to chunk j + D.
-// The caller's stream gates the first write into destination memory (entry
-// event) and waits for the last scatter (done event), so the load is ordered
-// on it like any other stream work. Destinations are checked (aligned,
-// disjoint, reachable by the device) before anything is enqueued.
+// The caller's stream gates the first write into destination memory: lane
+// 0 waits for an entry event recorded on it before its first scatter (and
+// runs a switch's scrub), the other lanes wait for lane 0's `go` event; the
+// copies into the ring need no such wait. At the end lane 0 joins the other
+// lanes and the caller's stream waits for its done event, so the load is
+// ordered on that stream like any other stream work. Destinations are
+// checked (aligned, disjoint, reachable by the device) before anything is
+// enqueued.
 #include <hip/hip_runtime.h>
 
 #include <fcntl.h>

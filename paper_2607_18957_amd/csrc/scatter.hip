@@ -48,7 +48,9 @@
 // prefix sums in LDS. Consecutive lanes get consecutive units, so a large
 // segment is copied with fully coalesced 16-byte accesses, and many
 // segments smaller than a wavefront (64 lanes x 16 B = 1 KiB) are served by
-// one wavefront in the same pass.
+// one wavefront in the same pass. (The resident-image kernel's variant for
+// tables of many small tensors skips this staging for tiles that one
+// segment meets: every lane forms that one row itself.)
 //
 // Phase shift. The 16 source bytes of a destination block start at any
 // address a. The lane loads the aligned 16-byte words at a & ~15 and
