@@ -146,7 +146,7 @@ __device__ __forceinline__ void move_units(DevMem& mem, uint32_t base, uint32_t 
 #pragma unroll
         for (int j = 0; j < kUnroll; ++j) {
             const uint32_t u = base + (uint32_t)j * kBlock + threadIdx.x;
-            io[j].c0 = io[j].c1 = 0;
+            io[j].c0 = io[j].c1 = io[j].p = 0;  // every unit is shifted below
             x0[j] = x1[j] = U4{0, 0, 0, 0};
             if (u < total) {
                 io[j] = unit_io(row_at(u), u);
