@@ -39,7 +39,6 @@ What pins what (InstantInfer, arXiv 2607.18957):
 from __future__ import annotations
 
 import itertools
-import math
 import random
 
 import numpy as np
