@@ -443,8 +443,10 @@ int ii_plan_layout_tiles(const ii_plan_t* plan, uint64_t* num_tiles, uint32_t* s
  * meets take a path without LDS staging, and every tile issues all its
  * loads before using any), chosen when at least II_LAYOUT_MIXED_PCT percent
  * (default 5; 0 = always, 101 = never) of the tiles meet three or more
- * segments; 0 for the other (fewer loads in flight, faster on tables of
- * large tensors). Both write the same bytes. 0 for a NULL plan. */
+ * segments, or when at least 3% meet two or more and most payload bytes
+ * are phase-shifted (blob offset and layout position differ mod 16); 0 for
+ * the other (fewer loads in flight, faster on tables of large tensors).
+ * Both write the same bytes. 0 for a NULL plan. */
 int ii_plan_layout_mixed(const ii_plan_t* plan);
 /* name of row i as given to ii_plan ("" if none); valid while the plan lives */
 const char* ii_plan_tensor_name(const ii_plan_t* plan, size_t i);

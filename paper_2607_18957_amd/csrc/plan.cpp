@@ -417,16 +417,30 @@ extern "C" int ii_plan(const ii_tensor_desc* table, size_t n, uint64_t chunk_byt
             // holds segment bytes exactly when the last tile is window G - 1
             if (p->ltiles.empty() || p->lwin.back() == p->ltiles.size() - 1)
                 std::vector<uint32_t>().swap(p->lwin);
-            // the image kernel's variant for tables of many small tensors
+            // The image kernel's variant for tables of many small tensors
             // (ii_plan_layout_mixed): when at least II_LAYOUT_MIXED_PCT
-            // percent (default 5) of the tiles meet three or more segments
-            // (0 = always, 101 = never).
-            // The 100,000-tensor set has 10.4% such tiles; a tensor-parallel
-            // shard of rows of 15 KB, none; tables of large tensors, none.
-            uint64_t many = 0;
-            for (const TileDev& td : p->ltiles) many += td.last - td.first >= 3;
+            // percent (default 5; 0 = always, 101 = never) of the tiles meet
+            // three or more segments, or when at least 3% meet two or more
+            // and most payload bytes are phase-shifted (their blob offset
+            // and layout position differ mod 16, so each 16-byte block takes
+            // two loads). The 100,000-tensor set has 10.4% tiles of three or
+            // more; 20,000 byte-sized tensors of 16-256 KiB, 4.3% of two and
+            // shifted bytes; a tensor-parallel shard of 4-15 KB rows, aligned
+            // rows; tables of large tensors, none of either.
+            uint64_t many = 0, two = 0, shifted = 0, bytes = 0;
+            for (const TileDev& td : p->ltiles) {
+                many += td.last - td.first >= 3;
+                two += td.last - td.first >= 2;
+            }
+            for (size_t x = 0; x < S; ++x) {
+                const uint64_t src = p->lo + (uint64_t)p->seg_chunk[x] * C + p->seg_off[x];
+                bytes += p->seg_len[x];
+                if ((src - pos[x]) & 15) shifted += p->seg_len[x];
+            }
+            const uint64_t G = p->ltiles.size();
             const uint32_t pct = env_u32("II_LAYOUT_MIXED_PCT", 5, 0, 101);
-            p->layout_mixed = pct <= 100 && many * 100 >= (uint64_t)pct * p->ltiles.size();
+            p->layout_mixed = pct <= 100 && (many * 100 >= (uint64_t)pct * G ||
+                                             (two * 100 >= 3 * G && shifted * 2 >= bytes));
         }
         p->na_rows.resize(S);
         p->na_ranges.reserve(n);

@@ -143,10 +143,18 @@ def _check_layout_tiles(plan, s):
     assert np.array_equal(lt["first"].astype(np.int64), first)
     assert np.array_equal(lt["last"].astype(np.int64), last)
     # the kernel variant: the one for many small tensors when at least
-    # II_LAYOUT_MIXED_PCT percent (default 5) of the tiles meet 3+ segments
+    # II_LAYOUT_MIXED_PCT percent (default 5) of the tiles meet 3+ segments,
+    # or 3% meet 2+ and most payload bytes sit at a source offset that
+    # differs from their layout position mod 16
     pct = min(101, max(0, int(os.environ.get("II_LAYOUT_MIXED_PCT", "5"))))
     many = int(((last - first) >= 3).sum())
-    assert plan.layout_mixed == (pct <= 100 and many * 100 >= pct * win.size)
+    two = int(((last - first) >= 2).sum())
+    lo, _ = plan.span
+    src = lo + s["chunk"].astype(np.int64) * plan.chunk_bytes + s["chunk_off"].astype(np.int64)
+    shifted = int(ln[(src - pos) % 16 != 0].sum())
+    want = pct <= 100 and (many * 100 >= pct * win.size or
+                           (two * 100 >= 3 * win.size and 2 * shifted >= int(ln.sum())))
+    assert plan.layout_mixed == want
 
 
 @pytest.mark.parametrize("name", ["tiny", "llama8b", "mistral7b", "llama70b"])
@@ -168,11 +176,19 @@ def test_stress_set(orc):
 def test_image_kernel_variant_by_table(monkeypatch):
     """The image kernel's variant for many small tensors is chosen for the
     100,000-tensor set (10% of its tiles meet three or more segments) and
-    not for tables of large tensors or a tensor-parallel shard (whose tiles
-    meet at most two); II_LAYOUT_MIXED_PCT forces either."""
-    want = {"stress": True, "tiny": False, "llama8b": False, "llama8b_tp": False}
+    for byte-sized tensors of 16-256 KiB (4% of tiles meet two, most bytes
+    phase-shifted), not for tables of large tensors (aligned or behind an
+    odd header) or a tensor-parallel shard (aligned rows, at most two
+    segments a tile); II_LAYOUT_MIXED_PCT forces either."""
+    want = {"stress": True, "tiny": False, "llama8b": False, "llama8b_tp": False,
+            "mid": True, "header": False}
     make = {"stress": synth.stress, "tiny": synth.tiny, "llama8b": synth.llama8b,
-            "llama8b_tp": lambda: synth.llama8b_tp(1, 4)}
+            "llama8b_tp": lambda: synth.llama8b_tp(1, 4),
+            # 16-256 KiB tensors of any byte size: few tiles of two
+            # segments, most bytes phase-shifted
+            "mid": lambda: synth.stress(n=20_000, lo_bytes=16384, hi_bytes=262144),
+            # large tensors, every byte phase-shifted, no tile of two
+            "header": lambda: synth.tiny(header=1000)}
     for name, m in make.items():
         plan = ii.ii_plan(m())
         assert plan.layout_mixed == want[name], name
