@@ -1,6 +1,7 @@
 """Host-side pieces of bench.py that need no GPU: the refusal of more than
-one GPU, the algorithmic table bytes of a launch, and the per-dispatch
-counter means read from rocprofv3's CSV output."""
+one GPU, the algorithmic table bytes of a launch, the per-dispatch counter
+means read from rocprofv3's CSV output, the image kernel's names in it, and
+the kernel source hash that recorded profiles are matched by."""
 import os
 import subprocess
 import sys
@@ -84,3 +85,26 @@ def test_ring_kernel_from_trace():
     segs = np.diff(sb.astype(np.int64))[full].mean()
     assert abs(r["bytes_per_chunk"] - (2 * (1 << 20) + 16 * segs + 8 * 256)) < 1e-6
     assert abs(r["copy_us_per_chunk"] - 100.0) < 1e-2
+
+
+def test_image_kernel_names():
+    """Both variants of the image kernel, as a profiler names them, are the
+    image kernel; the ring's kernel is not."""
+    assert bench._is_image_kernel("void ii::scatter_layout<true>")
+    assert bench._is_image_kernel("void ii::scatter_layout<false>")
+    assert bench._is_image_kernel("ii::scatter_layout")
+    assert not bench._is_image_kernel("ii::scatter_slot")
+    assert not bench._is_image_kernel("void ii::scatter_layout_x<true>")
+
+
+def test_kernel_source_hash_ignores_comments(tmp_path, monkeypatch):
+    """Recorded profiles stay current across comment edits, not code edits."""
+    code = "int f(int x) { return x + 1; }\n"
+    (tmp_path / "a.hip").write_text("// a comment\n" + code + "/* block\n comment */\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "KERNEL_SOURCES", ["a.hip"])
+    h0 = bench.kernel_source_hash()
+    (tmp_path / "a.hip").write_text(code.replace("{ ", "{\n    ") + "// another\n")
+    assert bench.kernel_source_hash() == h0
+    (tmp_path / "a.hip").write_text(code.replace("+ 1", "+ 2"))
+    assert bench.kernel_source_hash() != h0
